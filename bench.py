@@ -1,0 +1,303 @@
+"""Benchmark of the LEAP GRPO hot path on one MI355X.
+
+One step = one pass of the whole hot path over one RL training step of the
+"mid" workload (16 prompts x G=16 rollouts, up to 2 turns of U[256,1024]
+generated tokens with masked environment-feedback rows between turns,
+vocabulary 151936, 8192-row microbatches):
+
+  leap_dcp_gate                    first-turn outcomes -> multi-turn gate
+  leap_rank_advantages             final outcomes -> tournament reward, advantage
+  leap_token_advantages            every row of the step -> token advantage, weight
+  leap_grpo_logprob_loss_fwd_bwd   per microbatch: log-softmax, surrogate, KL,
+                                   loss and bf16 dlogits
+
+Every input (all microbatches' bf16 logits included) is resident in HBM
+before the timed region; dlogits go to separate buffers, so every step sees
+the same inputs.  Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k4_grpo_rows_traffic.json")
+K4_SOURCE = os.path.join(ROOT, "paper_2608_01804_amd", "csrc", "grpo_loss.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def k4_source_hash() -> str:
+    return hashlib.sha256(open(K4_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def row_bytes(V: int, valid: bool) -> int:
+    """Algorithmic HBM bytes of one row of the fused kernel.
+    valid row : read 2V (logits) + 20 (token id, old, ref, adv, w)
+                write 2V (dlogits) + 8 (logp, weighted row loss)
+    masked row: read 8 (w, token id); write 2V (zero dlogits) + 8."""
+    return 4 * V + 28 if valid else 2 * V + 16
+
+
+def build_step(L, torch, dev, name, seed):
+    import workloads as wl
+    lat = wl.draw_latent(name)
+    cfg = lat.cfg
+    G, M, V, R = lat.G, lat.M, cfg["V"], cfg["rows_per_mb"]
+    tmin, tmax = L.leap_dcp_tau_from_pass_rate(G, 0, 1, 1, 3, 4, 1)  # 0 < pass rate < 3/4
+    ftp_d = torch.from_numpy(lat.first_turn_pass).to(dev)
+    gate_d = torch.empty(lat.n_groups, dtype=torch.uint8, device=dev)
+    nf_d = torch.empty(lat.n_groups, dtype=torch.int32, device=dev)
+    L.leap_dcp_gate(ftp_d, lat.n_groups, G, tmin, tmax, nf_d, gate_d)
+    ro = wl.realize(lat, gate_d.cpu().numpy())
+    mbs = wl.pack(ro, R)
+    n_mb = len(mbs)
+    rows = n_mb * R
+    tok_r = np.concatenate([m.tok_rollout for m in mbs])
+    tok_t = np.concatenate([m.tok_turn for m in mbs])
+    valid = tok_r >= 0
+    log(f"[bench] workload {name}: {ro.n_rollouts} rollouts, {n_mb} microbatches x {R} rows, "
+        f"{int(valid.sum())} generated tokens, V={V}; logits {rows * V * 2 / 1e9:.1f} GB")
+
+    s = {"lat": lat, "ro": ro, "mbs": mbs, "V": V, "R": R, "rows": rows, "n_mb": n_mb,
+         "G": G, "M": M, "tau": (tmin, tmax), "valid": valid, "gamma": cfg["gamma"]}
+    s["ftp"] = ftp_d
+    s["gate"] = gate_d
+    s["n_fail"] = nf_d
+    s["pass_turn"] = torch.from_numpy(ro.pass_turn).to(dev)
+    s["n_turns"] = torch.from_numpy(ro.n_turns).to(dev)
+    s["n_gen"] = torch.from_numpy(ro.n_tokens).to(dev)
+    s["tok_r"] = torch.from_numpy(tok_r).to(dev)
+    s["tok_t"] = torch.from_numpy(tok_t).to(dev)
+    n = ro.n_rollouts
+    s["reward"] = torch.empty(n, dtype=torch.float32, device=dev)
+    s["adv_roll"] = torch.empty(n, dtype=torch.float32, device=dev)
+    s["adv_tok"] = torch.empty(rows, dtype=torch.float32, device=dev)
+    s["w_tok"] = torch.empty(rows, dtype=torch.float32, device=dev)
+
+    # every microbatch's logits, resident; dlogits in separate buffers
+    t0 = time.time()
+    s["logits"] = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
+    s["dlogits"] = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
+    tok = torch.empty(rows, dtype=torch.int32, device=dev)
+    for i in range(n_mb):
+        sl = slice(i * R, (i + 1) * R)
+        wl.logits_device(seed + i, R, V, device=dev, out=s["logits"][sl])
+        tok[sl] = wl.sample_tokens_device(s["logits"][sl], V, seed + i)
+    s["tok"] = tok
+    torch.cuda.synchronize()
+    log(f"[bench] logits and sampled tokens ready in {time.time() - t0:.1f} s")
+
+    # current log-probs from the library's own forward pass (w = 1, A = 0),
+    # then old / reference = current + N(0, 0.05^2) / N(0, 0.1^2)
+    ones = torch.ones(R, dtype=torch.float32, device=dev)
+    zeros = torch.zeros(R, dtype=torch.float32, device=dev)
+    cur = torch.empty(rows, dtype=torch.float32, device=dev)
+    ws_bytes = L.leap_grpo_workspace_size(R, V)
+    s["ws"] = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    s["ws_bytes"] = ws_bytes
+    s["loss"] = torch.empty(n_mb, dtype=torch.float32, device=dev)
+    p0 = L.leap_grpo_params(0.2, 0.2, 0.0, L.LEAP_KL_K3, 1.0)
+    for i in range(n_mb):
+        sl = slice(i * R, (i + 1) * R)
+        L.leap_grpo_logprob_loss_fwd_bwd(s["logits"][sl], V, R, V, tok[sl], zeros, zeros, zeros,
+                                         ones, p0, cur[sl], None, s["loss"][i:i + 1],
+                                         s["dlogits"][sl], s["ws"], ws_bytes)
+    n_old, n_ref = wl.logp_noise(seed, rows)
+    s["old"] = cur + torch.from_numpy(n_old.astype(np.float32)).to(dev)
+    s["ref"] = cur + torch.from_numpy(n_ref.astype(np.float32)).to(dev)
+    s["err"] = torch.zeros(1, dtype=torch.int32, device=dev)
+    s["params"] = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+    torch.cuda.synchronize()
+    return s
+
+
+def run_step(L, s, events=None):
+    """The whole hot path over one step.  events: list of (start, end) CUDA
+    event pairs to record around each fused-kernel call, or None."""
+    import torch
+    G, M, R, V = s["G"], s["M"], s["R"], s["V"]
+    n = s["ro"].n_rollouts
+    L.leap_dcp_gate(s["ftp"], n // G, G, s["tau"][0], s["tau"][1], s["n_fail"], s["gate"])
+    L.leap_rank_advantages(s["pass_turn"], None, None, n // G, G, M, L.LEAP_KEY_TURN,
+                           L.LEAP_ADV_STD, 1e-6, None, None, None, s["reward"], s["adv_roll"],
+                           s["err"])
+    L.leap_token_advantages(s["adv_roll"], s["tok_r"], s["tok_t"], s["n_turns"], s["n_gen"], n,
+                            s["rows"], s["gamma"], L.LEAP_AGG_SEQ_MEAN_TOKEN_MEAN, float(n),
+                            s["adv_tok"], s["w_tok"], s["err"])
+    stream = torch.cuda.current_stream()
+    for i in range(s["n_mb"]):
+        sl = slice(i * R, (i + 1) * R)
+        if events is not None:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        L.leap_grpo_logprob_loss_fwd_bwd(s["logits"][sl], V, R, V, s["tok"][sl], s["old"][sl],
+                                         s["ref"][sl], s["adv_tok"][sl], s["w_tok"][sl],
+                                         s["params"], None, None, s["loss"][i:i + 1],
+                                         s["dlogits"][sl], s["ws"], s["ws_bytes"], s["err"])
+        if events is not None:
+            e1.record(stream)
+            events.append((e0, e1))
+
+
+def copy_probe(torch, dev):
+    """A plain device copy of known size (1 GiB each way), the reference the
+    HBM byte counters are scaled by."""
+    a = torch.empty(1 << 29, dtype=torch.int16, device=dev)
+    a.fill_(1)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+
+
+def cpu_baseline(s, seconds: float):
+    """The fp64 oracle (as it is) on the host cores over a bounded sample of
+    the same step: the tournament, gate and token advantages over the whole
+    step, then fused rows of microbatch 0 until `seconds` have passed."""
+    import torch
+
+    import oracle
+    ro, lat, V, R = s["ro"], s["lat"], s["V"], s["R"]
+    cores = oracle.get_threads()
+    t0 = time.perf_counter()
+    nf, gate = oracle.dcp_gate(lat.first_turn_pass, s["G"], *s["tau"])
+    rk = oracle.rank_tournament(ro.pass_turn, s["G"], s["M"], eps=float(np.float32(1e-6)))
+    tok_r = s["tok_r"].cpu().numpy()
+    tok_t = s["tok_t"].cpu().numpy()
+    adv, w, _ = oracle.token_advantages(rk["A"], tok_r, tok_t, ro.n_turns, ro.n_tokens,
+                                        s["gamma"], oracle.AGG_SEQ_MEAN_TOKEN_MEAN,
+                                        float(ro.n_rollouts))
+    t_small = time.perf_counter() - t0
+    valid_rows = np.flatnonzero(w[:R] != 0)
+    chunk = 4 * cores
+    done = 0
+    t_rows = 0.0  # oracle time only; device->host copies of the sample are excluded
+    while done < valid_rows.size and t_rows < seconds:
+        rows = valid_rows[done:done + chunk]
+        idx = torch.as_tensor(rows, device=s["logits"].device)
+        lg = s["logits"].index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)
+        tok = s["tok"][idx].cpu().numpy()
+        old = s["old"][idx].cpu().numpy()
+        ref = s["ref"][idx].cpu().numpy()
+        tc = time.perf_counter()
+        oracle.grpo_rows(lg, tok, old, ref, adv[rows], w[rows])
+        t_rows += time.perf_counter() - tc
+        done += rows.size
+    n_valid = int(s["valid"].sum())
+    # whole-step time at the measured per-row rate, plus the small steps
+    step_time = t_small + t_rows / max(done, 1) * n_valid
+    return {"value": n_valid / step_time, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s) and "
+                      f"the fused objective with dlogits on {done} generated-token rows of "
+                      f"microbatch 0 ({t_rows:.1f} s), scaled to the step's {n_valid} tokens"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mid", choices=["mid", "full"])
+    ap.add_argument("--seed", type=int, default=1002)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the LEAP hot path here is built and timed on a "
+              "single MI355X; run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_01804_amd import leap as L
+    L.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.workload == "full":
+        raise SystemExit("the full workload does not fit resident; bench runs 'mid'")
+
+    s = build_step(L, torch, dev, args.workload, args.seed)
+    copy_probe(torch, dev)
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        run_step(L, s)
+    torch.cuda.synchronize()
+    assert int(s["err"].item()) == 0, "data errors reported by the kernels"
+
+    events = []
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_step(L, s, events)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    V, R = s["V"], s["R"]
+    k4_ms = np.array([a.elapsed_time(b) for a, b in events])
+    per_mb_bytes = []
+    for m in s["mbs"]:
+        nv = m.n_valid
+        per_mb_bytes.append(nv * row_bytes(V, True) + (R - nv) * row_bytes(V, False))
+    bytes_per_launch = float(np.mean(per_mb_bytes))
+    k4_avg_s = float(k4_ms.mean()) / 1e3
+    achieved = bytes_per_launch / k4_avg_s
+    n_valid = int(s["valid"].sum())
+    value = n_valid * args.steps / elapsed
+    log(f"[bench] {elapsed / args.steps * 1e3:.3f} ms/step; fused call {k4_avg_s * 1e6:.1f} us avg "
+        f"over {len(k4_ms)} launches; {achieved / 1e9:.0f} GB/s algorithmic")
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        t = json.load(open(TRAFFIC_FILE))
+        if t.get("k4_source_sha256_16") == k4_source_hash() and t.get("workload") == args.workload:
+            traffic = t.get("bytes_per_launch")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
+        cpu = cpu_baseline(s, args.cpu_seconds)
+
+    out = {
+        "metric": "rollout tokens/sec for fused GRPO logprob+loss+dlogits; % of HBM roofline",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: 16 prompts x G=16, up to 2 turns, "
+                               f"U[256,1024] tokens/turn, V={V}, {s['n_mb']} microbatches x {R} rows",
+                   "generated_tokens_per_step": n_valid, "rows_per_step": s["rows"],
+                   "vocab": V, "microbatch_rows": R, "G": s["G"], "max_turns": s["M"]},
+        "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": traffic,
+                     "kernel": "grpo_rows_resident<1024,19> + loss_reduce (one fused call)",
+                     "avg_launch_us": k4_avg_s * 1e6, "bytes_per_launch": bytes_per_launch},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

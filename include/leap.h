@@ -1,0 +1,229 @@
+/*
+ * leap.h -- C ABI of libleap, the MI355X (gfx950) hot path of the GRPO
+ * training step of "LEAP: Lean Environment-Feedback via Adaptive Pruning for
+ * Code RL in GPU Kernel Generation" (arXiv 2608.01804).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every array pointer is a DEVICE pointer, allocated and owned by the
+ *    caller.  The library never allocates or frees memory and never
+ *    synchronises; each call enqueues its kernels on `stream` (0 = the null
+ *    stream) and returns.
+ *  - The returned leap_status reports what the host can check before
+ *    launching: argument values, pointer alignment, workspace size, and a
+ *    launch error from the HIP runtime (LEAP_ERR_HIP).  On any status other
+ *    than LEAP_OK nothing has been enqueued.
+ *  - Errors that depend on device data (a token id outside [0, V), a
+ *    pass_turn outside [0, M], a rollout index out of range, a row whose
+ *    logits are all -inf) add 1 per offending item to the optional device
+ *    counter *dev_err (nullable; the caller zeroes it and reads it after its
+ *    own synchronisation).  The offending item is treated as excluded from
+ *    the objective, as described per call.
+ *  - No exception crosses the ABI.  The library keeps no state between
+ *    calls, is reentrant, and gives bitwise identical results for identical
+ *    inputs and shapes.
+ *  - Row-major layouts; "group-major" means rollout i of group g is at
+ *    index g*G + i.
+ */
+#ifndef LEAP_H_
+#define LEAP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum leap_status {
+    LEAP_OK = 0,
+    LEAP_ERR_INVALID_ARG = 1, /* null required pointer, size or enum out of range */
+    LEAP_ERR_MISALIGNED = 2,  /* a pointer or leading dimension breaks the alignment rule */
+    LEAP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size() value */
+    LEAP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
+    LEAP_ERR_HIP = 5          /* the HIP runtime reported an error at launch */
+} leap_status;
+
+/* Ordering key of the tournament. */
+typedef enum leap_key_mode {
+    /* The paper's order (Sec. 3.2, Eq. 4): first pass on an earlier turn is
+     * strictly preferred; every failure ties at the bottom. */
+    LEAP_KEY_TURN = 0,
+    /* Extension, not in the paper: tier first, then the larger quantised
+     * speedup, then the smaller generated-token count; equal tuples tie. */
+    LEAP_KEY_LEX = 1
+} leap_key_mode;
+
+/* Advantage from the tournament reward ("standard GRPO formulation",
+ * end of Sec. 3.2). */
+typedef enum leap_adv_norm {
+    LEAP_ADV_STD = 0,  /* A_i = (R_i - mean_g R) / (std_g R + eps), unbiased std */
+    LEAP_ADV_NONE = 1  /* A_i = R_i */
+} leap_adv_norm;
+
+/* Aggregation weight of a token in the loss (Sec. 4.1, sample-level loss;
+ * Eq. 3's 1/G sum over samples). */
+typedef enum leap_loss_agg {
+    LEAP_AGG_SEQ_MEAN_TOKEN_MEAN = 0, /* w = 1 / (denominator * |M_i|), denominator = sequences in the step */
+    LEAP_AGG_TOKEN_MEAN = 1,          /* w = 1 / denominator, denominator = generated tokens in the step */
+    LEAP_AGG_SUM = 2                  /* w = 1 */
+} leap_loss_agg;
+
+/* Estimator of the reference-KL term of Eq. 3. */
+typedef enum leap_kl_type {
+    LEAP_KL_K3 = 0, /* exp(r - lp) - (r - lp) - 1 (GRPO's estimator) */
+    LEAP_KL_K1 = 1, /* lp - r */
+    LEAP_KL_K2 = 2  /* (lp - r)^2 / 2 */
+} leap_kl_type;
+
+/* Hyper-parameters of the per-token objective (host struct, read at call). */
+typedef struct leap_grpo_params {
+    float clip_eps_low;    /* >= 0; ratio clipped below at 1 - clip_eps_low */
+    float clip_eps_high;   /* >= 0; ratio clipped above at 1 + clip_eps_high */
+    float kl_coef;         /* beta of Eq. 3, >= 0 */
+    int32_t kl_type;       /* leap_kl_type */
+    float inv_temperature; /* > 0; logits are multiplied by it before the softmax */
+} leap_grpo_params;
+
+/* Human-readable name of a status code (static string). */
+const char *leap_status_string(leap_status s);
+
+/* Library version, e.g. "0.1.0" (static string). */
+const char *leap_version(void);
+
+/*
+ * Rank-based reward and advantage (Sec. 3.2, Eqs. 4-6).
+ *
+ * For every group of G rollouts: the tier r_i = 0 if pass_turn[i] == 0
+ * (never passed), else M - pass_turn[i] + 1 (Eq. 4); the tournament counts
+ * n_worse_i = #{j != i : key_i > key_j}, n_better_i = #{j != i : key_i <
+ * key_j} (Eq. 5); the reward R_i = (n_worse_i - n_better_i) / (G - 1)
+ * (Eq. 6), computed in double precision and rounded once to float; and the
+ * advantage A_i per `norm` (eps is the std guard; 1e-6 is conventional).
+ *
+ * pass_turn  int32 [n_groups*G], group-major; 0 or 1..M.  An entry outside
+ *            0..M counts in *dev_err and ranks as a failure (r = 0).
+ * speedup_q  int32 [n_groups*G], LEX mode only (NULL otherwise).
+ * n_tokens   int32 [n_groups*G], LEX mode only (NULL otherwise).
+ * n_groups   >= 0;  G in 2..1024;  M >= 1.
+ * n_worse, n_better, rank_r   int32 [n_groups*G], each nullable.
+ * reward, advantage           float [n_groups*G], required.
+ * Errors: LEAP_ERR_INVALID_ARG for G < 2 or > 1024, M < 1, n_groups < 0,
+ * eps < 0 or not finite, an unknown key/norm, a required pointer NULL.
+ */
+leap_status leap_rank_advantages(const int32_t *pass_turn, const int32_t *speedup_q,
+                                 const int32_t *n_tokens, int64_t n_groups, int32_t G,
+                                 int32_t M, int32_t key, int32_t norm, float eps,
+                                 int32_t *n_worse, int32_t *n_better, int32_t *rank_r,
+                                 float *reward, float *advantage, int32_t *dev_err,
+                                 hipStream_t stream);
+
+/*
+ * Difficulty-Conditioned Pruning gate (Sec. 3.1, Eqs. 1-2).
+ *
+ * n_fail[g] = number of rollouts of group g whose first-turn response
+ * failed verification (first_turn_pass == 0; any nonzero byte is a pass);
+ * gate[g] = 1 iff tau_min <= n_fail[g] <= tau_max (inclusive), else 0.
+ *
+ * first_turn_pass  uint8 [n_groups*G], group-major.
+ * n_fail           int32 [n_groups], nullable.   gate  uint8 [n_groups].
+ * Errors: LEAP_ERR_INVALID_ARG for G < 1 or > 1024, n_groups < 0,
+ * tau_min > tau_max, tau_min < 0, tau_max > G, a required pointer NULL.
+ */
+leap_status leap_dcp_gate(const uint8_t *first_turn_pass, int64_t n_groups, int32_t G,
+                          int32_t tau_min, int32_t tau_max, int32_t *n_fail,
+                          uint8_t *gate, hipStream_t stream);
+
+/*
+ * Host helper (no device work): the inclusive integer bounds [tau_min,
+ * tau_max] on N_fail that select exactly the groups whose first-turn pass
+ * rate (G - N_fail)/G lies in the interval from lo_num/lo_den to
+ * hi_num/hi_den, each end open (strict = 1) or closed (strict = 0).  The
+ * conversion is exact rational arithmetic (Sec. 3.1 phrases the thresholds
+ * as pass rates in its pruning study; Eq. 2 takes failure counts).
+ * Errors: LEAP_ERR_INVALID_ARG for G < 1, a denominator <= 0, NULL outputs,
+ * or an interval that admits no N_fail in 0..G.
+ */
+leap_status leap_dcp_tau_from_pass_rate(int32_t G, int32_t lo_num, int32_t lo_den,
+                                        int32_t lo_strict, int32_t hi_num, int32_t hi_den,
+                                        int32_t hi_strict, int32_t *tau_min,
+                                        int32_t *tau_max);
+
+/*
+ * Discounted per-turn token advantage (Sec. 3.3) and aggregation weight.
+ *
+ * Token k belongs to rollout i = tok_rollout[k] (-1: excluded -- padding,
+ * prompt or environment feedback) and generated turn t = tok_turn[k] of its
+ * T_i = n_turns[i] turns.  beta_i = gamma if A_i >= 0 else 1;
+ * adv_tok[k] = beta_i^(T_i - t - 1) * A_i.  w_tok[k] per `agg` with
+ * |M_i| = n_gen_tokens[i] (generated tokens of rollout i over all its
+ * turns).  Excluded tokens get adv = 0 and w = 0.  Computed in double and
+ * rounded once to float.
+ *
+ * advantage     float [n_rollouts]     tok_rollout, tok_turn  int32 [N]
+ * n_turns, n_gen_tokens  int32 [n_rollouts]
+ * adv_tok, w_tok         float [N]
+ * gamma in (0, 1];  denominator > 0 (ignored for LEAP_AGG_SUM).
+ * A token with tok_rollout < -1 or >= n_rollouts, a turn outside 0..T_i-1,
+ * or a rollout with T_i < 1 or n_gen_tokens < 1 counts in *dev_err and is
+ * excluded.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, n_rollouts < 0, gamma or
+ * denominator out of range, an unknown agg, a required pointer NULL.
+ */
+leap_status leap_token_advantages(const float *advantage, const int32_t *tok_rollout,
+                                  const int32_t *tok_turn, const int32_t *n_turns,
+                                  const int32_t *n_gen_tokens, int32_t n_rollouts, int64_t N,
+                                  float gamma, int32_t agg, double denominator,
+                                  float *adv_tok, float *w_tok, int32_t *dev_err,
+                                  hipStream_t stream);
+
+/* Workspace bytes leap_grpo_logprob_loss_fwd_bwd needs for N rows. */
+size_t leap_grpo_workspace_size(int64_t N, int32_t V);
+
+/*
+ * Fused per-token GRPO objective and its logits gradient over one
+ * microbatch of N rows (Sec. 3.1, Eq. 3, per token; surrogate read as
+ * PPO-clip, KL per params->kl_type).
+ *
+ * For each row k with w_tok[k] != 0, with z = inv_temperature * logits[k]:
+ *   logp_k  = z[y_k] - log sum_v exp(z[v])                (y_k = token_ids[k])
+ *   rho_k   = exp(logp_k - old_logp[k])
+ *   surr_k  = min(rho_k * A_k, clip(rho_k, 1 - eps_lo, 1 + eps_hi) * A_k)
+ *   loss_k  = -surr_k + kl_coef * KL(logp_k, ref_logp[k])
+ *   g_k     = w_k * d loss_k / d logp_k * inv_temperature
+ *   dlogits[k][v] = g_k * ([v == y_k] - softmax(z)[v])      (bf16, RNE)
+ * where A_k = adv_tok[k] and w_k = w_tok[k].  The ratio's gradient flows
+ * when A_k > 0 and rho_k <= 1 + eps_hi, or A_k < 0 and rho_k >= 1 - eps_lo.
+ * A row with w_tok[k] == 0 is excluded: its logits are not read, its
+ * dlogits row is written as zeros, logp_out and tok_loss_out get 0.
+ * A row with w != 0 but a token id outside [0, V), or all logits -inf,
+ * counts in *dev_err and is excluded the same way.
+ *
+ * logits_bf16  [N][ld] bf16 (row k at element k*ld; V columns used).
+ * dlogits_bf16 [N][ld] bf16, written in columns 0..V-1; may equal
+ *              logits_bf16 (in place), must not otherwise overlap it.
+ * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
+ * logp_out, tok_loss_out  float [N], nullable (tok_loss is unweighted loss_k).
+ * loss_out   float [1], required: sum_k w_k * loss_k, summed in a fixed order.
+ * workspace  device buffer of >= leap_grpo_workspace_size(N, V) bytes.
+ * Alignment: logits and dlogits 16-byte aligned, ld % 8 == 0, ld >= V.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a parameter out of
+ * range, a required pointer NULL; LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE;
+ * LEAP_ERR_UNSUPPORTED for an unknown kl_type.
+ */
+leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, int64_t N,
+                                           int32_t V, const int32_t *token_ids,
+                                           const float *old_logp, const float *ref_logp,
+                                           const float *adv_tok, const float *w_tok,
+                                           const leap_grpo_params *params, float *logp_out,
+                                           float *tok_loss_out, float *loss_out,
+                                           void *dlogits_bf16, void *workspace,
+                                           size_t ws_bytes, int32_t *dev_err,
+                                           hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LEAP_H_ */

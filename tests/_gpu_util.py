@@ -1,0 +1,175 @@
+"""Helpers of the GPU parity tests: run each libleap entry point on seeded
+inputs and return numpy results.  Inputs come from ``workloads``; expected
+values come from ``oracle`` only."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+import workloads as wl
+
+EPS_ADV = float(np.float32(1e-6))
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev():
+    import torch
+    return torch.device("cuda:0")
+
+
+def T(a, dtype=None):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(dev())
+
+
+def zeros_i32(n):
+    import torch
+    return torch.zeros(max(1, n), dtype=torch.int32, device=dev())
+
+
+def run_rank(pass_turn, G, M, key=0, norm=0, speedup_q=None, n_tokens=None, eps=EPS_ADV):
+    import torch
+    from paper_2608_01804_amd import leap as L
+    pt = np.ascontiguousarray(pass_turn, np.int32).reshape(-1)
+    n = pt.size
+    n_groups = n // G
+    nw = torch.full((n,), -7, dtype=torch.int32, device=dev())
+    nb = torch.full((n,), -7, dtype=torch.int32, device=dev())
+    rr = torch.full((n,), -7, dtype=torch.int32, device=dev())
+    R = torch.full((n,), float("nan"), dtype=torch.float32, device=dev())
+    A = torch.full((n,), float("nan"), dtype=torch.float32, device=dev())
+    err = zeros_i32(1)
+    L.leap_rank_advantages(T(pt), None if speedup_q is None else T(np.asarray(speedup_q, np.int32)),
+                           None if n_tokens is None else T(np.asarray(n_tokens, np.int32)),
+                           n_groups, G, M, key, norm, eps, nw, nb, rr, R, A, err)
+    torch.cuda.synchronize()
+    return {"n_worse": nw.cpu().numpy(), "n_better": nb.cpu().numpy(), "r": rr.cpu().numpy(),
+            "R": R.cpu().numpy(), "A": A.cpu().numpy(), "bad": int(err.item())}
+
+
+def check_rank(gpu, ora):
+    assert np.array_equal(gpu["n_worse"], ora["n_worse"])
+    assert np.array_equal(gpu["n_better"], ora["n_better"])
+    assert np.array_equal(gpu["r"], ora["r"])
+    assert np.array_equal(gpu["R"], ora["R"].astype(np.float32)), "R not bit-exact"
+    tol = 1e-6 * np.maximum(1.0, np.abs(ora["A"]))
+    assert np.all(np.abs(gpu["A"].astype(np.float64) - ora["A"]) <= tol)
+    assert gpu["bad"] == ora["bad"]
+
+
+def run_gate(first_turn_pass, G, tmin, tmax):
+    import torch
+    from paper_2608_01804_amd import leap as L
+    ftp = np.ascontiguousarray(first_turn_pass, np.uint8).reshape(-1)
+    n_groups = ftp.size // G
+    nf = torch.full((max(1, n_groups),), -1, dtype=torch.int32, device=dev())
+    gate = torch.full((max(1, n_groups),), 7, dtype=torch.uint8, device=dev())
+    L.leap_dcp_gate(T(ftp), n_groups, G, tmin, tmax, nf, gate)
+    torch.cuda.synchronize()
+    return nf.cpu().numpy()[:n_groups], gate.cpu().numpy()[:n_groups]
+
+
+def run_token_adv(A32, tok_r, tok_t, n_turns, n_gen, gamma, agg, denom):
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N = len(tok_r)
+    adv = torch.full((N,), float("nan"), dtype=torch.float32, device=dev())
+    w = torch.full((N,), float("nan"), dtype=torch.float32, device=dev())
+    err = zeros_i32(1)
+    L.leap_token_advantages(T(np.asarray(A32, np.float32)), T(np.asarray(tok_r, np.int32)),
+                            T(np.asarray(tok_t, np.int32)), T(np.asarray(n_turns, np.int32)),
+                            T(np.asarray(n_gen, np.int32)), len(A32), N, gamma, agg, denom, adv,
+                            w, err)
+    torch.cuda.synchronize()
+    return adv.cpu().numpy(), w.cpu().numpy(), int(err.item())
+
+
+def bf16_device(lg_u16):
+    import torch
+    return T(lg_u16.view(np.int16)).view(torch.bfloat16)
+
+
+def run_grpo(lg_dev, V, tok, old, ref, adv, w, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0,
+             inv_temp=1.0, inplace=False, want_tok_loss=True):
+    """lg_dev: bf16 device tensor [N, ld].  Returns numpy logp, tok_loss, loss,
+    dlogits (bf16 bits as uint16 [N, ld], device copy kept as 'dl_dev'), bad."""
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N, ld = lg_dev.shape
+    dl = lg_dev if inplace else torch.full_like(lg_dev, float("nan"))
+    lp = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+    tl = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+    loss = torch.full((1,), float("nan"), dtype=torch.float32, device=dev())
+    ws_bytes = L.leap_grpo_workspace_size(N, V)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev())
+    err = zeros_i32(1)
+    p = L.leap_grpo_params(eps_lo, eps_hi, kl_coef, kl_type, inv_temp)
+    L.leap_grpo_logprob_loss_fwd_bwd(lg_dev, ld, N, V, T(np.asarray(tok, np.int32)),
+                                     T(np.asarray(old, np.float32)), T(np.asarray(ref, np.float32)),
+                                     T(np.asarray(adv, np.float32)), T(np.asarray(w, np.float32)),
+                                     p, lp, tl if want_tok_loss else None, loss, dl, ws, ws_bytes,
+                                     err)
+    torch.cuda.synchronize()
+    return {"logp": lp.cpu().numpy()[:N], "tok_loss": tl.cpu().numpy()[:N],
+            "loss": float(loss.item()), "dl_dev": dl, "bad": int(err.item())}
+
+
+def dl_rows(dl_dev, rows, V):
+    """fp32 copy of the selected dlogits rows [len(rows), V]."""
+    import torch
+    idx = torch.as_tensor(np.asarray(rows, np.int64), device=dl_dev.device)
+    return dl_dev.index_select(0, idx)[:, :V].float().cpu().numpy().astype(np.float64)
+
+
+def boundary_rows(logp_o, old, eps_lo, eps_hi, A, rel=1e-4):
+    """Rows whose ratio sits within `rel` of a clip boundary: a rounding-level
+    difference may legitimately put the GPU on the other side there."""
+    rho = np.exp(logp_o - np.asarray(old, np.float64))
+    near = (np.abs(rho - (1 + eps_hi)) < rel * (1 + eps_hi)) | \
+           (np.abs(rho - (1 - eps_lo)) < rel * max(1e-30, 1 - eps_lo))
+    return near & (np.asarray(A) != 0)
+
+
+def check_dlogits(gpu_rows, lg_u16, rows, tok, old, ref, adv, w, V, atol, kw, rel_to_max=False):
+    """Compare GPU dlogits rows with the oracle; rows at a clip boundary may
+    match either one-sided gradient."""
+    o = oracle.grpo_rows(lg_u16, tok, old, ref, adv, w, V=V, rows=rows, **kw)
+    ref_d = o["dlogits"]
+    scale = np.max(np.abs(ref_d)) if rel_to_max else 1.0
+    lim = atol * scale
+    sel = np.asarray(rows)
+    near = boundary_rows(o["logp"], np.asarray(old, np.float64)[sel], kw.get("eps_lo", 0.2),
+                         kw.get("eps_hi", 0.2), np.asarray(adv)[sel])
+    for j in range(len(sel)):
+        err = np.max(np.abs(gpu_rows[j] - ref_d[j])) if V else 0.0
+        if err <= lim:
+            continue
+        assert near[j], f"row {sel[j]}: max |d dlogits| = {err:.3e} > {lim:.3e}"
+        ok = False
+        for shift in (2e-4, -2e-4):
+            old2 = np.asarray(old, np.float64).copy()
+            old2[sel[j]] += shift
+            o2 = oracle.grpo_rows(lg_u16, tok, old2, ref, adv, w, V=V, rows=[sel[j]], **kw)
+            if np.max(np.abs(gpu_rows[j] - o2["dlogits"][0])) <= lim:
+                ok = True
+        assert ok, f"boundary row {sel[j]} matches neither one-sided gradient"
+    return o
+
+
+def make_inputs_host(seed, N, V, ld=None, old_sigma=wl.OLD_SIGMA):
+    """Host-generated bf16 logits and the derived token ids and log-probs."""
+    lg = wl.logits_host(seed, N, V, ld)
+    tok = wl.sample_tokens_host(lg, V, seed)
+    cur, bad = oracle.logprob_rows(lg, tok, V=V)
+    assert bad == 0
+    n_old, n_ref = wl.logp_noise(seed, N, old_sigma=old_sigma)
+    return lg, tok, (cur + n_old).astype(np.float32), (cur + n_ref).astype(np.float32)

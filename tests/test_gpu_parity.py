@@ -1,0 +1,347 @@
+"""GPU parity: every libleap entry point against the fp64 oracle on the same
+seeded inputs (integers bit-exact; R bit-exact as float32; A within 1e-6
+relative; token advantages within float32 rounding; log-probs within 2e-3
+absolute, loss within 1e-3 relative, dlogits within 2e-2 absolute).
+
+Small shapes get full element-by-element parity; the full microbatch shapes
+(8192 and 16384 rows of a 151936 vocabulary), in the same launch
+configuration the benchmark times, get every log-prob, the loss, and sampled
+dlogits rows."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests import _gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+KW = dict(eps_lo=0.2, eps_hi=0.2, kl_coef=0.01)
+
+
+def _default_tau(G):
+    return oracle.tau_from_pass_rate(G, Fraction(0), True, Fraction(3, 4), True)
+
+
+def _step(name):
+    lat = wl.draw_latent(name)
+    tmin, tmax = _default_tau(lat.G)
+    _, gate = oracle.dcp_gate(lat.first_turn_pass, lat.G, tmin, tmax)
+    ro = wl.realize(lat, gate)
+    return lat, ro
+
+
+# ----------------------------------------------------------------------------
+# DCP gate
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "mid", "full", "stress"])
+def test_gate_parity(name):
+    lat = wl.draw_latent(name)
+    G = lat.G
+    windows = [_default_tau(G), (0, G), (G // 2, G), (0, G // 2), (G, G), (0, 0)]
+    for tmin, tmax in windows:
+        U.log(f"gate {name} G={G} tau=[{tmin},{tmax}]")
+        nf_o, g_o = oracle.dcp_gate(lat.first_turn_pass, G, tmin, tmax)
+        nf_g, g_g = U.run_gate(lat.first_turn_pass, G, tmin, tmax)
+        assert np.array_equal(nf_g, nf_o) and np.array_equal(g_g, g_o)
+
+
+@pytest.mark.parametrize("G", [1, 3, 64, 65, 200, 1024])
+def test_gate_sizes(G):
+    rng = np.random.default_rng(G)
+    n_groups = 37
+    ftp = (rng.random((n_groups, G)) < 0.4).astype(np.uint8) * rng.integers(1, 256, (n_groups, G))
+    tmin, tmax = G // 4, G - G // 5
+    U.log(f"gate G={G}")
+    nf_o, g_o = oracle.dcp_gate(ftp.astype(np.uint8), G, tmin, tmax)
+    nf_g, g_g = U.run_gate(ftp.astype(np.uint8), G, tmin, tmax)
+    assert np.array_equal(nf_g, nf_o) and np.array_equal(g_g, g_o)
+
+
+# ----------------------------------------------------------------------------
+# Rank advantages
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("name,key", [("tiny", 0), ("mid", 0), ("full", 0), ("stress", 0),
+                                      ("stress", 1), ("full", 1)])
+def test_rank_parity(name, key):
+    lat, ro = _step(name)
+    nt = wl.stress_token_counts(lat) if name == "stress" else ro.n_tokens
+    U.log(f"rank {name} key={key} rollouts={ro.n_rollouts}")
+    ora = oracle.rank_tournament(ro.pass_turn, ro.G, ro.M, key_mode=key, eps=U.EPS_ADV,
+                                 speedup_q=ro.speedup_q, n_tokens=nt)
+    gpu = U.run_rank(ro.pass_turn, ro.G, ro.M, key=key, speedup_q=ro.speedup_q if key else None,
+                     n_tokens=nt if key else None)
+    U.check_rank(gpu, ora)
+
+
+@pytest.mark.parametrize("G", [2, 3, 63, 64, 65, 128, 200, 256, 1000, 1024])
+@pytest.mark.parametrize("key", [0, 1])
+def test_rank_group_sizes(G, key):
+    rng = np.random.default_rng(1000 + G)
+    n_groups, M = 29, 3
+    pt = rng.integers(0, M + 1, size=n_groups * G).astype(np.int32)
+    sq = np.where(pt > 0, rng.integers(0, 5, pt.size), 0).astype(np.int32)
+    nt = rng.integers(1, 6, pt.size).astype(np.int32)
+    U.log(f"rank G={G} key={key}")
+    ora = oracle.rank_tournament(pt, G, M, key_mode=key, eps=U.EPS_ADV, speedup_q=sq, n_tokens=nt)
+    gpu = U.run_rank(pt, G, M, key=key, speedup_q=sq if key else None, n_tokens=nt if key else None)
+    U.check_rank(gpu, ora)
+
+
+def test_rank_invalid_and_adv_none():
+    pt = np.array([1, 4, -1, 0, 2, 2, 0, 1], np.int32)
+    ora = oracle.rank_tournament(pt, 4, 2, adv_norm=oracle.ADV_NONE)
+    gpu = U.run_rank(pt, 4, 2, norm=1)
+    U.check_rank(gpu, ora)
+    assert gpu["bad"] == 2
+    assert np.array_equal(gpu["A"], gpu["R"])
+
+
+def test_rank_all_equal_gives_zero():
+    pt = np.ones(64 * 8, np.int32)
+    gpu = U.run_rank(pt, 64, 2)
+    assert np.all(gpu["R"] == 0) and np.all(gpu["A"] == 0)
+
+
+# ----------------------------------------------------------------------------
+# Token advantages
+# ----------------------------------------------------------------------------
+def _step_tokens(name):
+    lat, ro = _step(name)
+    mbs = wl.pack(ro, lat.cfg["rows_per_mb"])
+    tok_r = np.concatenate([m.tok_rollout for m in mbs])
+    tok_t = np.concatenate([m.tok_turn for m in mbs])
+    ora = oracle.rank_tournament(ro.pass_turn, ro.G, ro.M, eps=U.EPS_ADV)
+    return lat, ro, mbs, tok_r, tok_t, ora["A"].astype(np.float32)
+
+
+def _denom(agg, ro):
+    if agg == oracle.AGG_SEQ_MEAN_TOKEN_MEAN:
+        return float(ro.n_rollouts)
+    if agg == oracle.AGG_TOKEN_MEAN:
+        return float(ro.n_tokens.sum())
+    return 1.0
+
+
+@pytest.mark.parametrize("name", ["tiny", "mid", "full"])
+@pytest.mark.parametrize("agg", [0, 1, 2])
+def test_token_adv_parity(name, agg):
+    lat, ro, mbs, tok_r, tok_t, A32 = _step_tokens(name)
+    gamma = float(np.float32(lat.cfg["gamma"]))
+    U.log(f"token_adv {name} agg={agg} N={tok_r.size}")
+    adv_o, w_o, bad_o = oracle.token_advantages(A32.astype(np.float64), tok_r, tok_t, ro.n_turns,
+                                                ro.n_tokens, gamma, agg, _denom(agg, ro))
+    adv_g, w_g, bad_g = U.run_token_adv(A32, tok_r, tok_t, ro.n_turns, ro.n_tokens, gamma, agg,
+                                        _denom(agg, ro))
+    assert bad_o == 0 and bad_g == 0
+    ulp = 2.0 ** -23
+    assert np.all(np.abs(adv_g - adv_o) <= ulp * np.abs(adv_o))
+    assert np.all(np.abs(w_g - w_o) <= ulp * np.abs(w_o))
+    assert np.all((tok_r < 0) <= (w_g == 0))
+
+
+def test_token_adv_invalid_rows_count():
+    A = np.array([0.5, -1.0], np.float32)
+    tok_r = np.array([0, 1, 2, -2, 1, -1], np.int32)
+    tok_t = np.array([0, 1, 0, 0, 5, 0], np.int32)
+    n_turns = np.array([1, 2], np.int32)
+    n_gen = np.array([1, 2], np.int32)
+    adv_o, w_o, bad_o = oracle.token_advantages(A.astype(np.float64), tok_r, tok_t, n_turns, n_gen,
+                                                0.5, oracle.AGG_SUM, 1.0)
+    adv_g, w_g, bad_g = U.run_token_adv(A, tok_r, tok_t, n_turns, n_gen, 0.5, oracle.AGG_SUM, 1.0)
+    assert bad_o == bad_g == 3
+    assert np.array_equal(adv_g, adv_o.astype(np.float32)) and np.array_equal(w_g, w_o)
+
+
+# ----------------------------------------------------------------------------
+# Fused log-softmax + surrogate + KL + dlogits
+# ----------------------------------------------------------------------------
+def _check_rows(gpu, o, valid, what=""):
+    assert np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0) < 2e-3, what
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
+
+
+def _tiny_weights(agg):
+    lat, ro, mbs, tok_r, tok_t, A32 = _step_tokens("tiny")
+    adv, w, _ = oracle.token_advantages(A32.astype(np.float64), tok_r, tok_t, ro.n_turns,
+                                        ro.n_tokens, 1.0, agg, _denom(agg, ro))
+    return adv.astype(np.float32), w.astype(np.float32)
+
+
+@pytest.mark.parametrize("mode", ["sum", "seq_mean", "clip"])
+def test_grpo_tiny_full_parity(mode):
+    N, V = 2048, 32768
+    old_sigma = wl.CLIP_CASE_OLD_SIGMA if mode == "clip" else wl.OLD_SIGMA
+    lg, tok, old, ref = U.make_inputs_host(1001, N, V, old_sigma=old_sigma)
+    adv, w = _tiny_weights(oracle.AGG_SEQ_MEAN_TOKEN_MEAN if mode == "seq_mean" else oracle.AGG_SUM)
+    U.log(f"grpo tiny {mode}")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
+    valid = w != 0
+    _check_rows(gpu, o, valid, mode)
+    assert gpu["bad"] == 0
+    for r0 in range(0, N, 256):
+        rows = np.arange(r0, r0 + 256)
+        U.check_dlogits(U.dl_rows(gpu["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
+                        atol=1e-2 if mode == "seq_mean" else 2e-2, kw=KW,
+                        rel_to_max=(mode == "seq_mean"))
+
+
+SHAPES = [(16, 16, 64), (100, 104, 64), (1000, 1008, 64), (4093, 4096, 32), (8192, 8192, 32),
+          (32000, 32000, 32), (32768, 32768, 32), (50257, 50264, 16), (65536, 65536, 16),
+          (100000, 100000, 16), (128256, 128256, 16), (151936, 151936, 16),
+          (152064, 152064, 16), (160000, 160000, 8), (196608, 196608, 8), (200003, 200008, 8)]
+
+
+@pytest.mark.parametrize("V,ld,N", SHAPES, ids=[f"V{s[0]}" for s in SHAPES])
+def test_grpo_shapes(V, ld, N):
+    rng = np.random.default_rng(V)
+    lg, tok, old, ref = U.make_inputs_host(V, N, V, ld=ld)
+    tok[0] = V - 1
+    adv = rng.normal(0, 1.5, N).astype(np.float32)
+    w = rng.choice([0.0, 1.0, 0.5], N).astype(np.float32)
+    w[0] = 1.0
+    U.log(f"grpo V={V} ld={ld} N={N}")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
+    _check_rows(gpu, o, w != 0, f"V={V}")
+    rows = np.arange(N)
+    U.check_dlogits(U.dl_rows(gpu["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
+                    atol=2e-2, kw=KW)
+    if ld > V:  # padding columns are left untouched
+        pad = gpu["dl_dev"][:, V:].float().cpu().numpy()
+        assert np.all(np.isnan(pad))
+
+
+@pytest.mark.parametrize("kl_type,inv_temp", [(0, 0.7), (1, 1.0), (2, 1.3)])
+def test_grpo_kl_types_and_temperature(kl_type, inv_temp):
+    N, V = 64, 5000
+    rng = np.random.default_rng(kl_type)
+    lg = wl.logits_host(77, N, V)
+    tok = wl.sample_tokens_host(lg, V, 77)
+    cur, _ = oracle.logprob_rows(lg, tok, inv_temp=inv_temp)
+    old = (cur + rng.normal(0, 0.05, N)).astype(np.float32)
+    ref = (cur + rng.normal(0, 0.1, N)).astype(np.float32)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = np.ones(N, np.float32)
+    kw = dict(KW, kl_coef=0.1, kl_type=kl_type, inv_temp=inv_temp)
+    U.log(f"grpo kl={kl_type} T^-1={inv_temp}")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, want_dlogits=False, **kw)
+    _check_rows(gpu, o, w != 0)
+    rows = np.arange(N)
+    U.check_dlogits(U.dl_rows(gpu["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
+                    atol=2e-2, kw=kw)
+
+
+def test_grpo_special_values_and_errors():
+    N, V = 8, 3000
+    lg, tok, old, ref = U.make_inputs_host(5, N, V)
+    lg[1, ::5] = 0xFF80  # -inf columns
+    tok[1] = 1  # a finite column
+    lg[2, :] = 0xFF80  # all -inf: counted, excluded
+    tok[3] = V  # out of range: counted, excluded
+    tok[4] = -3  # out of range
+    tok[5] = V - 1
+    adv = np.linspace(-2, 2, N).astype(np.float32)
+    w = np.ones(N, np.float32)
+    w[6] = 0.0  # masked
+    U.log("grpo special values")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, want_dlogits=False, **KW)
+    assert gpu["bad"] == o["bad"] == 3
+    valid = np.array([True, True, False, False, False, True, False, True])
+    _check_rows(gpu, o, valid)
+    rows = np.arange(N)
+    got = U.dl_rows(gpu["dl_dev"], rows, V)
+    for k in (2, 3, 4, 6):
+        assert np.all(got[k] == 0)
+    U.check_dlogits(got, lg, rows, tok, old, ref, adv, w, V, atol=2e-2, kw=KW)
+
+
+def test_grpo_inplace_and_deterministic():
+    N, V = 256, 151936
+    lg, tok, old, ref = U.make_inputs_host(9, N, V)
+    rng = np.random.default_rng(9)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = rng.choice([0.0, 1.0], N, p=[0.2, 0.8]).astype(np.float32)
+    U.log("grpo in-place / determinism")
+    a = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    b = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    c = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, inplace=True, **KW)
+    import torch
+    assert torch.equal(a["dl_dev"].view(torch.int16), b["dl_dev"].view(torch.int16))
+    assert torch.equal(a["dl_dev"].view(torch.int16), c["dl_dev"].view(torch.int16))
+    assert a["loss"] == b["loss"] == c["loss"]
+    assert np.array_equal(a["logp"], c["logp"])
+
+
+def test_grpo_all_masked_and_empty():
+    N, V = 32, 1024
+    lg, tok, old, ref = U.make_inputs_host(3, N, V)
+    z = np.zeros(N, np.float32)
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, z, z, **KW)
+    assert gpu["loss"] == 0.0 and np.all(gpu["logp"] == 0)
+    assert np.all(U.dl_rows(gpu["dl_dev"], np.arange(N), V) == 0)
+    import torch
+    empty = torch.empty((0, V), dtype=torch.bfloat16, device=U.dev())
+    e = U.run_grpo(empty, V, [], [], [], [], [], **KW)
+    assert e["loss"] == 0.0
+
+
+# ----------------------------------------------------------------------------
+# Full-size microbatches (sampled rows), in the benchmark's configuration
+# ----------------------------------------------------------------------------
+def _full_size_case(name, mb_index, seed):
+    import torch
+    lat, ro, mbs, tok_r, tok_t, A32 = _step_tokens(name)
+    mb = mbs[mb_index]
+    V = lat.cfg["V"]
+    N = mb.tok_rollout.size
+    gamma = float(np.float32(lat.cfg["gamma"]))
+    agg = oracle.AGG_SEQ_MEAN_TOKEN_MEAN
+    adv, w, _ = oracle.token_advantages(A32.astype(np.float64), mb.tok_rollout, mb.tok_turn,
+                                        ro.n_turns, ro.n_tokens, gamma, agg, float(ro.n_rollouts))
+    U.log(f"{name} microbatch {mb_index}: generating {N}x{V} logits on the device")
+    lg_dev = wl.logits_device(seed, N, V, device=U.dev())
+    tok = wl.sample_tokens_device(lg_dev, V, seed).cpu().numpy()
+    lg = lg_dev.view(torch.int16).cpu().numpy().view(np.uint16)
+    U.log("oracle log-probs for the old / reference inputs")
+    cur, bad = oracle.logprob_rows(lg, tok)
+    assert bad == 0
+    n_old, n_ref = wl.logp_noise(seed, N)
+    old = (cur + n_old).astype(np.float32)
+    ref = (cur + n_ref).astype(np.float32)
+    return lg_dev, lg, tok, old, ref, adv.astype(np.float32), w.astype(np.float32), V, N
+
+
+@pytest.mark.parametrize("name,mb_index", [("mid", 0), ("mid", -1), ("full", 0)])
+def test_grpo_full_size_microbatch(name, mb_index):
+    import torch
+    seed = 4242 + (mb_index % 7)
+    lg_dev, lg, tok, old, ref, adv, w, V, N = _full_size_case(name, mb_index, seed)
+    valid = w != 0
+    rng = np.random.default_rng(seed)
+    sample = np.unique(np.concatenate([rng.choice(np.flatnonzero(valid), 24, replace=False),
+                                       rng.choice(N, 8, replace=False), [0, N - 1]]))
+    # (1) the configuration the benchmark runs: sample-level weights
+    U.log(f"{name}[{mb_index}] GPU run, default weights")
+    gpu = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, **KW)
+    U.log("oracle over every row (log-probs and loss)")
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, want_dlogits=False, **KW)
+    _check_rows(gpu, o, valid, name)
+    U.check_dlogits(U.dl_rows(gpu["dl_dev"], sample, V), lg, sample, tok, old, ref, adv, w, V,
+                    atol=1e-2, kw=KW, rel_to_max=True)
+    del gpu
+    torch.cuda.empty_cache()
+    # (2) unit weights, where a 2e-2 absolute bound on dlogits is meaningful
+    w1 = valid.astype(np.float32)
+    U.log(f"{name}[{mb_index}] GPU run, unit weights")
+    gpu1 = U.run_grpo(lg_dev, V, tok, old, ref, adv, w1, want_tok_loss=False, **KW)
+    U.check_dlogits(U.dl_rows(gpu1["dl_dev"], sample, V), lg, sample, tok, old, ref, adv, w1, V,
+                    atol=2e-2, kw=KW)
+    assert gpu1["bad"] == 0
