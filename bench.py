@@ -153,13 +153,15 @@ def run_step(L, s, events=None):
             events.append((e0, e1))
 
 
+COPY_PROBE_BYTES = 1 << 30
+
+
 def copy_probe(torch, dev):
-    """A plain device copy of known size (1 GiB each way), the reference the
-    HBM byte counters are scaled by."""
-    a = torch.empty(1 << 29, dtype=torch.int16, device=dev)
-    a.fill_(1)
+    """A plain elementwise kernel of known size (reads 1 GiB, writes 1 GiB):
+    the reference the profiler's HBM byte counters are scaled by."""
+    a = torch.ones(COPY_PROBE_BYTES // 2, dtype=torch.int16, device=dev)
     b = torch.empty_like(a)
-    b.copy_(a)
+    torch.bitwise_not(a, out=b)
     torch.cuda.synchronize()
 
 
@@ -181,7 +183,7 @@ def cpu_baseline(s, seconds: float):
                                         s["gamma"], oracle.AGG_SEQ_MEAN_TOKEN_MEAN,
                                         float(ro.n_rollouts))
     t_small = time.perf_counter() - t0
-    valid_rows = np.flatnonzero(w[:R] != 0)
+    valid_rows = np.flatnonzero(w != 0)  # generated-token rows of the whole step
     chunk = 4 * cores
     done = 0
     t_rows = 0.0  # oracle time only; device->host copies of the sample are excluded
@@ -201,8 +203,8 @@ def cpu_baseline(s, seconds: float):
     step_time = t_small + t_rows / max(done, 1) * n_valid
     return {"value": n_valid / step_time, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s) and "
-                      f"the fused objective with dlogits on {done} generated-token rows of "
-                      f"microbatch 0 ({t_rows:.1f} s), scaled to the step's {n_valid} tokens"}
+                      f"the fused objective with dlogits on the first {done} generated-token rows "
+                      f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens"}
 
 
 def main():

@@ -165,11 +165,17 @@ def check_dlogits(gpu_rows, lg_u16, rows, tok, old, ref, adv, w, V, atol, kw, re
     return o
 
 
-def make_inputs_host(seed, N, V, ld=None, old_sigma=wl.OLD_SIGMA):
-    """Host-generated bf16 logits and the derived token ids and log-probs."""
+def make_inputs_host(seed, N, V, ld=None, old_sigma=wl.OLD_SIGMA, edit=None):
+    """Host-generated bf16 logits and the derived token ids and log-probs.
+    ``edit(lg, tok)`` may change logits or token ids in place first; the old
+    and reference log-probs always follow the final logits and ids (rows the
+    oracle cannot score get 0)."""
     lg = wl.logits_host(seed, N, V, ld)
     tok = wl.sample_tokens_host(lg, V, seed)
-    cur, bad = oracle.logprob_rows(lg, tok, V=V)
-    assert bad == 0
+    if edit is not None:
+        edit(lg, tok)
+    safe = np.where((tok >= 0) & (tok < V), tok, 0)
+    cur, _ = oracle.logprob_rows(lg, safe, V=V)
+    cur = np.where(np.isfinite(cur) & (tok >= 0) & (tok < V), cur, 0.0)
     n_old, n_ref = wl.logp_noise(seed, N, old_sigma=old_sigma)
     return lg, tok, (cur + n_old).astype(np.float32), (cur + n_ref).astype(np.float32)

@@ -200,8 +200,11 @@ SHAPES = [(16, 16, 64), (100, 104, 64), (1000, 1008, 64), (4093, 4096, 32), (819
 @pytest.mark.parametrize("V,ld,N", SHAPES, ids=[f"V{s[0]}" for s in SHAPES])
 def test_grpo_shapes(V, ld, N):
     rng = np.random.default_rng(V)
-    lg, tok, old, ref = U.make_inputs_host(V, N, V, ld=ld)
-    tok[0] = V - 1
+
+    def last_token(lg, tok):
+        tok[0] = V - 1
+
+    lg, tok, old, ref = U.make_inputs_host(V, N, V, ld=ld, edit=last_token)
     adv = rng.normal(0, 1.5, N).astype(np.float32)
     w = rng.choice([0.0, 1.0, 0.5], N).astype(np.float32)
     w[0] = 1.0
@@ -240,13 +243,16 @@ def test_grpo_kl_types_and_temperature(kl_type, inv_temp):
 
 def test_grpo_special_values_and_errors():
     N, V = 8, 3000
-    lg, tok, old, ref = U.make_inputs_host(5, N, V)
-    lg[1, ::5] = 0xFF80  # -inf columns
-    tok[1] = 1  # a finite column
-    lg[2, :] = 0xFF80  # all -inf: counted, excluded
-    tok[3] = V  # out of range: counted, excluded
-    tok[4] = -3  # out of range
-    tok[5] = V - 1
+
+    def edit(lg, tok):
+        lg[1, ::5] = 0xFF80  # -inf columns
+        tok[1] = 1  # a finite column
+        lg[2, :] = 0xFF80  # all -inf: counted, excluded
+        tok[3] = V  # out of range: counted, excluded
+        tok[4] = -3  # out of range
+        tok[5] = V - 1
+
+    lg, tok, old, ref = U.make_inputs_host(5, N, V, edit=edit)
     adv = np.linspace(-2, 2, N).astype(np.float32)
     w = np.ones(N, np.float32)
     w[6] = 0.0  # masked
