@@ -206,8 +206,13 @@ size_t leap_grpo_workspace_size(int64_t N, int32_t V);
  * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
  * logp_out, tok_loss_out  float [N], nullable (tok_loss is unweighted loss_k).
  * loss_out   float [1], required: sum_k w_k * loss_k, summed in a fixed order.
- * workspace  device buffer of >= leap_grpo_workspace_size(N, V) bytes.
+ * workspace  device buffer of >= leap_grpo_workspace_size(N, V) bytes,
+ *            8-byte aligned; its contents on entry do not matter and it is
+ *            scratch for this call only (calls that share one workspace
+ *            must be ordered on one stream).
  * Alignment: logits and dlogits 16-byte aligned, ld % 8 == 0, ld >= V.
+ * Finite logits are expected below 2^121 in magnitude (the row maximum is
+ *            taken on an fp16 reading of the bf16 bits, exact below that).
  * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a parameter out of
  * range, a required pointer NULL; LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE;
  * LEAP_ERR_UNSUPPORTED for an unknown kl_type.

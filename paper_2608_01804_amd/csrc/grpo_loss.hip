@@ -2,24 +2,32 @@
 // token), over bf16 [rows x vocab] logits.
 //
 // Design (gfx950, wave64):
-//  * One workgroup per row.  For V up to 196608 the whole row is held in
-//    VGPRs: each lane owns CH 16-byte chunks (8 bf16 each) at chunk index
-//    j*BLOCK + lane, so every load and store instruction of a wave covers
-//    1 KiB of contiguous HBM.  The row is read from HBM exactly once.
-//  * Pass A (registers only): the lane's running maximum, with gfx950's
-//    NaN-propagating v_maximum3_f32.
-//  * Pass B (registers only): e = 2^(x*c - m_lane*c) with c = log2(e)/T, the
-//    lane's sum of e, and e itself re-packed as fp16 into the registers that
-//    held the bf16 logits (e lies in [0, 1], so fp16 keeps 11 significant
-//    bits).  One transcendental per element for the whole kernel.
-//  * One (max, sum) merge across the workgroup: wave butterfly, then the
-//    per-wave partials through LDS, merged by every thread in a fixed order,
-//    so all threads hold the same bitwise result and no second barrier is
-//    needed.  Every thread then evaluates the scalar per-token epilogue
-//    (log-prob, ratio, clipped surrogate, KL, dloss/dlogp) redundantly.
-//  * Pass C: dlogits = scale_lane * e (one fp16->fp32 convert and one
-//    multiply per element), packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and
-//    stored 16 bytes at a time; the token's own column gets g * (1 - p_y).
+//  * Persistent workgroups, one row at a time each, rows handed out by an
+//    atomic queue in the workspace (masked rows cost far less than live
+//    ones, so a static split would leave a long tail).  For V up to 196608
+//    the whole row is held in VGPRs: each lane owns CH 16-byte chunks (8 bf16
+//    each) at chunk index j*BLOCK + lane, so every load and store
+//    instruction of a wave covers 1 KiB of contiguous HBM, and the row is
+//    read from HBM exactly once.
+//  * Pass A (registers only): the lane maximum with v_pk_max_f16 applied to
+//    the raw bf16 words.  For finite values below 2^121 in magnitude the
+//    fp16 reading of a bf16 bit pattern orders like the bf16 value, and the
+//    bf16 -inf pattern reads as a quiet NaN, which the max ignores.
+//  * Pass B (registers only): e = 2^(x*c - m_lane*c) with c = log2(e)/T
+//    (one transcendental per element for the whole kernel), e re-packed as
+//    fp16 into the registers that held the logits (e is in [0, 1]), and the
+//    lane sum taken from the packed pairs with v_dot2c_f32_f16.
+//  * One (max, sum) merge across the workgroup: wave butterfly, per-wave
+//    partials through LDS, and the same butterfly in every wave, so all
+//    threads hold bitwise identical values.  Every thread then evaluates the
+//    scalar per-token epilogue (log-prob, ratio, clipped surrogate, KL,
+//    dloss/dlogp) redundantly.
+//  * Pass C: dlogits = scale_lane * e with v_fma_mix_f32 reading the fp16
+//    value directly, packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and stored
+//    16 bytes at a time; the token's own column gets g * (1 - p_y).  As each
+//    chunk is stored, the same registers start loading the chunk of the
+//    next row, so the next row's HBM reads overlap this row's compute and
+//    writes.
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
 //  * Larger vocabularies use a streaming variant that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
@@ -106,12 +114,17 @@ struct RowOut {
     float logp, loss, g, lse2;
 };
 
+// Hardware exp2 / log2 (v_exp_f32, v_log_f32, about 1 ulp): no polynomial
+// constants, which would otherwise be hoisted into registers in the
+// persistent row loop.
+__device__ __forceinline__ float hw_exp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+
 __device__ __forceinline__ RowOut row_epilogue(float lse2, float xy, float old_lp, float ref_lp,
                                                float A, float w, const Params& p) {
     RowOut o;
     const float lse = lse2 * kLn2;
     const float logp = p.inv_temp * xy - lse;
-    const float rho = expf(logp - old_lp);
+    const float rho = hw_exp(logp - old_lp);
     const float clipped = fminf(fmaxf(rho, 1.0f - p.eps_lo), 1.0f + p.eps_hi);
     const float surr = fminf(rho * A, clipped * A);
     float kl, dkl;
@@ -124,7 +137,7 @@ __device__ __forceinline__ RowOut row_epilogue(float lse2, float xy, float old_l
         dkl = dd;
     } else {
         const float dd = ref_lp - logp;
-        const float em1 = expm1f(dd);
+        const float em1 = hw_exp(dd) - 1.0f;
         kl = em1 - dd;
         dkl = -em1;
     }
@@ -176,153 +189,285 @@ __device__ __forceinline__ void block_ms_reduce(float& m, float& s, float* s_m, 
 }
 
 // ---------------------------------------------------------------------------
-// Register-resident variant: BLOCK threads x CH chunks x 8 columns >= V.
-// Slots j < SAFE are full for every V this instantiation is picked for
-// (BLOCK*SAFE < number of chunks), so only the trailing slots carry range
-// checks.
+// Register-resident, persistent variant: BLOCK threads x CH chunks x 8
+// columns >= V.  Slots j < SAFE are full for every V this instantiation is
+// picked for (BLOCK*SAFE < number of chunks), so only the trailing slots
+// carry range checks.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t pk_max_f16(uint32_t a, uint32_t b) {
+    uint32_t d;
+    asm("v_pk_max_f16 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+    return d;
+}
+
+// fp16 half of a packed word times s, in fp32 (v_fma_mix_f32 reads the fp16
+// operand directly).
+__device__ __forceinline__ float mix_lo(uint32_t h2, float s) {
+    float d;
+    asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel_hi:[1,0,0]" : "=v"(d) : "v"(h2), "v"(s));
+    return d;
+}
+__device__ __forceinline__ float mix_hi(uint32_t h2, float s) {
+    float d;
+    asm("v_fma_mix_f32 %0, %1, %2, 0 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(h2),
+        "v"(s));
+    return d;
+}
+
+// fp16 bit pattern of a lane maximum -> the bf16 value it stands for, as
+// fp32; a NaN pattern means the lane saw no finite value (-inf).
+__device__ __forceinline__ float max_half_to_f32(uint32_t h) {
+    h &= 0xffffu;
+    if ((h & 0x7c00u) == 0x7c00u && (h & 0x03ffu) != 0u) return -INFINITY;
+    return __uint_as_float(h << 16);
+}
+
+// Values every lane of the workgroup holds identically (read back from LDS),
+// moved to scalar registers so that row addressing stays scalar.
+__device__ __forceinline__ int64_t uniform_i64(long long v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+__device__ __forceinline__ float uniform_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
+__device__ __forceinline__ bool row_live(float w, int y, int V) {
+    return w != 0.0f && y >= 0 && y < V;
+}
+
+// Chunk j of a lane.  Slots below SAFE are in the row for every V the
+// instantiation serves, so their slot offset goes in the scalar offset and
+// all of them share one VGPR lane offset; trailing slots put the whole offset
+// in the VGPR, where the descriptor's range check applies (a load past the
+// row returns 0, a store past it is dropped).
+template <int BLOCK, int SAFE>
+__device__ __forceinline__ u32x4 load_chunk(__amdgpu_buffer_rsrc_t rs, int lane16, int j) {
+    if (j < SAFE) return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16, j * BLOCK * 16, kCacheNT);
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16 + j * BLOCK * 16, 0, kCacheNT);
+}
+
+template <int BLOCK, int SAFE>
+__device__ __forceinline__ void store_chunk(u32x4 v, __amdgpu_buffer_rsrc_t rs, int lane16, int j) {
+    if (j < SAFE)
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16, j * BLOCK * 16, kCacheNT);
+    else
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16 + j * BLOCK * 16, 0, kCacheNT);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const uint16_t* row, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(row), 0, bytes, kBufferFlags);
+}
+
+template <int BLOCK, int CH, int SAFE>
+__device__ __forceinline__ void load_row(u32x4 (&x)[CH], const uint16_t* xrow, int nchunks,
+                                         int lane16) {
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(xrow, nchunks * 16);
+#pragma unroll
+    for (int j = 0; j < CH; ++j) x[j] = load_chunk<BLOCK, SAFE>(rs, lane16, j);
+}
+
 template <int BLOCK, int CH, int SAFE>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
-grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, const int32_t* __restrict__ token_ids,
-                   const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
-                   const float* __restrict__ adv_tok, const float* __restrict__ w_tok, Params p,
-                   float* __restrict__ logp_out, float* __restrict__ tok_loss_out,
-                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
-    __shared__ float s_m[BLOCK / kWave];
-    __shared__ float s_s[BLOCK / kWave];
+grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, int64_t N,
+                   const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+                   const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+                   const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+                   float* __restrict__ tok_loss_out, float* __restrict__ row_loss,
+                   uint16_t* dlogits, int32_t* __restrict__ dev_err,
+                   unsigned long long* __restrict__ queue) {
+    constexpr int NW = BLOCK / kWave;
+    __shared__ float s_m[2][NW];
+    __shared__ float s_s[2][NW];
+    __shared__ long long s_next[2];
+    __shared__ float s_nw[2];
+    __shared__ int s_ny[2];
     const int tid = threadIdx.x;
-    const int64_t row = blockIdx.x;
+    const int lane16 = tid * 16;
     const int nchunks = (V + 7) >> 3;
     const int nfull = V >> 3;
-    const uint16_t* xrow = logits + row * ld;
-    uint16_t* drow = dlogits + row * ld;
-
-    const float w = w_tok[row];
-    const int y = token_ids[row];
-    bool live = (w != 0.0f);
-    if (live && (y < 0 || y >= V)) {
-        if (tid == 0) count_error(dev_err);
-        live = false;
-    }
-    if (!live) {
-        zero_row<BLOCK>(drow, V, tid);
-        if (tid == 0) write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-        return;
-    }
-
-    // The whole row into registers: one read of HBM.  Buffer instructions
-    // over a descriptor for this row take a 32-bit lane offset, so no 64-bit
-    // address per chunk is kept live; the descriptor's size is the row, so
-    // the hardware range check backs up the explicit slot checks below.
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(xrow), 0, nchunks * 16, kBufferFlags);
-    u32x4 x[CH];
-#pragma unroll
-    for (int j = 0; j < CH; ++j)
-        x[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, (j * BLOCK + tid) * 16, 0, kCacheNT);
-    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
-    // Only the trailing slots can reach past the row (the host picks the
-    // smallest CH that covers it): empty slots and the columns >= V of a
-    // partial chunk become -inf.
-#pragma unroll
-    for (int j = SAFE; j < CH; ++j) {
-        if ((j + 1) * BLOCK > nfull) {
-            const int c = j * BLOCK + tid;
-            if (c >= nchunks)
-                x[j] = u32x4_of(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
-            else if (c == nfull)
-                x[j] = mask_tail(x[j], V & 7);
-        }
-    }
-
-    // Pass A: lane maximum.
-    float m = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < CH; ++j) {
-        m = vmax(m, vmax(bf_lo(x[j].x), bf_hi(x[j].x)));
-        m = vmax(m, vmax(bf_lo(x[j].y), bf_hi(x[j].y)));
-        m = vmax(m, vmax(bf_lo(x[j].z), bf_hi(x[j].z)));
-        m = vmax(m, vmax(bf_lo(x[j].w), bf_hi(x[j].w)));
-    }
-
-    // Keep the bf16 words as the only live copy of the row: without this the
-    // compiler keeps pass A's unpacked fp32 values alive for pass B and the
-    // row no longer fits in VGPRs.
-#pragma unroll
-    for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
-
-    // Pass B: e = 2^(x c - m c), lane sum, e kept as fp16 in place.  Chunk
-    // j's inputs are tied to chunk j-1's packed output, so the scheduler
-    // keeps about one chunk of fp32 temporaries live instead of hoisting
-    // every exponential of the row at once.
     const float c2 = kLog2e * p.inv_temp;
-    const float mc = (m == -INFINITY) ? 0.0f : m * c2;
-    float s = 0.0f;
-#pragma unroll
-    for (int j = 0; j < CH; ++j) {
-        if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
-        uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
-            const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
-            s += a;
-            s += b;
-            wv[q] = pack_f16(a, b);
-        }
-        x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
-    }
 
-    float M = (m == -INFINITY) ? -INFINITY : mc;
-    float S = s;
-    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
-    if (M == -INFINITY) {  // every logit of the row is -inf
-        if (tid == 0) count_error(dev_err);
-        zero_row<BLOCK>(drow, V, tid);
-        if (tid == 0) write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-        return;
-    }
-    const float lse2 = M + log2f(S);
-    const RowOut o = row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
+    int64_t row = blockIdx.x;
+    float w = w_tok[row];
+    int y = token_ids[row];
+    bool live = row_live(w, y, V);
+    u32x4 x[CH];
+    if (live) load_row<BLOCK, CH, SAFE>(x, logits + row * ld, nchunks, lane16);
+    int par = 0;
 
-    // Pass C: dlogits = -g * p_v = sc * e_v; the token's column gets g (1 - p_y).
-    const float sc = -o.g * exp2f(mc - lse2);
-    const float dy = o.g * (1.0f - expf(o.logp));
-    const int cy = y >> 3;
-    const int ey = y & 7;
-    const __amdgpu_buffer_rsrc_t rd =
-        __builtin_amdgcn_make_buffer_rsrc(drow, 0, nfull * 16, kBufferFlags);
-    u32x4 prev = u32x4_of(0u, 0u, 0u, 0u);
-#pragma unroll
-    for (int j = 0; j < CH; ++j) {
-        const int c = j * BLOCK + tid;
-        asm volatile("" : "+v"(x[j]) : "v"(prev));
-        const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
-        float d[8];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            d[2 * q] = sc * f16_lo(wv[q]);
-            d[2 * q + 1] = sc * f16_hi(wv[q]);
+    for (;;) {
+        // Claim the row after this one; its weight and token id arrive while
+        // this row computes and are published at this row's barrier.
+        long long nxt = 0;
+        float nw = 0.0f;
+        int ny = 0;
+        if (tid == 0) {
+            nxt = static_cast<long long>(atomicAdd(queue, 1ull));
+            if (nxt < N) {
+                nw = w_tok[nxt];
+                ny = token_ids[nxt];
+            }
+            if (w != 0.0f && !live) count_error(dev_err);  // token id out of range
         }
-        if (c == cy) {
+        const uint16_t* xrow = logits + row * ld;
+        uint16_t* drow = dlogits + row * ld;
+        int64_t next_row;
+        float next_w;
+        int next_y;
+        bool next_live;
+
+        if (live) {
+            const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+            // Only the trailing slots can reach past the row: empty slots and
+            // the columns >= V of a partial chunk become -inf.
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (e == ey) d[e] = dy;
-        }
-        const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
-                                   pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
-        if (j < SAFE || c < nfull) {
-            __builtin_amdgcn_raw_buffer_store_b128(out, rd, c * 16, 0, kCacheNT);
-        } else if (c == nfull) {  // partial last chunk (V % 8 != 0)
-            const int rem = V & 7;
+            for (int j = SAFE; j < CH; ++j) {
+                if ((j + 1) * BLOCK > nfull) {
+                    const int c = j * BLOCK + tid;
+                    if (c >= nchunks)
+                        x[j] = u32x4_of(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
+                    else if (c == nfull)
+                        x[j] = mask_tail(x[j], V & 7);
+                }
+            }
+
+            // Pass A: lane maximum over the raw bf16 words.
+            uint32_t mh = kNegInfPair;
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (e < rem)
-                    drow[(c << 3) + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+            for (int j = 0; j < CH; ++j)
+                mh = pk_max_f16(pk_max_f16(mh, x[j].x),
+                                pk_max_f16(x[j].y, pk_max_f16(x[j].z, x[j].w)));
+            const float m = fmaxf(max_half_to_f32(mh), max_half_to_f32(mh >> 16));
+
+            // Keep the bf16 words as the only live copy of the row.
+#pragma unroll
+            for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
+
+            // Pass B: e = 2^(x c - m c) kept as fp16 in place; lane sum from
+            // the packed pairs.  Chunk j's inputs are tied to chunk j-1's
+            // output so about one chunk of fp32 temporaries is live at once.
+            const float mc = (m == -INFINITY) ? 0.0f : m * c2;
+            const half2v ones = {static_cast<_Float16>(1.0f), static_cast<_Float16>(1.0f)};
+            float s = 0.0f;
+#pragma unroll
+            for (int j = 0; j < CH; ++j) {
+                if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
+                uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
+                    const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+                    wv[q] = pack_f16(a, b);
+                    s = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, wv[q]), ones, s, false);
+                }
+                x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
+            }
+
+            if (tid == 0) {
+                s_next[par] = nxt;
+                s_nw[par] = nw;
+                s_ny[par] = ny;
+            }
+            float M = (m == -INFINITY) ? -INFINITY : mc;
+            float S = s;
+            block_ms_reduce<BLOCK>(M, S, s_m[par], s_s[par], tid);  // the row's barrier
+            next_row = uniform_i64(s_next[par]);
+            next_w = uniform_f32(s_nw[par]);
+            next_y = __builtin_amdgcn_readfirstlane(s_ny[par]);
+            next_live = next_row < N && row_live(next_w, next_y, V);
+
+            if (M == -INFINITY) {  // every logit of the row is -inf
+                if (tid == 0) {
+                    count_error(dev_err);
+                    write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+                }
+                zero_row<BLOCK>(drow, V, tid);
+                if (next_live) load_row<BLOCK, CH, SAFE>(x, logits + next_row * ld, nchunks, lane16);
+            } else {
+                const float lse2 = M + __builtin_amdgcn_logf(S);
+                const RowOut o =
+                    row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
+
+                // Pass C: dlogits = -g * p_v = sc * e_v; the token's column
+                // gets g (1 - p_y).  Each chunk's registers then start
+                // loading the next row's chunk.
+                const float sc = -o.g * __builtin_amdgcn_exp2f(mc - lse2);
+                const float dy = o.g * (1.0f - hw_exp(o.logp));
+                const int cy = y >> 3;
+                const int ey = y & 7;
+                const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+                const __amdgpu_buffer_rsrc_t rn =
+                    row_rsrc(next_live ? logits + next_row * ld : xrow, nchunks * 16);
+                u32x4 prev = u32x4_of(0u, 0u, 0u, 0u);
+#pragma unroll
+                for (int j = 0; j < CH; ++j) {
+                    const int c = j * BLOCK + tid;
+                    asm volatile("" : "+v"(x[j]) : "v"(prev));
+                    const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
+                    float d[8];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        d[2 * q] = mix_lo(wv[q], sc);
+                        d[2 * q + 1] = mix_hi(wv[q], sc);
+                    }
+                    if (c == cy) {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (e == ey) d[e] = dy;
+                    }
+                    const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
+                                               pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
+                    if (j < SAFE || c < nfull) {
+                        store_chunk<BLOCK, SAFE>(out, rd, lane16, j);
+                    } else if (c == nfull) {  // partial last chunk (V % 8 != 0)
+                        const int rem = V & 7;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (e < rem)
+                                drow[(c << 3) + e] =
+                                    static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+                    }
+                    prev = out;
+                    if (next_live) {
+                        // The address depends on this chunk's output, so the
+                        // load cannot be hoisted above its last use of x[j].
+                        int off = lane16;
+                        asm volatile("" : "+v"(off) : "v"(out));
+                        x[j] = load_chunk<BLOCK, SAFE>(rn, off, j);
+                    }
+                }
+                if (tid == 0)
+                    write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+            }
+        } else {
+            zero_row<BLOCK>(drow, V, tid);
+            if (tid == 0) {
+                write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+                s_next[par] = nxt;
+                s_nw[par] = nw;
+                s_ny[par] = ny;
+            }
+            __syncthreads();
+            next_row = uniform_i64(s_next[par]);
+            next_w = uniform_f32(s_nw[par]);
+            next_y = __builtin_amdgcn_readfirstlane(s_ny[par]);
+            next_live = next_row < N && row_live(next_w, next_y, V);
+            if (next_live) load_row<BLOCK, CH, SAFE>(x, logits + next_row * ld, nchunks, lane16);
         }
-        prev = out;
+        if (next_row >= N) break;
+        row = next_row;
+        w = next_w;
+        y = next_y;
+        live = next_live;
+        par ^= 1;
     }
-    if (tid == 0) write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+}
+
+// The row queue starts after the rows every workgroup takes first.
+__global__ void queue_init_kernel(unsigned long long* queue, unsigned long long first) {
+    *queue = first;
 }
 
 // ---------------------------------------------------------------------------
@@ -442,45 +587,76 @@ __global__ __launch_bounds__(kReduceBlock) void loss_reduce_kernel(const float* 
 // ---------------------------------------------------------------------------
 // Host dispatch
 // ---------------------------------------------------------------------------
-using RowKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*, const float*,
-                           const float*, const float*, Params, float*, float*, float*, uint16_t*,
-                           int32_t*);
+using ResidentKernel = void (*)(const uint16_t*, int64_t, int, int64_t, const int32_t*,
+                                const float*, const float*, const float*, const float*, Params,
+                                float*, float*, float*, uint16_t*, int32_t*, unsigned long long*);
+using StreamKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*,
+                              const float*, const float*, const float*, Params, float*, float*,
+                              float*, uint16_t*, int32_t*);
 
 struct RowConfig {
-    RowKernel fn;
+    ResidentKernel fn;  // nullptr: streaming variant
     int block;
-    int ch;  // 0 for the streaming variant
+    int ch;
+    int slot;  // index into the occupancy cache
 };
 
-#define LEAP_RES(B, C, S) RowConfig{grpo_rows_resident<B, C, S>, B, C}
+#define LEAP_RES(B, C, S, I) RowConfig{grpo_rows_resident<B, C, S>, B, C, I}
+
+constexpr int kNumConfigs = 14;
 
 // Smallest resident configuration whose BLOCK*CH*8 columns cover V.  SAFE of
 // each entry is the CH of the entry before it with the same BLOCK (0 for the
 // first), which is what makes its leading slots provably full.
 RowConfig pick_row_config(int V) {
-    static const RowConfig table[] = {
-        LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
-        LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
-        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_RES(1024, 8, 0),
-        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_RES(1024, 19, 16),
-        LEAP_RES(1024, 20, 19), LEAP_RES(1024, 24, 20),
+    static const RowConfig table[kNumConfigs] = {
+        LEAP_RES(64, 1, 0, 0),      LEAP_RES(64, 2, 1, 1),      LEAP_RES(64, 4, 2, 2),
+        LEAP_RES(64, 8, 4, 3),      LEAP_RES(256, 4, 0, 4),     LEAP_RES(256, 8, 4, 5),
+        LEAP_RES(256, 12, 8, 6),    LEAP_RES(256, 16, 12, 7),   LEAP_RES(1024, 8, 0, 8),
+        LEAP_RES(1024, 12, 8, 9),   LEAP_RES(1024, 16, 12, 10), LEAP_RES(1024, 19, 16, 11),
+        LEAP_RES(1024, 20, 19, 12), LEAP_RES(1024, 24, 20, 13),
     };
     const int64_t nchunks = (static_cast<int64_t>(V) + 7) / 8;
     for (const RowConfig& r : table)
         if (static_cast<int64_t>(r.block) * r.ch >= nchunks) return r;
-    return RowConfig{grpo_rows_stream<1024>, 1024, 0};
+    return RowConfig{nullptr, 1024, 0, -1};
 }
 
 #undef LEAP_RES
+
+// Resident workgroups per device for each configuration: compute units times
+// the workgroups one compute unit holds (queried once per device).
+constexpr int kMaxDevices = 64;
+int g_resident[kMaxDevices][kNumConfigs];
+
+int resident_workgroups(const RowConfig& rc) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+    int& cached = g_resident[dev][rc.slot];
+    if (cached > 0) return cached;
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, rc.fn, rc.block, 0) != hipSuccess)
+        return 0;
+    if (cus < 1) cus = 1;
+    if (per_cu < 1) per_cu = 1;
+    cached = cus * per_cu;
+    return cached;
+}
+
+size_t row_loss_bytes(int64_t N) {
+    const size_t b = static_cast<size_t>(N > 0 ? N : 0) * sizeof(float);
+    return (b + 255) & ~static_cast<size_t>(255);
+}
 
 }  // namespace
 }  // namespace leap
 
 LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
     (void)V;
-    if (N <= 0) return 256;
-    const size_t b = static_cast<size_t>(N) * sizeof(float);
-    return (b + 255) & ~static_cast<size_t>(255);
+    // per-row weighted losses, then the row queue (one 256-byte line)
+    return leap::row_loss_bytes(N) + 256;
 }
 
 LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
@@ -512,15 +688,30 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
         if (a0 != b0 && a0 < b0 + bytes && b0 < a0 + bytes) return LEAP_ERR_INVALID_ARG;
     }
     if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 7u) != 0) return LEAP_ERR_MISALIGNED;
 
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     float* row_loss = static_cast<float*>(workspace);
+    unsigned long long* queue = reinterpret_cast<unsigned long long*>(
+        static_cast<char*>(workspace) + row_loss_bytes(N));
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
-        hipLaunchKernelGGL(rc.fn, dim3(static_cast<unsigned>(N)), dim3(rc.block), 0, stream,
-                           static_cast<const uint16_t*>(logits_bf16), ld, V, token_ids, old_logp,
-                           ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss,
-                           static_cast<uint16_t*>(dlogits_bf16), dev_err);
+        const uint16_t* lg = static_cast<const uint16_t*>(logits_bf16);
+        uint16_t* dl = static_cast<uint16_t*>(dlogits_bf16);
+        if (rc.fn) {
+            const int res = resident_workgroups(rc);
+            if (res <= 0) return LEAP_ERR_HIP;
+            const int64_t grid = N < res ? N : res;
+            hipLaunchKernelGGL(queue_init_kernel, dim3(1), dim3(1), 0, stream, queue,
+                               static_cast<unsigned long long>(grid));
+            hipLaunchKernelGGL(rc.fn, dim3(static_cast<unsigned>(grid)), dim3(rc.block), 0, stream,
+                               lg, ld, V, N, token_ids, old_logp, ref_logp, adv_tok, w_tok, p,
+                               logp_out, tok_loss_out, row_loss, dl, dev_err, queue);
+        } else {
+            hipLaunchKernelGGL(grpo_rows_stream<1024>, dim3(static_cast<unsigned>(N)), dim3(1024),
+                               0, stream, lg, ld, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
+                               p, logp_out, tok_loss_out, row_loss, dl, dev_err);
+        }
         const leap_status st = launch_status();
         if (st != LEAP_OK) return st;
     }
