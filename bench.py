@@ -165,6 +165,29 @@ def copy_probe(torch, dev):
     torch.cuda.synchronize()
 
 
+def hbm_probe(L, torch, dev, gib: int = 4, reps: int = 5):
+    """Achievable HBM rates of the device for the three access mixes, from
+    the library's streaming probe (median of `reps` launches over `gib` GiB)."""
+    n = gib << 30
+    a = torch.ones(n // 2, dtype=torch.int16, device=dev)
+    b = torch.empty_like(a)
+    out = {}
+    for mode, name, moved in ((0, "copy", 2 * n), (1, "read", n), (2, "write", n)):
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            L.leap_probe_hbm(a, b, n, mode)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        out[f"{name}_GBps"] = moved / float(np.median(ts)) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(s, seconds: float):
     """The fp64 oracle (as it is) on the host cores over a bounded sample of
     the same step: the tournament, gate and token advantages over the whole
@@ -232,6 +255,8 @@ def main():
     if args.workload == "full":
         raise SystemExit("the full workload does not fit resident; bench runs 'mid'")
 
+    probe = hbm_probe(L, torch, dev)
+    log(f"[bench] HBM probe: " + ", ".join(f"{k} {v:.0f}" for k, v in probe.items()))
     s = build_step(L, torch, dev, args.workload, args.seed)
     copy_probe(torch, dev)
 
@@ -295,7 +320,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": traffic,
                      "kernel": "grpo_rows_resident<1024,19> + loss_reduce (one fused call)",
-                     "avg_launch_us": k4_avg_s * 1e6, "bytes_per_launch": bytes_per_launch},
+                     "avg_launch_us": k4_avg_s * 1e6, "bytes_per_launch": bytes_per_launch,
+                     "probe_GBps": probe,
+                     "frac_of_probe_copy": achieved / 1e9 / probe["copy_GBps"]},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

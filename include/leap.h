@@ -227,6 +227,19 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
                                            size_t ws_bytes, int32_t *dev_err,
                                            hipStream_t stream);
 
+/*
+ * Measurement helper, not part of the method: streams device memory with the
+ * access shape of the fused kernel (16-byte non-temporal accesses) so the
+ * achievable HBM rate of each access mix can be set beside the published
+ * peak.  mode 0: dst = src over `bytes` (read + write); 1: read src only
+ * (dst receives at most 16 bytes); 2: write zeros to dst.
+ * bytes % 16 == 0; src (modes 0, 1) and dst 16-byte aligned, device memory.
+ * Errors: LEAP_ERR_INVALID_ARG for an unknown mode, bytes % 16 != 0 or a NULL
+ * pointer that the mode needs; LEAP_ERR_MISALIGNED.
+ */
+leap_status leap_probe_hbm(const void *src, void *dst, size_t bytes, int32_t mode,
+                           hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2,21 +2,20 @@
 // token), over bf16 [rows x vocab] logits.
 //
 // Design (gfx950, wave64):
-//  * Persistent workgroups, one row at a time each, rows handed out by an
-//    atomic queue in the workspace (masked rows cost far less than live
-//    ones, so a static split would leave a long tail).  For V up to 196608
-//    the whole row is held in VGPRs: each lane owns CH 16-byte chunks (8 bf16
-//    each) at chunk index j*BLOCK + lane, so every load and store
-//    instruction of a wave covers 1 KiB of contiguous HBM, and the row is
-//    read from HBM exactly once.
+//  * One workgroup per row.  For V up to 196608 the whole row is held in
+//    VGPRs: each lane owns CH 16-byte chunks (8 bf16 each) at chunk index
+//    j*BLOCK + lane, so every load and store instruction of a wave covers
+//    1 KiB of contiguous HBM, and the row is read from HBM exactly once.
+//    Buffer instructions address the row through one descriptor, so a lane
+//    keeps one 32-bit offset instead of a 64-bit address per chunk.
 //  * Pass A (registers only): the lane maximum with v_pk_max_f16 applied to
 //    the raw bf16 words.  For finite values below 2^121 in magnitude the
 //    fp16 reading of a bf16 bit pattern orders like the bf16 value, and the
 //    bf16 -inf pattern reads as a quiet NaN, which the max ignores.
 //  * Pass B (registers only): e = 2^(x*c - m_lane*c) with c = log2(e)/T
-//    (one transcendental per element for the whole kernel), e re-packed as
-//    fp16 into the registers that held the logits (e is in [0, 1]), and the
-//    lane sum taken from the packed pairs with v_dot2c_f32_f16.
+//    (one transcendental per element for the whole kernel), summed in fp32,
+//    and re-packed as fp16 into the registers that held the logits (e is in
+//    [0, 1]).
 //  * One (max, sum) merge across the workgroup: wave butterfly, per-wave
 //    partials through LDS, and the same butterfly in every wave, so all
 //    threads hold bitwise identical values.  Every thread then evaluates the
@@ -24,10 +23,7 @@
 //    dloss/dlogp) redundantly.
 //  * Pass C: dlogits = scale_lane * e with v_fma_mix_f32 reading the fp16
 //    value directly, packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and stored
-//    16 bytes at a time; the token's own column gets g * (1 - p_y).  As each
-//    chunk is stored, the same registers start loading the chunk of the
-//    next row, so the next row's HBM reads overlap this row's compute and
-//    writes.
+//    16 bytes at a time; the token's own column gets g * (1 - p_y).
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
 //  * Larger vocabularies use a streaming variant that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
@@ -43,8 +39,10 @@ constexpr uint32_t kNegInfBf16 = 0xFF80u;
 constexpr uint32_t kNegInfPair = 0xFF80FF80u;
 // Word 3 of a raw gfx9 buffer descriptor (32-bit data format, no swizzle).
 constexpr int kBufferFlags = 0x00020000;
-// Cache policy of streaming accesses: non-temporal.
-constexpr int kCacheNT = 2;
+// Cache policies of the row loads and of the dlogits stores (buffer
+// instruction aux bits: 0 = default, 2 = non-temporal).
+constexpr int kLoadPolicy = 2;
+constexpr int kStorePolicy = 2;
 
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf162v __attribute__((ext_vector_type(2)));
@@ -222,17 +220,6 @@ __device__ __forceinline__ float max_half_to_f32(uint32_t h) {
     return __uint_as_float(h << 16);
 }
 
-// Values every lane of the workgroup holds identically (read back from LDS),
-// moved to scalar registers so that row addressing stays scalar.
-__device__ __forceinline__ int64_t uniform_i64(long long v) {
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
-    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
-    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
-}
-__device__ __forceinline__ float uniform_f32(float v) {
-    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
-}
-
 __device__ __forceinline__ bool row_live(float w, int y, int V) {
     return w != 0.0f && y >= 0 && y < V;
 }
@@ -244,16 +231,16 @@ __device__ __forceinline__ bool row_live(float w, int y, int V) {
 // row returns 0, a store past it is dropped).
 template <int BLOCK, int SAFE>
 __device__ __forceinline__ u32x4 load_chunk(__amdgpu_buffer_rsrc_t rs, int lane16, int j) {
-    if (j < SAFE) return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16, j * BLOCK * 16, kCacheNT);
-    return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16 + j * BLOCK * 16, 0, kCacheNT);
+    if (j < SAFE) return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16, j * BLOCK * 16, kLoadPolicy);
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, lane16 + j * BLOCK * 16, 0, kLoadPolicy);
 }
 
 template <int BLOCK, int SAFE>
 __device__ __forceinline__ void store_chunk(u32x4 v, __amdgpu_buffer_rsrc_t rs, int lane16, int j) {
     if (j < SAFE)
-        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16, j * BLOCK * 16, kCacheNT);
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16, j * BLOCK * 16, kStorePolicy);
     else
-        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16 + j * BLOCK * 16, 0, kCacheNT);
+        __builtin_amdgcn_raw_buffer_store_b128(v, rs, lane16 + j * BLOCK * 16, 0, kStorePolicy);
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const uint16_t* row, int bytes) {
@@ -270,204 +257,133 @@ __device__ __forceinline__ void load_row(u32x4 (&x)[CH], const uint16_t* xrow, i
 
 template <int BLOCK, int CH, int SAFE>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
-grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, int64_t N,
+grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
                    const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
                    const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
                    const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
                    float* __restrict__ tok_loss_out, float* __restrict__ row_loss,
-                   uint16_t* dlogits, int32_t* __restrict__ dev_err,
-                   unsigned long long* __restrict__ queue) {
-    constexpr int NW = BLOCK / kWave;
-    __shared__ float s_m[2][NW];
-    __shared__ float s_s[2][NW];
-    __shared__ long long s_next[2];
-    __shared__ float s_nw[2];
-    __shared__ int s_ny[2];
+                   uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    __shared__ float s_m[BLOCK / kWave];
+    __shared__ float s_s[BLOCK / kWave];
     const int tid = threadIdx.x;
     const int lane16 = tid * 16;
+    const int64_t row = blockIdx.x;
     const int nchunks = (V + 7) >> 3;
     const int nfull = V >> 3;
-    const float c2 = kLog2e * p.inv_temp;
+    const uint16_t* xrow = logits + row * ld;
+    uint16_t* drow = dlogits + row * ld;
 
-    int64_t row = blockIdx.x;
-    float w = w_tok[row];
-    int y = token_ids[row];
-    bool live = row_live(w, y, V);
-    u32x4 x[CH];
-    if (live) load_row<BLOCK, CH, SAFE>(x, logits + row * ld, nchunks, lane16);
-    int par = 0;
-
-    for (;;) {
-        // Claim the row after this one; its weight and token id arrive while
-        // this row computes and are published at this row's barrier.
-        long long nxt = 0;
-        float nw = 0.0f;
-        int ny = 0;
+    const float w = w_tok[row];
+    const int y = token_ids[row];
+    if (!row_live(w, y, V)) {
         if (tid == 0) {
-            nxt = static_cast<long long>(atomicAdd(queue, 1ull));
-            if (nxt < N) {
-                nw = w_tok[nxt];
-                ny = token_ids[nxt];
-            }
-            if (w != 0.0f && !live) count_error(dev_err);  // token id out of range
+            if (w != 0.0f) count_error(dev_err);  // token id out of range
+            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
         }
-        const uint16_t* xrow = logits + row * ld;
-        uint16_t* drow = dlogits + row * ld;
-        int64_t next_row;
-        float next_w;
-        int next_y;
-        bool next_live;
-
-        if (live) {
-            const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
-            // Only the trailing slots can reach past the row: empty slots and
-            // the columns >= V of a partial chunk become -inf.
-#pragma unroll
-            for (int j = SAFE; j < CH; ++j) {
-                if ((j + 1) * BLOCK > nfull) {
-                    const int c = j * BLOCK + tid;
-                    if (c >= nchunks)
-                        x[j] = u32x4_of(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
-                    else if (c == nfull)
-                        x[j] = mask_tail(x[j], V & 7);
-                }
-            }
-
-            // Pass A: lane maximum over the raw bf16 words.
-            uint32_t mh = kNegInfPair;
-#pragma unroll
-            for (int j = 0; j < CH; ++j)
-                mh = pk_max_f16(pk_max_f16(mh, x[j].x),
-                                pk_max_f16(x[j].y, pk_max_f16(x[j].z, x[j].w)));
-            const float m = fmaxf(max_half_to_f32(mh), max_half_to_f32(mh >> 16));
-
-            // Keep the bf16 words as the only live copy of the row.
-#pragma unroll
-            for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
-
-            // Pass B: e = 2^(x c - m c) kept as fp16 in place; lane sum from
-            // the packed pairs.  Chunk j's inputs are tied to chunk j-1's
-            // output so about one chunk of fp32 temporaries is live at once.
-            const float mc = (m == -INFINITY) ? 0.0f : m * c2;
-            const half2v ones = {static_cast<_Float16>(1.0f), static_cast<_Float16>(1.0f)};
-            float s = 0.0f;
-#pragma unroll
-            for (int j = 0; j < CH; ++j) {
-                if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
-                uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
-                    const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
-                    wv[q] = pack_f16(a, b);
-                    s = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, wv[q]), ones, s, false);
-                }
-                x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
-            }
-
-            if (tid == 0) {
-                s_next[par] = nxt;
-                s_nw[par] = nw;
-                s_ny[par] = ny;
-            }
-            float M = (m == -INFINITY) ? -INFINITY : mc;
-            float S = s;
-            block_ms_reduce<BLOCK>(M, S, s_m[par], s_s[par], tid);  // the row's barrier
-            next_row = uniform_i64(s_next[par]);
-            next_w = uniform_f32(s_nw[par]);
-            next_y = __builtin_amdgcn_readfirstlane(s_ny[par]);
-            next_live = next_row < N && row_live(next_w, next_y, V);
-
-            if (M == -INFINITY) {  // every logit of the row is -inf
-                if (tid == 0) {
-                    count_error(dev_err);
-                    write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-                }
-                zero_row<BLOCK>(drow, V, tid);
-                if (next_live) load_row<BLOCK, CH, SAFE>(x, logits + next_row * ld, nchunks, lane16);
-            } else {
-                const float lse2 = M + __builtin_amdgcn_logf(S);
-                const RowOut o =
-                    row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
-
-                // Pass C: dlogits = -g * p_v = sc * e_v; the token's column
-                // gets g (1 - p_y).  Each chunk's registers then start
-                // loading the next row's chunk.
-                const float sc = -o.g * __builtin_amdgcn_exp2f(mc - lse2);
-                const float dy = o.g * (1.0f - hw_exp(o.logp));
-                const int cy = y >> 3;
-                const int ey = y & 7;
-                const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
-                const __amdgpu_buffer_rsrc_t rn =
-                    row_rsrc(next_live ? logits + next_row * ld : xrow, nchunks * 16);
-                u32x4 prev = u32x4_of(0u, 0u, 0u, 0u);
-#pragma unroll
-                for (int j = 0; j < CH; ++j) {
-                    const int c = j * BLOCK + tid;
-                    asm volatile("" : "+v"(x[j]) : "v"(prev));
-                    const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
-                    float d[8];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        d[2 * q] = mix_lo(wv[q], sc);
-                        d[2 * q + 1] = mix_hi(wv[q], sc);
-                    }
-                    if (c == cy) {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            if (e == ey) d[e] = dy;
-                    }
-                    const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
-                                               pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
-                    if (j < SAFE || c < nfull) {
-                        store_chunk<BLOCK, SAFE>(out, rd, lane16, j);
-                    } else if (c == nfull) {  // partial last chunk (V % 8 != 0)
-                        const int rem = V & 7;
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            if (e < rem)
-                                drow[(c << 3) + e] =
-                                    static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
-                    }
-                    prev = out;
-                    if (next_live) {
-                        // The address depends on this chunk's output, so the
-                        // load cannot be hoisted above its last use of x[j].
-                        int off = lane16;
-                        asm volatile("" : "+v"(off) : "v"(out));
-                        x[j] = load_chunk<BLOCK, SAFE>(rn, off, j);
-                    }
-                }
-                if (tid == 0)
-                    write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
-            }
-        } else {
-            zero_row<BLOCK>(drow, V, tid);
-            if (tid == 0) {
-                write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-                s_next[par] = nxt;
-                s_nw[par] = nw;
-                s_ny[par] = ny;
-            }
-            __syncthreads();
-            next_row = uniform_i64(s_next[par]);
-            next_w = uniform_f32(s_nw[par]);
-            next_y = __builtin_amdgcn_readfirstlane(s_ny[par]);
-            next_live = next_row < N && row_live(next_w, next_y, V);
-            if (next_live) load_row<BLOCK, CH, SAFE>(x, logits + next_row * ld, nchunks, lane16);
-        }
-        if (next_row >= N) break;
-        row = next_row;
-        w = next_w;
-        y = next_y;
-        live = next_live;
-        par ^= 1;
+        zero_row<BLOCK>(drow, V, tid);
+        return;
     }
-}
 
-// The row queue starts after the rows every workgroup takes first.
-__global__ void queue_init_kernel(unsigned long long* queue, unsigned long long first) {
-    *queue = first;
+    // The whole row into registers: one read of HBM.
+    u32x4 x[CH];
+    load_row<BLOCK, CH, SAFE>(x, xrow, nchunks, lane16);
+    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+    // Only the trailing slots can reach past the row: empty slots and the
+    // columns >= V of a partial chunk become -inf.
+#pragma unroll
+    for (int j = SAFE; j < CH; ++j) {
+        if ((j + 1) * BLOCK > nfull) {
+            const int c = j * BLOCK + tid;
+            if (c >= nchunks)
+                x[j] = u32x4_of(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
+            else if (c == nfull)
+                x[j] = mask_tail(x[j], V & 7);
+        }
+    }
+
+    // Pass A: lane maximum over the raw bf16 words.
+    uint32_t mh = kNegInfPair;
+#pragma unroll
+    for (int j = 0; j < CH; ++j)
+        mh = pk_max_f16(pk_max_f16(mh, x[j].x), pk_max_f16(x[j].y, pk_max_f16(x[j].z, x[j].w)));
+    const float m = fmaxf(max_half_to_f32(mh), max_half_to_f32(mh >> 16));
+
+    // Keep the bf16 words as the only live copy of the row.
+#pragma unroll
+    for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
+
+    // Pass B: e = 2^(x c - m c) summed in fp32 and kept as fp16 in place.
+    // Chunk j's inputs are tied to chunk j-1's output so about one chunk of
+    // fp32 temporaries is live at once.
+    const float c2 = kLog2e * p.inv_temp;
+    const float mc = (m == -INFINITY) ? 0.0f : m * c2;
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
+        uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
+            const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+            s += a;
+            s += b;
+            wv[q] = pack_f16(a, b);
+        }
+        x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
+    }
+
+    float M = (m == -INFINITY) ? -INFINITY : mc;
+    float S = s;
+    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+    if (M == -INFINITY) {  // every logit of the row is -inf
+        if (tid == 0) {
+            count_error(dev_err);
+            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+        }
+        zero_row<BLOCK>(drow, V, tid);
+        return;
+    }
+    const float lse2 = M + __builtin_amdgcn_logf(S);
+    const RowOut o = row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
+
+    // Pass C: dlogits = -g * p_v = sc * e_v; the token's column gets g (1 - p_y).
+    const float sc = -o.g * __builtin_amdgcn_exp2f(mc - lse2);
+    const float dy = o.g * (1.0f - hw_exp(o.logp));
+    const int cy_rel = (y >> 3) - tid;  // chunk of the token, relative to this lane
+    const int ey = y & 7;
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+    u32x4 prev = u32x4_of(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+        asm volatile("" : "+v"(x[j]) : "v"(prev));
+        const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
+        float d[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            d[2 * q] = mix_lo(wv[q], sc);
+            d[2 * q + 1] = mix_hi(wv[q], sc);
+        }
+        if (cy_rel == j * BLOCK) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e == ey) d[e] = dy;
+        }
+        const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
+                                   pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
+        if (j < SAFE || tid < nfull - j * BLOCK) {
+            store_chunk<BLOCK, SAFE>(out, rd, lane16, j);
+        } else if (tid == nfull - j * BLOCK && nfull != nchunks) {  // partial last chunk
+            const int c = j * BLOCK + tid;
+            const int rem = V & 7;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e < rem)
+                    drow[(c << 3) + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+        }
+        prev = out;
+    }
+    if (tid == 0) write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
 }
 
 // ---------------------------------------------------------------------------
@@ -587,76 +503,45 @@ __global__ __launch_bounds__(kReduceBlock) void loss_reduce_kernel(const float* 
 // ---------------------------------------------------------------------------
 // Host dispatch
 // ---------------------------------------------------------------------------
-using ResidentKernel = void (*)(const uint16_t*, int64_t, int, int64_t, const int32_t*,
-                                const float*, const float*, const float*, const float*, Params,
-                                float*, float*, float*, uint16_t*, int32_t*, unsigned long long*);
-using StreamKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*,
-                              const float*, const float*, const float*, Params, float*, float*,
-                              float*, uint16_t*, int32_t*);
+using RowKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*,
+                           const float*, const float*, const float*, Params, float*, float*,
+                           float*, uint16_t*, int32_t*);
 
 struct RowConfig {
-    ResidentKernel fn;  // nullptr: streaming variant
+    RowKernel fn;
     int block;
-    int ch;
-    int slot;  // index into the occupancy cache
+    int ch;  // 0: streaming variant
 };
 
-#define LEAP_RES(B, C, S, I) RowConfig{grpo_rows_resident<B, C, S>, B, C, I}
-
-constexpr int kNumConfigs = 14;
+#define LEAP_RES(B, C, S) RowConfig{grpo_rows_resident<B, C, S>, B, C}
 
 // Smallest resident configuration whose BLOCK*CH*8 columns cover V.  SAFE of
 // each entry is the CH of the entry before it with the same BLOCK (0 for the
 // first), which is what makes its leading slots provably full.
 RowConfig pick_row_config(int V) {
-    static const RowConfig table[kNumConfigs] = {
-        LEAP_RES(64, 1, 0, 0),      LEAP_RES(64, 2, 1, 1),      LEAP_RES(64, 4, 2, 2),
-        LEAP_RES(64, 8, 4, 3),      LEAP_RES(256, 4, 0, 4),     LEAP_RES(256, 8, 4, 5),
-        LEAP_RES(256, 12, 8, 6),    LEAP_RES(256, 16, 12, 7),   LEAP_RES(1024, 8, 0, 8),
-        LEAP_RES(1024, 12, 8, 9),   LEAP_RES(1024, 16, 12, 10), LEAP_RES(1024, 19, 16, 11),
-        LEAP_RES(1024, 20, 19, 12), LEAP_RES(1024, 24, 20, 13),
+    static const RowConfig table[] = {
+        LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
+        LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
+        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_RES(1024, 8, 0),
+        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_RES(1024, 19, 16),
+        LEAP_RES(1024, 20, 19), LEAP_RES(1024, 24, 20),
     };
     const int64_t nchunks = (static_cast<int64_t>(V) + 7) / 8;
     for (const RowConfig& r : table)
         if (static_cast<int64_t>(r.block) * r.ch >= nchunks) return r;
-    return RowConfig{nullptr, 1024, 0, -1};
+    return RowConfig{grpo_rows_stream<1024>, 1024, 0};
 }
 
 #undef LEAP_RES
-
-// Resident workgroups per device for each configuration: compute units times
-// the workgroups one compute unit holds (queried once per device).
-constexpr int kMaxDevices = 64;
-int g_resident[kMaxDevices][kNumConfigs];
-
-int resident_workgroups(const RowConfig& rc) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
-    int& cached = g_resident[dev][rc.slot];
-    if (cached > 0) return cached;
-    int cus = 0, per_cu = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, rc.fn, rc.block, 0) != hipSuccess)
-        return 0;
-    if (cus < 1) cus = 1;
-    if (per_cu < 1) per_cu = 1;
-    cached = cus * per_cu;
-    return cached;
-}
-
-size_t row_loss_bytes(int64_t N) {
-    const size_t b = static_cast<size_t>(N > 0 ? N : 0) * sizeof(float);
-    return (b + 255) & ~static_cast<size_t>(255);
-}
 
 }  // namespace
 }  // namespace leap
 
 LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
     (void)V;
-    // per-row weighted losses, then the row queue (one 256-byte line)
-    return leap::row_loss_bytes(N) + 256;
+    // one fp32 weighted loss per row, in whole 256-byte lines
+    const size_t b = static_cast<size_t>(N > 0 ? N : 1) * sizeof(float);
+    return (b + 255) & ~static_cast<size_t>(255);
 }
 
 LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
@@ -688,30 +573,16 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
         if (a0 != b0 && a0 < b0 + bytes && b0 < a0 + bytes) return LEAP_ERR_INVALID_ARG;
     }
     if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
-    if ((reinterpret_cast<uintptr_t>(workspace) & 7u) != 0) return LEAP_ERR_MISALIGNED;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
 
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     float* row_loss = static_cast<float*>(workspace);
-    unsigned long long* queue = reinterpret_cast<unsigned long long*>(
-        static_cast<char*>(workspace) + row_loss_bytes(N));
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
-        const uint16_t* lg = static_cast<const uint16_t*>(logits_bf16);
-        uint16_t* dl = static_cast<uint16_t*>(dlogits_bf16);
-        if (rc.fn) {
-            const int res = resident_workgroups(rc);
-            if (res <= 0) return LEAP_ERR_HIP;
-            const int64_t grid = N < res ? N : res;
-            hipLaunchKernelGGL(queue_init_kernel, dim3(1), dim3(1), 0, stream, queue,
-                               static_cast<unsigned long long>(grid));
-            hipLaunchKernelGGL(rc.fn, dim3(static_cast<unsigned>(grid)), dim3(rc.block), 0, stream,
-                               lg, ld, V, N, token_ids, old_logp, ref_logp, adv_tok, w_tok, p,
-                               logp_out, tok_loss_out, row_loss, dl, dev_err, queue);
-        } else {
-            hipLaunchKernelGGL(grpo_rows_stream<1024>, dim3(static_cast<unsigned>(N)), dim3(1024),
-                               0, stream, lg, ld, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
-                               p, logp_out, tok_loss_out, row_loss, dl, dev_err);
-        }
+        hipLaunchKernelGGL(rc.fn, dim3(static_cast<unsigned>(N)), dim3(rc.block), 0, stream,
+                           static_cast<const uint16_t*>(logits_bf16), ld, V, token_ids, old_logp,
+                           ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss,
+                           static_cast<uint16_t*>(dlogits_bf16), dev_err);
         const leap_status st = launch_status();
         if (st != LEAP_OK) return st;
     }

@@ -36,6 +36,7 @@ EXPORTED = (
     "leap_token_advantages",
     "leap_grpo_workspace_size",
     "leap_grpo_logprob_loss_fwd_bwd",
+    "leap_probe_hbm",
 )
 
 
@@ -87,6 +88,8 @@ def lib() -> ctypes.CDLL:
     L.leap_grpo_logprob_loss_fwd_bwd.argtypes = [P, i64, i64, i32, P, P, P, P, P,
                                                  ctypes.POINTER(leap_grpo_params), P, P, P, P,
                                                  P, ctypes.c_size_t, P, P]
+    L.leap_probe_hbm.restype = ctypes.c_int
+    L.leap_probe_hbm.argtypes = [P, P, ctypes.c_size_t, i32, P]
     _lib = L
     return L
 
@@ -206,3 +209,9 @@ def leap_grpo_logprob_loss_fwd_bwd(logits, ld, N, V, token_ids, old_logp, ref_lo
         _ptr(workspace, None, "workspace"), int(ws_bytes), _ptr(dev_err, "int32", "dev_err"),
         _stream(stream))
     _check(st, "leap_grpo_logprob_loss_fwd_bwd")
+
+
+def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:
+    st = lib().leap_probe_hbm(_ptr(src, None, "src"), _ptr(dst, None, "dst"), int(nbytes),
+                              int(mode), _stream(stream))
+    _check(st, "leap_probe_hbm")
