@@ -228,6 +228,26 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
                                            hipStream_t stream);
 
 /*
+ * Forward-only log-probability of each row's token: the old-policy and
+ * reference forward passes whose outputs enter the ratio and the KL term of
+ * the per-token objective (Sec. 3.1, Eq. 3).
+ *
+ *   logp_out[k] = z[y_k] - log sum_v exp(z[v]),  z = inv_temperature * logits[k]
+ *
+ * logits_bf16 [N][ld] bf16, token_ids int32 [N], logp_out float [N].
+ * w_tok float [N], nullable: a row with w_tok[k] == 0 is not read and gets 0.
+ * A token id outside [0, V) or a row of all -inf logits counts in *dev_err
+ * and gets NaN.  Alignment and range rules as leap_grpo_logprob_loss_fwd_bwd;
+ * no workspace.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a non-positive or
+ * non-finite inv_temperature, a required pointer NULL; LEAP_ERR_MISALIGNED.
+ */
+leap_status leap_logprob_fwd(const void *logits_bf16, int64_t ld, int64_t N, int32_t V,
+                             const int32_t *token_ids, const float *w_tok,
+                             float inv_temperature, float *logp_out, int32_t *dev_err,
+                             hipStream_t stream);
+
+/*
  * Measurement helper, not part of the method: streams device memory with the
  * access shape of the fused kernel (16-byte non-temporal accesses) so the
  * achievable HBM rate of each access mix can be set beside the published

@@ -36,6 +36,7 @@ EXPORTED = (
     "leap_token_advantages",
     "leap_grpo_workspace_size",
     "leap_grpo_logprob_loss_fwd_bwd",
+    "leap_logprob_fwd",
     "leap_probe_hbm",
 )
 
@@ -88,6 +89,8 @@ def lib() -> ctypes.CDLL:
     L.leap_grpo_logprob_loss_fwd_bwd.argtypes = [P, i64, i64, i32, P, P, P, P, P,
                                                  ctypes.POINTER(leap_grpo_params), P, P, P, P,
                                                  P, ctypes.c_size_t, P, P]
+    L.leap_logprob_fwd.restype = ctypes.c_int
+    L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P]
     L.leap_probe_hbm.restype = ctypes.c_int
     L.leap_probe_hbm.argtypes = [P, P, ctypes.c_size_t, i32, P]
     _lib = L
@@ -209,6 +212,16 @@ def leap_grpo_logprob_loss_fwd_bwd(logits, ld, N, V, token_ids, old_logp, ref_lo
         _ptr(workspace, None, "workspace"), int(ws_bytes), _ptr(dev_err, "int32", "dev_err"),
         _stream(stream))
     _check(st, "leap_grpo_logprob_loss_fwd_bwd")
+
+
+def leap_logprob_fwd(logits, ld, N, V, token_ids, w_tok, inv_temperature, logp_out, dev_err=None,
+                     stream=None) -> None:
+    st = lib().leap_logprob_fwd(
+        _ptr(logits, "bfloat16", "logits"), int(ld), int(N), int(V),
+        _ptr(token_ids, "int32", "token_ids"), _ptr(w_tok, "float32", "w_tok"),
+        float(inv_temperature), _ptr(logp_out, "float32", "logp_out"),
+        _ptr(dev_err, "int32", "dev_err"), _stream(stream))
+    _check(st, "leap_logprob_fwd")
 
 
 def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:

@@ -179,3 +179,33 @@ def test_binding_refuses_cpu_tensors():
         L._ptr(torch.zeros(4, dtype=torch.int32), "int32", "x")
     with pytest.raises(TypeError):
         L._ptr(torch.zeros(4, dtype=torch.float32), "int32", "x")
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=-1), L.LEAP_ERR_INVALID_ARG),
+    (dict(V=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(ld=999), L.LEAP_ERR_INVALID_ARG),
+    (dict(inv_temperature=0.0), L.LEAP_ERR_INVALID_ARG),
+    (dict(inv_temperature=float("nan")), L.LEAP_ERR_INVALID_ARG),
+    (dict(token_ids=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(logp_out=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(logits=FAKE + 8), L.LEAP_ERR_MISALIGNED),
+    (dict(ld=1012), L.LEAP_ERR_MISALIGNED),
+])
+def test_logprob_fwd_rejects(kw, status):
+    a = dict(logits=FAKE, ld=1024, N=8, V=1000, token_ids=FAKE, w_tok=None, inv_temperature=1.0,
+             logp_out=FAKE, dev_err=None, stream=0)
+    a.update(kw)
+    with pytest.raises(L.LeapError) as e:
+        L.leap_logprob_fwd(**a)
+    assert e.value.status == status
+
+
+def test_probe_rejects():
+    with pytest.raises(L.LeapError):
+        L.leap_probe_hbm(FAKE, FAKE, 15, 0, stream=0)
+    with pytest.raises(L.LeapError):
+        L.leap_probe_hbm(FAKE, FAKE, 16, 3, stream=0)
+    with pytest.raises(L.LeapError) as e:
+        L.leap_probe_hbm(FAKE + 4, FAKE, 16, 0, stream=0)
+    assert e.value.status == L.LEAP_ERR_MISALIGNED

@@ -1,0 +1,69 @@
+"""GPU parity of the forward-only log-probability entry point against the
+oracle's log-softmax (log-probs within 2e-3 absolute)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests import _gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(16, 16, 64), (1000, 1008, 64), (4093, 4096, 32), (32768, 32768, 64),
+          (65536, 65536, 16), (151936, 151936, 64), (196608, 196608, 8), (200003, 200008, 8)]
+
+
+def _run(lg_dev, V, tok, w=None, inv_temp=1.0):
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N, ld = lg_dev.shape
+    out = torch.full((max(N, 1),), float("inf"), dtype=torch.float32, device=U.dev())
+    err = U.zeros_i32(1)
+    L.leap_logprob_fwd(lg_dev, ld, N, V, U.T(np.asarray(tok, np.int32)),
+                       None if w is None else U.T(np.asarray(w, np.float32)), inv_temp, out, err)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()[:N], int(err.item())
+
+
+@pytest.mark.parametrize("V,ld,N", SHAPES, ids=[f"V{s[0]}" for s in SHAPES])
+@pytest.mark.parametrize("inv_temp", [1.0, 0.75])
+def test_logprob_fwd_shapes(V, ld, N, inv_temp):
+    lg = wl.logits_host(V + 1, N, V, ld)
+    tok = wl.sample_tokens_host(lg, V, V + 1)
+    tok[0] = V - 1
+    U.log(f"logprob_fwd V={V} T^-1={inv_temp}")
+    got, err = _run(U.bf16_device(lg), V, tok, inv_temp=inv_temp)
+    want, bad = oracle.logprob_rows(lg, tok, V=V, inv_temp=inv_temp)
+    assert err == bad == 0
+    assert np.max(np.abs(got - want)) < 2e-3
+
+
+def test_logprob_fwd_mask_and_errors():
+    N, V = 12, 3000
+    lg = wl.logits_host(3, N, V)
+    tok = wl.sample_tokens_host(lg, V, 3)
+    lg[2, :] = 0xFF80  # all -inf
+    lg[3, ::4] = 0xFF80
+    tok[3] = 1
+    tok[4] = V  # out of range
+    w = np.ones(N, np.float32)
+    w[5] = 0.0  # not read, 0
+    got, err = _run(U.bf16_device(lg), V, tok, w=w)
+    safe = np.where(tok < V, tok, 0)
+    want, _ = oracle.logprob_rows(lg, safe, V=V)
+    assert err == 2
+    assert np.isnan(got[2]) and np.isnan(got[4]) and got[5] == 0.0
+    ok = np.ones(N, bool)
+    ok[[2, 4, 5]] = False
+    assert np.max(np.abs(got[ok] - want[ok])) < 2e-3
+
+
+def test_logprob_fwd_matches_fused_kernel_logp():
+    """The forward-only entry and the fused objective agree on log-probs
+    (same rounding path up to the fp16 repacking, which logp does not use)."""
+    N, V = 128, 151936
+    lg, tok, old, ref = U.make_inputs_host(21, N, V)
+    w = np.ones(N, np.float32)
+    fused = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, np.zeros(N, np.float32), w)
+    fwd, _ = _run(U.bf16_device(lg), V, tok)
+    assert np.max(np.abs(fwd - fused["logp"])) < 1e-5
