@@ -17,6 +17,8 @@ over ctypes with numpy arrays.  Functions and the passages they follow:
 * ``grpo_rows``        -- Sec. 3.1 Eq. 3 per token: log-softmax, ratio,
   clipped surrogate, reference KL, loss and dlogits.
 * ``logprob_rows``     -- forward-only log-probabilities (old / reference).
+* ``lmhead``           -- the same per-token objective on logits z = H W^T
+  (fused LM head), with dH = dZ W and dW = dZ^T H.
 """
 from __future__ import annotations
 
@@ -191,6 +193,54 @@ def logprob_rows(logits_bf16, token_ids, V=None, inv_temp=1.0):
     out = np.empty(N, np.float64)
     bad = lib.leap_oracle_logprob_rows_bf16(_p(lg), ld, N, V, _p(tok), float(inv_temp), _p(out))
     return out, int(bad)
+
+
+def _bf16_to_f64(a):
+    """bf16 bit patterns (uint16) -> exact float64; float64 arrays pass through."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert a.dtype == np.float64
+    return a
+
+
+def lmhead(hidden, weight, token_ids, old_logp, ref_logp, adv, w, eps_lo=0.2, eps_hi=0.2,
+           kl_coef=0.01, kl_type=KL_K3, inv_temp=1.0, rows=None, want_grads=True,
+           v_block=8192):
+    """Fused LM head: the per-token objective of ``grpo_rows`` (Sec. 3.1, Eq. 3
+    per token) on logits z = H W^T, and its gradients.
+
+    ``hidden`` [N, H] and ``weight`` [V, H] are float64 arrays or bf16 bit
+    patterns (uint16, converted exactly).  Z = H W^T is a float64 matrix
+    product (formed in blocks of ``v_block`` vocabulary rows); ``grpo_rows``
+    on Z gives logp, tok_loss, loss and dZ = d(sum_k w_k loss_k)/dZ; then
+    dH = dZ W and dW = dZ^T H.  ``rows`` evaluates only those rows (outputs in
+    its order, loss summed over them, dH for them); dW sums over every row and
+    is None then.  Returns dict: logp, tok_loss, loss, dH, dW, bad.
+    """
+    Hm = _bf16_to_f64(hidden)
+    Wm = _bf16_to_f64(weight)
+    assert Hm.ndim == 2 and Wm.ndim == 2 and Hm.shape[1] == Wm.shape[1]
+    V = Wm.shape[0]
+    sel = np.arange(Hm.shape[0]) if rows is None else np.asarray(rows, np.int64)
+    Hs = Hm[sel]
+    Z = np.empty((sel.size, V), np.float64)
+    for v0 in range(0, V, v_block):
+        Z[:, v0:v0 + v_block] = Hs @ Wm[v0:v0 + v_block].T
+    pick = lambda a: np.asarray(a)[sel]  # noqa: E731
+    r = grpo_rows(Z, pick(token_ids), pick(old_logp), pick(ref_logp), pick(adv), pick(w), V=V,
+                  eps_lo=eps_lo, eps_hi=eps_hi, kl_coef=kl_coef, kl_type=kl_type,
+                  inv_temp=inv_temp, want_dlogits=want_grads)
+    dH = dW = None
+    if want_grads:
+        dZ = r["dlogits"]
+        dH = np.zeros_like(Hs)
+        for v0 in range(0, V, v_block):
+            dH += dZ[:, v0:v0 + v_block] @ Wm[v0:v0 + v_block]
+        if rows is None:
+            dW = dZ.T @ Hm
+    return {"logp": r["logp"], "tok_loss": r["tok_loss"], "loss": r["loss"], "dH": dH, "dW": dW,
+            "bad": r["bad"]}
 
 
 def tau_from_pass_rate(G: int, lo: Fraction, lo_strict: bool, hi: Fraction, hi_strict: bool):

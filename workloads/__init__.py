@@ -55,6 +55,8 @@ LOGIT_SIGMA = 2.0
 OLD_SIGMA = 0.05
 REF_SIGMA = 0.1
 CLIP_CASE_OLD_SIGMA = 0.3
+LM_HIDDEN_SIGMA = 1.0
+LM_WEIGHT_SIGMA = 0.02
 
 
 @dataclass
@@ -299,6 +301,43 @@ def sample_tokens_device(logits, V: int, seed: int):
         gum = -torch.log(-torch.log(u))
         out[r0:r1] = torch.argmax(logits[r0:r1, :V].float() + gum, dim=1).to(torch.int32)
     return out
+
+
+def lmhead_operands_device(seed: int, N: int, V: int, H: int, device,
+                           hidden_sigma: float = LM_HIDDEN_SIGMA,
+                           weight_sigma: float = LM_WEIGHT_SIGMA):
+    """bf16 torch tensors hidden [N, H] ~ N(0, hidden_sigma^2) and weight
+    [V, H] ~ N(0, weight_sigma^2), drawn on the device."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 7919 + 11)
+    hid = torch.empty((N, H), dtype=torch.bfloat16, device=device)
+    wt = torch.empty((V, H), dtype=torch.bfloat16, device=device)
+    chunk = max(1, (1 << 26) // max(H, 1))
+    for r0 in range(0, N, chunk):
+        r1 = min(N, r0 + chunk)
+        hid[r0:r1] = (torch.randn((r1 - r0, H), generator=g, device=device) * hidden_sigma).to(torch.bfloat16)
+    for r0 in range(0, V, chunk):
+        r1 = min(V, r0 + chunk)
+        wt[r0:r1] = (torch.randn((r1 - r0, H), generator=g, device=device) * weight_sigma).to(torch.bfloat16)
+    return hid, wt
+
+
+def lmhead_tokens_device(hidden, weight, seed: int, row_chunk: int = 256):
+    """Gumbel-max draws y_k ~ softmax(hidden_k weight^T), the logits formed in
+    fp32 a block of rows at a time (generation only).  int32 tensor [N]."""
+    import torch
+    N = hidden.shape[0]
+    g = torch.Generator(device=hidden.device)
+    g.manual_seed(int(seed) * 7919 + 12)
+    y = torch.empty(N, dtype=torch.int32, device=hidden.device)
+    wf = weight.float()
+    for r0 in range(0, N, row_chunk):
+        r1 = min(N, r0 + row_chunk)
+        z = hidden[r0:r1].float() @ wf.T
+        u = torch.rand(z.shape, generator=g, device=z.device).clamp_(min=1e-38)
+        y[r0:r1] = torch.argmax(z - torch.log(-torch.log(u)), dim=1).to(torch.int32)
+    return y
 
 
 def logp_noise(seed: int, N: int, old_sigma: float = OLD_SIGMA,
