@@ -32,7 +32,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k4_grpo_rows_traffic.json")
-K4_SOURCE = os.path.join(ROOT, "paper_2608_01804_amd", "csrc", "grpo_loss.hip")
+# The fused row kernel's translation unit: the source and every header it includes.
+K4_SOURCES = [os.path.join(ROOT, "paper_2608_01804_amd", "csrc", f)
+              for f in ("grpo_loss.hip", "row_common.h", "objective.h", "leap_common.h")]
 
 
 def log(*a):
@@ -40,7 +42,10 @@ def log(*a):
 
 
 def k4_source_hash() -> str:
-    return hashlib.sha256(open(K4_SOURCE, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in K4_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def row_bytes(V: int, valid: bool) -> int:
@@ -223,6 +228,105 @@ def cpu_baseline(s, seconds: float):
                       f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens"}
 
 
+MFMA_BF16_PEAK = 2.5e15  # MI355X dense bf16 matrix-core peak, flop/s
+
+
+def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
+    """fp32 log-softmax of hidden weight^T at y with torch, a block of rows at
+    a time: input preparation for the old / reference log-probabilities."""
+    out = torch.empty(hidden.shape[0], dtype=torch.float32, device=hidden.device)
+    wf = weight.float()
+    yl = y.long()
+    for r0 in range(0, hidden.shape[0], row_chunk):
+        r1 = min(hidden.shape[0], r0 + row_chunk)
+        z = hidden[r0:r1].float() @ wf.T
+        out[r0:r1] = torch.log_softmax(z, dim=1).gather(1, yl[r0:r1, None])[:, 0]
+    del wf
+    return out
+
+
+def lmhead_leg(L, torch, dev, seed: int, reps: int):
+    """The fused LM-head variant on one 16384-row microbatch of the LM-head
+    workload (hidden [16384 x 4096] ~ N(0,1), weight [151936 x 4096] ~
+    N(0, 0.02^2), bf16): side arrays from the step's own rank and token
+    advantages, forward + dhidden + dweight per call, HIP events around each
+    call on the stream it runs on."""
+    import workloads as wl
+    lat = wl.draw_latent("lmhead")
+    cfg = lat.cfg
+    G, M, V, H, R = lat.G, lat.M, cfg["V"], cfg["H"], cfg["rows_per_mb"]
+    tmin, tmax = L.leap_dcp_tau_from_pass_rate(G, 0, 1, 1, 3, 4, 1)
+    ftp = torch.from_numpy(lat.first_turn_pass).to(dev)
+    gate = torch.empty(lat.n_groups, dtype=torch.uint8, device=dev)
+    L.leap_dcp_gate(ftp, lat.n_groups, G, tmin, tmax, None, gate)
+    ro = wl.realize(lat, gate.cpu().numpy())
+    mb = wl.pack(ro, R)[0]
+    n = ro.n_rollouts
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    reward = torch.empty(n, dtype=torch.float32, device=dev)
+    adv_roll = torch.empty(n, dtype=torch.float32, device=dev)
+    L.leap_rank_advantages(torch.from_numpy(ro.pass_turn).to(dev), None, None, n // G, G, M,
+                           L.LEAP_KEY_TURN, L.LEAP_ADV_STD, 1e-6, None, None, None, reward,
+                           adv_roll, err)
+    adv_tok = torch.empty(R, dtype=torch.float32, device=dev)
+    w_tok = torch.empty(R, dtype=torch.float32, device=dev)
+    L.leap_token_advantages(adv_roll, torch.from_numpy(mb.tok_rollout).to(dev),
+                            torch.from_numpy(mb.tok_turn).to(dev),
+                            torch.from_numpy(ro.n_turns).to(dev),
+                            torch.from_numpy(ro.n_tokens).to(dev), n, R, cfg["gamma"],
+                            L.LEAP_AGG_SEQ_MEAN_TOKEN_MEAN, float(n), adv_tok, w_tok, err)
+    hid, wt = wl.lmhead_operands_device(seed, R, V, H, dev)
+    y = wl.lmhead_tokens_device(hid, wt, seed)
+    cur = _token_logp_torch(torch, hid, wt, y)
+    n_old, n_ref = wl.logp_noise(seed, R)
+    old = cur + torch.from_numpy(n_old.astype(np.float32)).to(dev)
+    ref = cur + torch.from_numpy(n_ref.astype(np.float32)).to(dev)
+    logp = torch.empty(R, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dH = torch.empty((R, H), dtype=torch.float32, device=dev)
+    dW = torch.empty((V, H), dtype=torch.float32, device=dev)
+    ws_bytes = L.leap_lmhead_workspace_size(R, V, H)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+
+    def call():
+        L.leap_grpo_lmhead_fwd_bwd(hid, wt, R, V, H, y, old, ref, adv_tok, w_tok, p, logp, None,
+                                   loss, dH, dW, 0, ws, ws_bytes, err)
+
+    call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ms = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    assert int(err.item()) == 0, "data errors reported by the kernels"
+    assert bool(torch.isfinite(loss).item())
+    t = float(np.median(ms)) / 1e3
+    v_pad = (V + 255) // 256 * 256
+    n_pad = (R + 255) // 256 * 256
+    useful = 6.0 * R * H * V
+    executed = 8.0 * n_pad * H * v_pad
+    log(f"[bench] lmhead {R}x{V}x{H}: {t * 1e3:.2f} ms/call (median of {reps}); "
+        f"{useful / t / 1e12:.0f} TFLOP/s useful, {executed / t / 1e12:.0f} executed")
+    return {"workload": f"fused LM head, one microbatch: hidden [{R} x {H}] ~ N(0,1), weight "
+                        f"[{V} x {H}] ~ N(0,0.02^2), bf16; forward, dhidden and dweight (fp32)",
+            "ms_per_call": t * 1e3, "calls": reps, "rows_per_s": R / t,
+            "tokens_per_s": mb.n_valid / t, "generated_tokens": int(mb.n_valid),
+            "roofline": {"bound": "mfma", "achieved": useful / t / 1e12,
+                         "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                         "frac": useful / t / MFMA_BF16_PEAK, "traffic": None,
+                         "kernel": "one leap_grpo_lmhead_fwd_bwd call (4 GEMM passes)",
+                         "flops_per_call_useful": useful, "flops_per_call_executed": executed,
+                         "executed_TFLOPs": executed / t / 1e12,
+                         "executed_frac": executed / t / MFMA_BF16_PEAK}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,6 +336,10 @@ def main():
     ap.add_argument("--seed", type=int, default=1002)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lmhead-reps", type=int, default=5,
+                    help="timed calls of the fused LM-head variant (0 skips it)")
+    ap.add_argument("--lmhead-only", action="store_true",
+                    help="run only the fused LM-head leg and print its JSON object")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -247,6 +355,11 @@ def main():
     torch.cuda.set_device(dev)
     if args.workload == "full":
         raise SystemExit("the full workload does not fit resident; bench runs 'mid'")
+
+    if args.lmhead_only:
+        print(json.dumps({"lmhead": lmhead_leg(L, torch, dev, 1005, max(1, args.lmhead_reps))}),
+              flush=True)
+        return
 
     probe = hbm_probe(L, torch, dev)
     log(f"[bench] HBM probe: " + ", ".join(f"{k} {v:.0f}" for k, v in probe.items()))
@@ -293,6 +406,13 @@ def main():
         log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
         cpu = cpu_baseline(s, args.cpu_seconds)
 
+    meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
+    lm = None
+    if args.lmhead_reps > 0:
+        del s
+        torch.cuda.empty_cache()
+        lm = lmhead_leg(L, torch, dev, 1005, args.lmhead_reps)
+
     out = {
         "metric": "rollout tokens/sec for fused GRPO logprob+loss+dlogits; % of HBM roofline",
         "value": value,
@@ -307,9 +427,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: 16 prompts x G=16, up to 2 turns, "
-                               f"U[256,1024] tokens/turn, V={V}, {s['n_mb']} microbatches x {R} rows",
-                   "generated_tokens_per_step": n_valid, "rows_per_step": s["rows"],
-                   "vocab": V, "microbatch_rows": R, "G": s["G"], "max_turns": s["M"]},
+                               f"U[256,1024] tokens/turn, V={V}, {meta['n_mb']} microbatches x {R} rows",
+                   "generated_tokens_per_step": n_valid, "rows_per_step": meta["rows"],
+                   "vocab": V, "microbatch_rows": R, "G": meta["G"], "max_turns": meta["M"]},
         "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": traffic,
                      "kernel": "grpo_rows_resident<1024,19> + loss_reduce (one fused call)",
@@ -317,6 +437,7 @@ def main():
                      "probe_GBps": probe,
                      "frac_of_probe_copy": achieved / 1e9 / probe["copy_GBps"]},
         "cpu_baseline": cpu,
+        "lmhead": lm,
     }
     print(json.dumps(out), flush=True)
 

@@ -247,6 +247,54 @@ leap_status leap_logprob_fwd(const void *logits_bf16, int64_t ld, int64_t N, int
                              float inv_temperature, float *logp_out, int32_t *dev_err,
                              hipStream_t stream);
 
+/* Workspace bytes leap_grpo_lmhead_fwd_bwd needs (0 for invalid sizes). */
+size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
+
+/*
+ * Fused LM head + per-token GRPO objective (Sec. 3.1, Eq. 3, per token):
+ * the same per-row objective as leap_grpo_logprob_loss_fwd_bwd, on logits
+ * z = hidden * weight^T formed tile by tile on the matrix cores and never
+ * written to memory, plus the gradients of L = sum_k w_k * loss_k:
+ *
+ *   dZ[k][v]   = g_k * ([v == y_k] - softmax(inv_temperature * z_k)[v])
+ *   dhidden    = dZ * weight          [N][H]
+ *   dweight    = dZ^T * hidden        [V][H]
+ *
+ * Products accumulate in fp32 from bf16 operands; dZ is rounded to bf16
+ * (RNE) before the two gradient products.  logp, tok_loss, loss and g follow
+ * the rules of leap_grpo_logprob_loss_fwd_bwd, including excluded rows
+ * (w == 0: zero gradient rows, logp_out = tok_loss_out = 0) and bad token
+ * ids (counted in *dev_err, excluded).
+ *
+ * hidden_bf16 [N][H] bf16, weight_bf16 [V][H] bf16, both row-major, 16-byte
+ *              aligned.  H % 32 == 0 (else LEAP_ERR_UNSUPPORTED).
+ * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
+ * logp_out, tok_loss_out  float [N], nullable.  loss_out float [1], required.
+ * dhidden    float [N][H], overwritten; NULL skips it.
+ * dweight    float [V][H]; overwritten (accumulate_dweight = 0) or added to
+ *            (accumulate_dweight = 1); NULL skips it.  With both gradients
+ *            NULL only the forward outputs are computed.
+ * workspace  device buffer of >= leap_lmhead_workspace_size(N, V, H) bytes,
+ *            16-byte aligned, scratch for this call only (calls sharing one
+ *            workspace must be ordered on one stream).  It holds the
+ *            transposed operands, per-tile row statistics and one vocabulary
+ *            chunk of dZ in both layouts.
+ * Limits: each operand and workspace matrix below 4 GiB (32-bit offsets in
+ * the GEMM core; for H = 4096 that allows V up to about 500000 and N up to
+ * about 500000); otherwise LEAP_ERR_UNSUPPORTED.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, H < 1, accumulate_dweight
+ * not 0 or 1, a parameter out of range, a required pointer NULL;
+ * LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE; LEAP_ERR_UNSUPPORTED.
+ */
+leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight_bf16, int64_t N,
+                                     int32_t V, int32_t H, const int32_t *token_ids,
+                                     const float *old_logp, const float *ref_logp,
+                                     const float *adv_tok, const float *w_tok,
+                                     const leap_grpo_params *params, float *logp_out,
+                                     float *tok_loss_out, float *loss_out, float *dhidden,
+                                     float *dweight, int32_t accumulate_dweight, void *workspace,
+                                     size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
+
 /*
  * Measurement helper, not part of the method: streams device memory with the
  * access shape of the fused kernel (16-byte non-temporal accesses) so the

@@ -216,7 +216,7 @@ def lmhead(hidden, weight, token_ids, old_logp, ref_logp, adv, w, eps_lo=0.2, ep
     on Z gives logp, tok_loss, loss and dZ = d(sum_k w_k loss_k)/dZ; then
     dH = dZ W and dW = dZ^T H.  ``rows`` evaluates only those rows (outputs in
     its order, loss summed over them, dH for them); dW sums over every row and
-    is None then.  Returns dict: logp, tok_loss, loss, dH, dW, bad.
+    is None then.  Returns dict: logp, tok_loss, loss, dZ, dH, dW, bad.
     """
     Hm = _bf16_to_f64(hidden)
     Wm = _bf16_to_f64(weight)
@@ -231,7 +231,7 @@ def lmhead(hidden, weight, token_ids, old_logp, ref_logp, adv, w, eps_lo=0.2, ep
     r = grpo_rows(Z, pick(token_ids), pick(old_logp), pick(ref_logp), pick(adv), pick(w), V=V,
                   eps_lo=eps_lo, eps_hi=eps_hi, kl_coef=kl_coef, kl_type=kl_type,
                   inv_temp=inv_temp, want_dlogits=want_grads)
-    dH = dW = None
+    dZ = dH = dW = None
     if want_grads:
         dZ = r["dlogits"]
         dH = np.zeros_like(Hs)
@@ -239,8 +239,8 @@ def lmhead(hidden, weight, token_ids, old_logp, ref_logp, adv, w, eps_lo=0.2, ep
             dH += dZ[:, v0:v0 + v_block] @ Wm[v0:v0 + v_block]
         if rows is None:
             dW = dZ.T @ Hm
-    return {"logp": r["logp"], "tok_loss": r["tok_loss"], "loss": r["loss"], "dH": dH, "dW": dW,
-            "bad": r["bad"]}
+    return {"logp": r["logp"], "tok_loss": r["tok_loss"], "loss": r["loss"], "dZ": dZ, "dH": dH,
+            "dW": dW, "bad": r["bad"]}
 
 
 def tau_from_pass_rate(G: int, lo: Fraction, lo_strict: bool, hi: Fraction, hi_strict: bool):

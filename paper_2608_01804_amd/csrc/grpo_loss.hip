@@ -28,53 +28,14 @@
 //  * Larger vocabularies use a streaming variant that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
 // kernel sums them in a fixed order (bitwise reproducible).
+#include "objective.h"
 #include "row_common.h"
 
 namespace leap {
 namespace {
 
 using namespace row;
-
-// Per-token scalar epilogue.  lse2 = log2 sum_v 2^(x_v * c).
-struct RowOut {
-    float logp, loss, g, lse2;
-};
-
-// Hardware exp2 / log2 (v_exp_f32, v_log_f32, about 1 ulp): no polynomial
-// constants, which would otherwise be hoisted into registers in the
-// persistent row loop.
-__device__ __forceinline__ float hw_exp(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
-
-__device__ __forceinline__ RowOut row_epilogue(float lse2, float xy, float old_lp, float ref_lp,
-                                               float A, float w, const Params& p) {
-    RowOut o;
-    const float lse = lse2 * kLn2;
-    const float logp = p.inv_temp * xy - lse;
-    const float rho = hw_exp(logp - old_lp);
-    const float clipped = fminf(fmaxf(rho, 1.0f - p.eps_lo), 1.0f + p.eps_hi);
-    const float surr = fminf(rho * A, clipped * A);
-    float kl, dkl;
-    if (p.kl_type == LEAP_KL_K1) {
-        kl = logp - ref_lp;
-        dkl = 1.0f;
-    } else if (p.kl_type == LEAP_KL_K2) {
-        const float dd = logp - ref_lp;
-        kl = 0.5f * dd * dd;
-        dkl = dd;
-    } else {
-        const float dd = ref_lp - logp;
-        const float em1 = hw_exp(dd) - 1.0f;
-        kl = em1 - dd;
-        dkl = -em1;
-    }
-    const bool active = (A > 0.0f && rho <= 1.0f + p.eps_hi) || (A < 0.0f && rho >= 1.0f - p.eps_lo);
-    const float dl = (active ? -A * rho : 0.0f) + p.kl_coef * dkl;
-    o.logp = logp;
-    o.loss = -surr + p.kl_coef * kl;
-    o.g = w * dl * p.inv_temp;
-    o.lse2 = lse2;
-    return o;
-}
+using namespace obj;
 
 // Zero the dlogits row of an excluded token.
 template <int BLOCK>
@@ -83,14 +44,6 @@ __device__ __forceinline__ void zero_row(uint16_t* drow, int V, int tid) {
     u32x4* d4 = reinterpret_cast<u32x4*>(drow);
     for (int c = tid; c < nfull; c += BLOCK) d4[c] = u32x4_of(0u, 0u, 0u, 0u);
     for (int e = (nfull << 3) + tid; e < V; e += BLOCK) drow[e] = 0;
-}
-
-__device__ __forceinline__ void write_row_outputs(int64_t row, float logp, float loss, float w,
-                                                  float* logp_out, float* tok_loss_out,
-                                                  float* row_loss) {
-    if (logp_out) logp_out[row] = logp;
-    if (tok_loss_out) tok_loss_out[row] = loss;
-    row_loss[row] = w * loss;
 }
 
 template <int BLOCK, int CH, int SAFE>
@@ -302,25 +255,6 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
         }
     }
     if (tid == 0) write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
-}
-
-// Fixed-order sum of the per-row weighted losses (one workgroup).
-constexpr int kReduceBlock = 1024;
-
-__global__ __launch_bounds__(kReduceBlock) void loss_reduce_kernel(const float* __restrict__ row_loss,
-                                                                   int64_t N, float* __restrict__ loss_out) {
-    __shared__ double s_w[kReduceBlock / kWave];
-    const int tid = threadIdx.x;
-    double acc = 0.0;
-    for (int64_t k = tid; k < N; k += kReduceBlock) acc += static_cast<double>(row_loss[k]);
-    acc = wave_sum_f64(acc);
-    if ((tid & (kWave - 1)) == 0) s_w[tid / kWave] = acc;
-    __syncthreads();
-    if (tid == 0) {
-        double t = 0.0;
-        for (int w = 0; w < kReduceBlock / kWave; ++w) t += s_w[w];
-        loss_out[0] = static_cast<float>(t);
-    }
 }
 
 // ---------------------------------------------------------------------------

@@ -1,0 +1,594 @@
+// Fused LM head + per-token GRPO objective: the objective of Sec. 3.1 (Eq. 3
+// per token: log-softmax at the rollout token, clipped importance ratio,
+// reference KL) on logits z = H W^T that are never written to HBM, with the
+// gradients dH = dZ W and dW = dZ^T H, where dZ = d(sum_k w_k l_k)/dz.
+//
+// Steps of one call, all on the caller's stream:
+//  1. H and W are transposed once into the workspace (Ht [H][N_pad], Wt
+//     [H][V_pad], zero padded), because every GEMM below runs on one NT core
+//     whose operands are both contiguous along the contraction index.
+//  2. Stats GEMM  Z = H W^T on MFMA.  Its epilogue turns every row of a
+//     256 x 256 tile into a partial (max, sum 2^(z c - max)) in base-2 units
+//     (c = log2(e) / T) and picks out the rollout token's logit.
+//  3. Combine: one wave per row merges the row's partials in a fixed order
+//     into the log-sum-exp and evaluates the same per-token objective as the
+//     logits-resident kernel (log-prob, ratio, surrogate, KL, loss and
+//     g = w dloss/dlogp / T).  A fixed-order reduction sums the loss.
+//  4. Per vocabulary chunk of up to 8192 columns: the Z tiles are recomputed
+//     and the epilogue writes dZ = g (onehot - p) in bf16, row-major
+//     [N_pad][chunk] and transposed [chunk][N_pad]; then dW[chunk] = dZ^T H
+//     and dH (+)= dZ W[chunk] run as two more GEMMs with fp32 epilogues.
+// Executed work is 8 N H V flops (the forward GEMM is recomputed once).
+#include "mfma_gemm.h"
+#include "row_common.h"
+
+namespace leap {
+namespace {
+
+using gemm::acc_row;
+using gemm::f32x16;
+using gemm::Tile;
+using obj::Params;
+using obj::RowOut;
+using row::ms_merge;
+using row::pack_bf16;
+using row::row_live;
+using row::u32x4;
+using row::wave_ms_reduce;
+
+constexpr int kChunkCols = 8192;  // vocabulary columns per backward chunk
+constexpr int kTile = gemm::kBM;  // 256: rows and columns of a GEMM tile
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------------------
+// Transpose with zero padding: dst[c][r] = src[r][c] for r < R, and 0 for
+// R <= r < ld_dst, for every c < C.  64 x 64 tiles through LDS; C % 8 == 0.
+// ---------------------------------------------------------------------------
+constexpr int kTr = 64;
+
+__global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src,
+                                                            int64_t R, int C, int64_t ld_src,
+                                                            uint16_t* __restrict__ dst,
+                                                            int64_t ld_dst) {
+    __shared__ uint32_t t[kTr][kTr / 2 + 1];  // row r of the tile: 64 bf16 packed in pairs
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTr;
+    const int c0 = blockIdx.y * kTr;
+    const int tid = threadIdx.x;
+    {
+        const int rr = tid >> 2, cc = (tid & 3) * 16;
+        const int64_t r = r0 + rr;
+        u32x4 a = {0u, 0u, 0u, 0u}, b = {0u, 0u, 0u, 0u};
+        if (r < R) {
+            const uint16_t* p = src + r * ld_src + c0 + cc;
+            if (c0 + cc < C) a = *reinterpret_cast<const u32x4*>(p);
+            if (c0 + cc + 8 < C) b = *reinterpret_cast<const u32x4*>(p + 8);
+        }
+        uint32_t* d = &t[rr][cc / 2];
+        d[0] = a.x, d[1] = a.y, d[2] = a.z, d[3] = a.w;
+        d[4] = b.x, d[5] = b.y, d[6] = b.z, d[7] = b.w;
+    }
+    __syncthreads();
+    const int cc = tid >> 2, rr = (tid & 3) * 16;
+    if (c0 + cc >= C) return;
+    uint32_t w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t lo = t[rr + 2 * e][cc >> 1], hi = t[rr + 2 * e + 1][cc >> 1];
+        w[e] = (cc & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    uint16_t* q = dst + static_cast<int64_t>(c0 + cc) * ld_dst + r0 + rr;
+    *reinterpret_cast<u32x4*>(q) = u32x4{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4*>(q + 8) = u32x4{w[4], w[5], w[6], w[7]};
+}
+
+__global__ __launch_bounds__(256) void fill_zero_f32_kernel(float* __restrict__ p, int64_t n) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
+        p[i] = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Stats epilogue.  Accumulator register r of lane l in 32 x 32 block (i, j)
+// of a wave holds row i*32 + acc_row(r, l), column j*32 + l%32, so the 32
+// lanes of each half-wave share 16 rows per block i.  Each lane first folds
+// its 4 columns, then the half-wave does a reduce-scatter: at every step a
+// lane keeps half of its (max, sum) pairs, sends the other half to its
+// partner and merges what it receives, so after xor 16, 8, 4, 2 and a final
+// xor 1 exchange every lane pair holds one row's pair over 128 columns.
+// The two waves covering the same rows merge through LDS.
+// ---------------------------------------------------------------------------
+template <int HALF>
+__device__ __forceinline__ void scatter_step(float (&m)[16], float (&s)[16], int lane, int b) {
+    const bool up = (lane & b) != 0;
+#pragma unroll
+    for (int k = 0; k < HALF; ++k) {
+        const float sm = up ? m[k] : m[k + HALF];
+        const float ss = up ? s[k] : s[k + HALF];
+        float km = up ? m[k + HALF] : m[k];
+        float ks = up ? s[k + HALF] : s[k];
+        const float rm = __shfl_xor(sm, b, kWave);
+        const float rs = __shfl_xor(ss, b, kWave);
+        ms_merge(km, ks, rm, rs);
+        m[k] = km;
+        s[k] = ks;
+    }
+}
+
+struct StatsEpi {
+    const int32_t* token_ids;
+    float2* part;  // [N][tiles_v] (max, sum) in base-2 units
+    float* zy;     // [N] logit of the rollout token (unscaled)
+    int64_t N;
+    int V, tiles_v;
+    float c2;  // log2(e) / T
+
+    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t* smem) const {
+        int* s_y = reinterpret_cast<int*>(smem);
+        float2* s_ms = reinterpret_cast<float2*>(smem + kTile * sizeof(int));
+        const int tid = threadIdx.x;
+        const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
+        {
+            const int64_t r = row0 + tid;
+            const int y = r < N ? token_ids[r] : -1;
+            s_y[tid] = (y >= 0 && y < V) ? y : -1;
+        }
+        __syncthreads();
+        const int lane = t.lane, l32 = lane & 31;
+        const int col0 = t.col0();
+        bool colok[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) colok[j] = col0 + j * 32 + l32 < V;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float m[16], s[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float z[4];
+                float mx = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    z[j] = colok[j] ? acc[i][j][r] * c2 : -INFINITY;
+                    mx = fmaxf(mx, z[j]);
+                }
+                float sum = 0.0f;
+                if (mx != -INFINITY) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) sum += __builtin_amdgcn_exp2f(z[j] - mx);
+                }
+                m[r] = mx;
+                s[r] = sum;
+            }
+            // The token's logit: exactly one lane of the grid holds each row's.
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rw = t.wm * 128 + i * 32 + acc_row(r, lane);
+                const int y = s_y[rw];
+                const int rel = y - col0;
+                if (y >= 0 && rel >= 0 && rel < 128 && (rel & 31) == l32) {
+                    const int jj = rel >> 5;
+                    float v = acc[i][0][r];
+                    v = jj == 1 ? acc[i][1][r] : v;
+                    v = jj == 2 ? acc[i][2][r] : v;
+                    v = jj == 3 ? acc[i][3][r] : v;
+                    zy[row0 + rw] = v;
+                }
+            }
+            scatter_step<8>(m, s, lane, 16);
+            scatter_step<4>(m, s, lane, 8);
+            scatter_step<2>(m, s, lane, 4);
+            scatter_step<1>(m, s, lane, 2);
+            {
+                const float rm = __shfl_xor(m[0], 1, kWave);
+                const float rs = __shfl_xor(s[0], 1, kWave);
+                ms_merge(m[0], s[0], rm, rs);
+            }
+            if ((lane & 1) == 0) {
+                const int rw = t.wm * 128 + i * 32 + acc_row((l32 >> 1) & 15, lane);
+                s_ms[t.wn * kTile + rw] = make_float2(m[0], s[0]);
+            }
+            // keep the next block's accumulators in AGPRs until they are used
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __syncthreads();
+        const float2 a = s_ms[tid], b = s_ms[kTile + tid];
+        float M = a.x, S = a.y;
+        ms_merge(M, S, b.x, b.y);
+        const int64_t r = row0 + tid;
+        if (r < N) part[r * tiles_v + t.tn] = make_float2(M, S);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Combine: one wave per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void lm_combine_kernel(
+    const float2* __restrict__ part, int tiles_v, const float* __restrict__ zy, int64_t N,
+    int64_t n_rows, int V, const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+    const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+    const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+    float* __restrict__ tok_loss_out, float* __restrict__ row_loss, float* __restrict__ g_out,
+    float* __restrict__ lse2_out, int32_t* __restrict__ dev_err) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + (threadIdx.x / kWave);
+    if (row >= n_rows) return;
+    // Padding rows and excluded tokens: g = 0 and an infinite log-sum-exp
+    // make every dZ entry of the row exactly zero.
+    if (row >= N) {
+        if (lane == 0) g_out[row] = 0.0f, lse2_out[row] = INFINITY;
+        return;
+    }
+    const float w = w_tok[row];
+    const int y = token_ids[row];
+    if (!row_live(w, y, V)) {
+        if (lane == 0) {
+            if (w != 0.0f) count_error(dev_err);  // token id out of range
+            obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+            g_out[row] = 0.0f;
+            lse2_out[row] = INFINITY;
+        }
+        return;
+    }
+    float m = -INFINITY, s = 0.0f;
+    for (int t = lane; t < tiles_v; t += kWave) {
+        const float2 q = part[row * tiles_v + t];
+        ms_merge(m, s, q.x, q.y);
+    }
+    wave_ms_reduce(m, s);
+    if (lane != 0) return;
+    if (m == -INFINITY) {  // every logit of the row is -inf
+        count_error(dev_err);
+        obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+        g_out[row] = 0.0f;
+        lse2_out[row] = INFINITY;
+        return;
+    }
+    const float lse2 = m + __builtin_amdgcn_logf(s);
+    const RowOut o = obj::row_epilogue(lse2, zy[row], old_logp[row], ref_logp[row], adv_tok[row], w, p);
+    obj::write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+    g_out[row] = o.g;
+    lse2_out[row] = lse2;
+}
+
+// ---------------------------------------------------------------------------
+// dZ epilogue: dz = g (onehot - 2^(z c - lse2)), zero past V, rounded to
+// bf16.  Register groups r = 4q..4q+3 of a lane are 4 consecutive rows of one
+// column: they go to the transposed copy as one 8-byte store, and after a
+// 4 x 4 transpose inside each lane quad (two DPP exchanges) each lane holds 4
+// consecutive columns of one row for the row-major copy.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float dpp_quad_xor1(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_quad_xor2(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+}
+
+// In: d[e] = M[row e][column q] where q = lane % 4.  Out: d[b] = M[row q][column b].
+__device__ __forceinline__ void quad_transpose(float (&d)[4], int lane) {
+    const bool odd = (lane & 1) != 0;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+        const float recv = dpp_quad_xor1(odd ? d[2 * a] : d[2 * a + 1]);
+        if (odd)
+            d[2 * a] = recv;
+        else
+            d[2 * a + 1] = recv;
+    }
+    const bool hi = (lane & 2) != 0;
+    const float r0 = dpp_quad_xor2(hi ? d[0] : d[2]);
+    const float r1 = dpp_quad_xor2(hi ? d[1] : d[3]);
+    if (hi) {
+        d[0] = r0, d[1] = r1;
+    } else {
+        d[2] = r0, d[3] = r1;
+    }
+}
+
+struct DzEpi {
+    const int32_t* token_ids;
+    const float* lse2;
+    const float* g;
+    uint16_t* dz;   // [N_pad][ld_dz], chunk-local columns; null: not written
+    int64_t ld_dz;
+    uint16_t* dzt;  // [chunk][ld_dzt]; null: not written
+    int64_t ld_dzt;
+    int64_t N;
+    int V, c0;  // vocabulary size, first column of the chunk
+    float c2;
+
+    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t* smem) const {
+        float* s_l = reinterpret_cast<float*>(smem);
+        float* s_g = s_l + kTile;
+        int* s_y = reinterpret_cast<int*>(s_g + kTile);
+        const int tid = threadIdx.x;
+        const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
+        {
+            const int64_t r = row0 + tid;
+            if (r < N) {
+                s_l[tid] = lse2[r];
+                s_g[tid] = g[r];
+                const int y = token_ids[r];
+                s_y[tid] = (y >= c0 && y < V) ? y - c0 : -1;
+            } else {
+                s_l[tid] = INFINITY;
+                s_g[tid] = 0.0f;
+                s_y[tid] = -1;
+            }
+        }
+        __syncthreads();
+        const int lane = t.lane, l32 = lane & 31, half = lane >> 5;
+        const int vw = t.col0();  // chunk-local column of the wave's block
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int v = vw + j * 32 + l32;
+                const bool colok = c0 + v < V;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int rq = t.wm * 128 + i * 32 + q * 8 + half * 4;  // tile row of e = 0
+                    float d[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float pz = __builtin_amdgcn_exp2f(acc[i][j][4 * q + e] * c2 - s_l[rq + e]);
+                        const float dd = s_g[rq + e] * ((v == s_y[rq + e] ? 1.0f : 0.0f) - pz);
+                        d[e] = colok ? dd : 0.0f;
+                    }
+                    if (dzt) {
+                        uint2 w2 = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
+                        *reinterpret_cast<uint2*>(dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rq) = w2;
+                    }
+                    if (dz) {
+                        quad_transpose(d, lane);
+                        uint2 w2 = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
+                        *reinterpret_cast<uint2*>(dz + (row0 + rq + (lane & 3)) * ld_dz + (v & ~3)) = w2;
+                    }
+                }
+            }
+        }
+    }
+};
+
+// fp32 result tile into C[rows][cols] (leading dimension ldc): stored, or
+// added to what C holds.
+template <bool ACCUMULATE>
+struct StoreF32Epi {
+    float* C;
+    int64_t ldc;
+    int64_t rows;
+    int cols;
+
+    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t*) const {
+        const int lane = t.lane;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = t.col0() + j * 32 + (lane & 31);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t m = t.row0() + i * 32 + acc_row(r, lane);
+                    if (m < rows && n < cols) {
+                        float* p = C + m * ldc + n;
+                        *p = ACCUMULATE ? *p + acc[i][j][r] : acc[i][j][r];
+                    }
+                }
+            }
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+struct Dims {
+    int64_t N, N_pad;
+    int V, V_pad, H, H_pad, tiles_v, Vc;
+};
+
+Dims dims_of(int64_t N, int V, int H) {
+    Dims d;
+    d.N = N;
+    d.N_pad = round_up(N > 0 ? N : 1, kTile);
+    d.V = V;
+    d.V_pad = static_cast<int>(round_up(V, kTile));
+    d.H = H;
+    d.H_pad = static_cast<int>(round_up(H, kTile));
+    d.tiles_v = d.V_pad / kTile;
+    d.Vc = d.V_pad < kChunkCols ? d.V_pad : kChunkCols;
+    return d;
+}
+
+struct Layout {
+    size_t ht, wt, part, zy, lse2, g, row_loss, dz, dzt, total;
+};
+
+Layout layout_of(const Dims& d) {
+    Layout L;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += (bytes + 255) & ~static_cast<size_t>(255);
+        return at;
+    };
+    L.ht = take(static_cast<size_t>(d.H) * d.N_pad * 2);
+    L.wt = take(static_cast<size_t>(d.H) * d.V_pad * 2);
+    L.part = take(static_cast<size_t>(d.N_pad) * d.tiles_v * sizeof(float2));
+    L.zy = take(static_cast<size_t>(d.N_pad) * 4);
+    L.lse2 = take(static_cast<size_t>(d.N_pad) * 4);
+    L.g = take(static_cast<size_t>(d.N_pad) * 4);
+    L.row_loss = take(static_cast<size_t>(d.N_pad) * 4);
+    L.dz = take(static_cast<size_t>(d.N_pad) * d.Vc * 2);
+    L.dzt = take(static_cast<size_t>(d.Vc) * d.N_pad * 2);
+    L.total = off;
+    return L;
+}
+
+// The GEMM core addresses each operand with 32-bit byte offsets: the last
+// row any tile touches must start below 4 GiB.
+bool fits32(int64_t rows_padded, int64_t ld) {
+    return static_cast<uint64_t>(rows_padded) * static_cast<uint64_t>(ld) * 2u < (1ull << 32) - 64u;
+}
+
+bool shapes_fit(const Dims& d) {
+    return fits32(d.N_pad, d.H) &&       // H   [N][H]
+           fits32(d.V_pad, d.H) &&       // W   [V][H]
+           fits32(d.Vc, d.N_pad) &&      // dZt [chunk][N_pad]
+           fits32(d.H_pad, d.N_pad) &&   // Ht  [H][N_pad]
+           fits32(d.N_pad, d.Vc) &&      // dZ  [N_pad][chunk]
+           fits32(d.H_pad, d.V_pad);     // Wt  [H][V_pad]
+}
+
+uint32_t extent32(uint64_t bytes) {
+    return bytes > 0xffffffffull ? 0xffffffffu : static_cast<uint32_t>(bytes);
+}
+
+template <class Epi>
+leap_status gemm_nt(const uint16_t* A, int64_t lda, uint64_t a_bytes, const uint16_t* B, int64_t ldb,
+                    uint64_t b_bytes, int K, int64_t M, int64_t Ncols, const Epi& epi,
+                    hipStream_t stream) {
+    const int tiles_m = static_cast<int>((M + kTile - 1) / kTile);
+    const int tiles_n = static_cast<int>((Ncols + kTile - 1) / kTile);
+    hipLaunchKernelGGL(gemm::gemm_nt_kernel<Epi>, dim3(gemm::gemm_grid(tiles_m, tiles_n)),
+                       dim3(gemm::kThreads), 0, stream, A, lda, extent32(a_bytes), B, ldb,
+                       extent32(b_bytes), K, tiles_m, tiles_n, epi);
+    return launch_status();
+}
+
+}  // namespace
+}  // namespace leap
+
+LEAP_API size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H) {
+    using namespace leap;
+    if (N < 0 || V < 1 || H < 1) return 0;
+    return layout_of(dims_of(N, V, H)).total;
+}
+
+LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
+    const void* hidden_bf16, const void* weight_bf16, int64_t N, int32_t V, int32_t H,
+    const int32_t* token_ids, const float* old_logp, const float* ref_logp, const float* adv_tok,
+    const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
+    float* loss_out, float* dhidden, float* dweight, int32_t accumulate_dweight, void* workspace,
+    size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
+    using namespace leap;
+    if (N < 0 || N > 0x7fffffffLL - kTile || V < 1 || H < 1 || !params || !loss_out)
+        return LEAP_ERR_INVALID_ARG;
+    if (accumulate_dweight != 0 && accumulate_dweight != 1) return LEAP_ERR_INVALID_ARG;
+    const leap_grpo_params& pp = *params;
+    if (!(pp.clip_eps_low >= 0.0f) || !(pp.clip_eps_high >= 0.0f) || !(pp.kl_coef >= 0.0f) ||
+        !(pp.inv_temperature > 0.0f) || !__builtin_isfinite(pp.clip_eps_low) ||
+        !__builtin_isfinite(pp.clip_eps_high) || !__builtin_isfinite(pp.kl_coef) ||
+        !__builtin_isfinite(pp.inv_temperature))
+        return LEAP_ERR_INVALID_ARG;
+    if (pp.kl_type != LEAP_KL_K3 && pp.kl_type != LEAP_KL_K1 && pp.kl_type != LEAP_KL_K2)
+        return LEAP_ERR_UNSUPPORTED;
+    if (H % 32 != 0) return LEAP_ERR_UNSUPPORTED;
+    const Dims d = dims_of(N, V, H);
+    if (!shapes_fit(d)) return LEAP_ERR_UNSUPPORTED;
+    if (N > 0) {
+        if (!hidden_bf16 || !weight_bf16 || !token_ids || !old_logp || !ref_logp || !adv_tok ||
+            !w_tok)
+            return LEAP_ERR_INVALID_ARG;
+        if (!aligned16(hidden_bf16) || !aligned16(weight_bf16)) return LEAP_ERR_MISALIGNED;
+    }
+    if ((reinterpret_cast<uintptr_t>(dhidden) & 3u) != 0 ||
+        (reinterpret_cast<uintptr_t>(dweight) & 3u) != 0)
+        return LEAP_ERR_MISALIGNED;
+    const Layout L = layout_of(d);
+    if (!workspace || ws_bytes < L.total) return LEAP_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return LEAP_ERR_MISALIGNED;
+
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    uint16_t* ht = reinterpret_cast<uint16_t*>(ws + L.ht);
+    uint16_t* wt = reinterpret_cast<uint16_t*>(ws + L.wt);
+    float2* part = reinterpret_cast<float2*>(ws + L.part);
+    float* zy = reinterpret_cast<float*>(ws + L.zy);
+    float* lse2 = reinterpret_cast<float*>(ws + L.lse2);
+    float* g = reinterpret_cast<float*>(ws + L.g);
+    float* row_loss = reinterpret_cast<float*>(ws + L.row_loss);
+    uint16_t* dz = reinterpret_cast<uint16_t*>(ws + L.dz);
+    uint16_t* dzt = reinterpret_cast<uint16_t*>(ws + L.dzt);
+    const uint16_t* Hm = static_cast<const uint16_t*>(hidden_bf16);
+    const uint16_t* Wm = static_cast<const uint16_t*>(weight_bf16);
+    leap_status st;
+
+    if (N == 0) {
+        if (dweight && !accumulate_dweight) {
+            hipLaunchKernelGGL(fill_zero_f32_kernel, dim3(1024), dim3(256), 0, stream, dweight,
+                               static_cast<int64_t>(V) * H);
+            if ((st = launch_status()) != LEAP_OK) return st;
+        }
+        hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
+                           row_loss, int64_t{0}, loss_out);
+        return launch_status();
+    }
+
+    const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
+    const float c2 = obj::kLog2e * pp.inv_temperature;
+    const uint64_t h_bytes = static_cast<uint64_t>(N) * H * 2;
+    const uint64_t w_bytes = static_cast<uint64_t>(V) * H * 2;
+
+    // 1. transposed operands of the backward GEMMs
+    if (dweight) {
+        hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.N_pad / kTr), (H + kTr - 1) / kTr),
+                           dim3(256), 0, stream, Hm, N, H, static_cast<int64_t>(H), ht, d.N_pad);
+        if ((st = launch_status()) != LEAP_OK) return st;
+    }
+    if (dhidden) {
+        hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.V_pad / kTr), (H + kTr - 1) / kTr),
+                           dim3(256), 0, stream, Wm, static_cast<int64_t>(V), H,
+                           static_cast<int64_t>(H), wt, static_cast<int64_t>(d.V_pad));
+        if ((st = launch_status()) != LEAP_OK) return st;
+    }
+
+    // 2. row statistics and the token logit
+    {
+        const StatsEpi epi{token_ids, part, zy, N, V, d.tiles_v, c2};
+        if ((st = gemm_nt(Hm, H, h_bytes, Wm, H, w_bytes, H, N, V, epi, stream)) != LEAP_OK) return st;
+    }
+    // 3. per-token objective
+    hipLaunchKernelGGL(lm_combine_kernel, dim3(static_cast<unsigned>(d.N_pad / 4)), dim3(256), 0,
+                       stream, part, d.tiles_v, zy, N, d.N_pad, V, token_ids, old_logp, ref_logp,
+                       adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
+    if ((st = launch_status()) != LEAP_OK) return st;
+    hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
+                       row_loss, N, loss_out);
+    if ((st = launch_status()) != LEAP_OK) return st;
+    if (!dhidden && !dweight) return LEAP_OK;
+
+    // 4. gradients, one vocabulary chunk at a time
+    for (int c0 = 0; c0 < V; c0 += d.Vc) {
+        const int vl = (d.V_pad - c0) < d.Vc ? (d.V_pad - c0) : d.Vc;  // multiple of 256
+        {
+            const DzEpi epi{token_ids, lse2, g, dhidden ? dz : nullptr, d.Vc,
+                            dweight ? dzt : nullptr, d.N_pad, N, V, c0, c2};
+            const uint64_t wb = static_cast<uint64_t>(V - c0) * H * 2;
+            if ((st = gemm_nt(Hm, H, h_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
+                              epi, stream)) != LEAP_OK)
+                return st;
+        }
+        if (dweight) {
+            const int64_t rows = (V - c0) < vl ? (V - c0) : vl;
+            float* C = dweight + static_cast<int64_t>(c0) * H;
+            const uint64_t ab = static_cast<uint64_t>(vl) * d.N_pad * 2;
+            const uint64_t bb = static_cast<uint64_t>(H) * d.N_pad * 2;
+            const int K = static_cast<int>(d.N_pad);
+            st = accumulate_dweight
+                     ? gemm_nt(dzt, d.N_pad, ab, ht, d.N_pad, bb, K, vl, H,
+                               StoreF32Epi<true>{C, H, rows, H}, stream)
+                     : gemm_nt(dzt, d.N_pad, ab, ht, d.N_pad, bb, K, vl, H,
+                               StoreF32Epi<false>{C, H, rows, H}, stream);
+            if (st != LEAP_OK) return st;
+        }
+        if (dhidden) {
+            const uint64_t ab = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
+            const uint64_t bb = static_cast<uint64_t>(H) * d.V_pad * 2 - static_cast<uint64_t>(c0) * 2;
+            st = c0 > 0 ? gemm_nt(dz, d.Vc, ab, wt + c0, d.V_pad, bb, vl, N, H,
+                                  StoreF32Epi<true>{dhidden, H, N, H}, stream)
+                        : gemm_nt(dz, d.Vc, ab, wt + c0, d.V_pad, bb, vl, N, H,
+                                  StoreF32Epi<false>{dhidden, H, N, H}, stream);
+            if (st != LEAP_OK) return st;
+        }
+    }
+    return LEAP_OK;
+}

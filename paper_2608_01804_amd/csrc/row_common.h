@@ -4,12 +4,14 @@
 #pragma once
 
 #include "leap_common.h"
+#include "objective.h"
 
 namespace leap {
 namespace row {
 
-constexpr float kLog2e = 1.44269504088896340736f;
-constexpr float kLn2 = 0.69314718055994530942f;
+using obj::kLog2e;
+using obj::kLn2;
+using obj::Params;
 constexpr uint32_t kNegInfBf16 = 0xFF80u;
 constexpr uint32_t kNegInfPair = 0xFF80FF80u;
 // Word 3 of a raw gfx9 buffer descriptor (32-bit data format, no swizzle).
@@ -23,11 +25,6 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf162v __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-struct Params {
-    float eps_lo, eps_hi, kl_coef, inv_temp;
-    int kl_type;
-};
 
 __device__ __forceinline__ u32x4 u32x4_of(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
     u32x4 v = {a, b, c, d};

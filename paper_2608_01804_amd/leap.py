@@ -37,6 +37,8 @@ EXPORTED = (
     "leap_grpo_workspace_size",
     "leap_grpo_logprob_loss_fwd_bwd",
     "leap_logprob_fwd",
+    "leap_lmhead_workspace_size",
+    "leap_grpo_lmhead_fwd_bwd",
     "leap_probe_hbm",
 )
 
@@ -91,6 +93,12 @@ def lib() -> ctypes.CDLL:
                                                  P, ctypes.c_size_t, P, P]
     L.leap_logprob_fwd.restype = ctypes.c_int
     L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P]
+    L.leap_lmhead_workspace_size.restype = ctypes.c_size_t
+    L.leap_lmhead_workspace_size.argtypes = [i64, i32, i32]
+    L.leap_grpo_lmhead_fwd_bwd.restype = ctypes.c_int
+    L.leap_grpo_lmhead_fwd_bwd.argtypes = [P, P, i64, i32, i32, P, P, P, P, P,
+                                           ctypes.POINTER(leap_grpo_params), P, P, P, P, P, i32,
+                                           P, ctypes.c_size_t, P, P]
     L.leap_probe_hbm.restype = ctypes.c_int
     L.leap_probe_hbm.argtypes = [P, P, ctypes.c_size_t, i32, P]
     _lib = L
@@ -222,6 +230,27 @@ def leap_logprob_fwd(logits, ld, N, V, token_ids, w_tok, inv_temperature, logp_o
         float(inv_temperature), _ptr(logp_out, "float32", "logp_out"),
         _ptr(dev_err, "int32", "dev_err"), _stream(stream))
     _check(st, "leap_logprob_fwd")
+
+
+def leap_lmhead_workspace_size(N, V, H) -> int:
+    return int(lib().leap_lmhead_workspace_size(int(N), int(V), int(H)))
+
+
+def leap_grpo_lmhead_fwd_bwd(hidden, weight, N, V, H, token_ids, old_logp, ref_logp, adv_tok, w_tok,
+                             params: leap_grpo_params, logp_out, tok_loss_out, loss_out, dhidden,
+                             dweight, accumulate_dweight, workspace, ws_bytes, dev_err=None,
+                             stream=None) -> None:
+    st = lib().leap_grpo_lmhead_fwd_bwd(
+        _ptr(hidden, "bfloat16", "hidden"), _ptr(weight, "bfloat16", "weight"), int(N), int(V),
+        int(H), _ptr(token_ids, "int32", "token_ids"), _ptr(old_logp, "float32", "old_logp"),
+        _ptr(ref_logp, "float32", "ref_logp"), _ptr(adv_tok, "float32", "adv_tok"),
+        _ptr(w_tok, "float32", "w_tok"), ctypes.byref(params) if params is not None else None,
+        _ptr(logp_out, "float32", "logp_out"), _ptr(tok_loss_out, "float32", "tok_loss_out"),
+        _ptr(loss_out, "float32", "loss_out"), _ptr(dhidden, "float32", "dhidden"),
+        _ptr(dweight, "float32", "dweight"), int(accumulate_dweight),
+        _ptr(workspace, None, "workspace"), int(ws_bytes), _ptr(dev_err, "int32", "dev_err"),
+        _stream(stream))
+    _check(st, "leap_grpo_lmhead_fwd_bwd")
 
 
 def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:

@@ -179,3 +179,114 @@ def make_inputs_host(seed, N, V, ld=None, old_sigma=wl.OLD_SIGMA, edit=None):
     cur = np.where(np.isfinite(cur) & (tok >= 0) & (tok < V), cur, 0.0)
     n_old, n_ref = wl.logp_noise(seed, N, old_sigma=old_sigma)
     return lg, tok, (cur + n_old).astype(np.float32), (cur + n_ref).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Fused LM head
+# ---------------------------------------------------------------------------
+def bf16_tensor_bits(t) -> np.ndarray:
+    """uint16 bit patterns of a bf16 torch tensor (copied to the host)."""
+    import torch
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def torch_token_logp(hidden, weight, y, row_chunk=256) -> np.ndarray:
+    """fp32 log-softmax of hidden weight^T at y, formed with torch a block of
+    rows at a time.  Input preparation only (the current policy from which
+    the old and reference log-probabilities are derived at sizes the oracle
+    cannot score whole); never an expected value."""
+    import torch
+    out = torch.empty(hidden.shape[0], dtype=torch.float32, device=hidden.device)
+    wf = weight.float()
+    yl = y.long()
+    for r0 in range(0, hidden.shape[0], row_chunk):
+        r1 = min(hidden.shape[0], r0 + row_chunk)
+        z = hidden[r0:r1].float() @ wf.T
+        out[r0:r1] = torch.log_softmax(z, dim=1).gather(1, yl[r0:r1, None].clamp(0, z.shape[1] - 1))[:, 0]
+    return out.double().cpu().numpy()
+
+
+def lmhead_inputs(seed, N, V, H, mask_frac=0.05, bad_rows=(), cur="oracle", inv_temp=1.0):
+    """Seeded LM-head inputs: bf16 hidden / weight on the device (with host
+    bit patterns), Gumbel-max tokens, old/ref = current log-prob + noise,
+    advantages ~ N(0, 1), weights 1/N with a fraction of excluded rows, and
+    optional rows with an out-of-range token id."""
+    import torch
+    hid, wt = wl.lmhead_operands_device(seed, N, V, H, dev())
+    y_t = wl.lmhead_tokens_device(hid, wt, seed)
+    y = y_t.cpu().numpy().astype(np.int32)
+    h_u16, w_u16 = bf16_tensor_bits(hid), bf16_tensor_bits(wt)
+    rng = np.random.default_rng(seed * 31 + 7)
+    w = np.full(N, 1.0 / max(N, 1))
+    w[rng.random(N) < mask_frac] = 0.0
+    adv = rng.normal(0.0, 1.0, N)
+    for r in bad_rows:
+        y[r] = V
+        w[r] = 1.0 / N
+    if cur == "oracle":
+        z = np.zeros(N)
+        c = oracle.lmhead(h_u16, w_u16, np.clip(y, 0, V - 1), z, z, z, np.ones(N),
+                          inv_temp=inv_temp, want_grads=False)["logp"]
+    else:
+        assert inv_temp == 1.0
+        c = torch_token_logp(hid, wt, T(np.clip(y, 0, V - 1)))
+    n_old, n_ref = wl.logp_noise(seed, N)
+    return {"hid": hid, "wt": wt, "h_u16": h_u16, "w_u16": w_u16, "y": y,
+            "old": (c + n_old).astype(np.float32), "ref": (c + n_ref).astype(np.float32),
+            "adv": adv.astype(np.float32), "w": w.astype(np.float32)}
+
+
+def run_lmhead(inp, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0, inv_temp=1.0, want_dH=True,
+               want_dW=True, accumulate=0, dW_init=None, to_host=True):
+    """Call leap_grpo_lmhead_fwd_bwd; returns numpy logp, tok_loss, loss, dH,
+    dW (or the device tensors with to_host=False), bad."""
+    import torch
+    from paper_2608_01804_amd import leap as L
+    hid, wt = inp["hid"], inp["wt"]
+    N, H = hid.shape
+    V = wt.shape[0]
+    lp = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+    tl = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+    loss = torch.full((1,), float("nan"), dtype=torch.float32, device=dev())
+    dH = torch.full((max(1, N), H), float("nan"), dtype=torch.float32, device=dev()) if want_dH else None
+    dW = None
+    if want_dW:
+        dW = (T(dW_init.astype(np.float32)) if dW_init is not None
+              else torch.full((V, H), float("nan"), dtype=torch.float32, device=dev()))
+    ws_bytes = L.leap_lmhead_workspace_size(N, V, H)
+    ws = torch.full((ws_bytes,), 0xA5, dtype=torch.uint8, device=dev())  # stale contents
+    err = zeros_i32(1)
+    p = L.leap_grpo_params(eps_lo, eps_hi, kl_coef, kl_type, inv_temp)
+    L.leap_grpo_lmhead_fwd_bwd(hid, wt, N, V, H, T(inp["y"]), T(inp["old"]), T(inp["ref"]),
+                               T(inp["adv"]), T(inp["w"]), p, lp, tl, loss, dH, dW, accumulate, ws,
+                               ws_bytes, err)
+    torch.cuda.synchronize()
+    out = {"logp": lp.cpu().numpy()[:N], "tok_loss": tl.cpu().numpy()[:N],
+           "loss": float(loss.item()), "bad": int(err.item())}
+    if to_host:
+        out["dH"] = dH.cpu().numpy()[:N] if dH is not None else None
+        out["dW"] = dW.cpu().numpy() if dW is not None else None
+    else:
+        out["dH"], out["dW"] = dH, dW
+    return out
+
+
+def bf16_f64(u16: np.ndarray) -> np.ndarray:
+    return (u16.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def check_grad(got, want, bound, what, slack=1e-6):
+    """|got - want| <= (2^-8 + 1e-4) * bound + slack * max|bound|, where bound
+    is the oracle's |dZ| times the absolute operand: rounding dZ to bf16 (8
+    significant bits, round to nearest) before the gradient products moves
+    each term by at most 2^-8 of itself, and the fp32 exp / log-sum-exp and
+    accumulation errors add about 1e-5 of it."""
+    err = np.abs(got.astype(np.float64) - want)
+    tol = (2.0 ** -8 + 1e-4) * bound + slack * max(float(np.max(bound, initial=0.0)), 1e-30)
+    bad = err > tol
+    fro = np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-300)
+    log(f"  {what}: max err {err.max(initial=0):.3e}, rel fro {fro:.3e}, "
+        f"max err/bound {np.max(err / np.maximum(bound, 1e-30), initial=0):.3e}")
+    assert not bad.any(), f"{what}: {int(bad.sum())} entries beyond the bound; first at " \
+                          f"{np.argwhere(bad)[0].tolist()}"
+    return fro

@@ -209,3 +209,58 @@ def test_probe_rejects():
     with pytest.raises(L.LeapError) as e:
         L.leap_probe_hbm(FAKE + 4, FAKE, 16, 0, stream=0)
     assert e.value.status == L.LEAP_ERR_MISALIGNED
+
+
+def _lmhead(**kw):
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+    a = dict(hidden=FAKE, weight=FAKE, N=8, V=1000, H=64, token_ids=FAKE, old_logp=FAKE,
+             ref_logp=FAKE, adv_tok=FAKE, w_tok=FAKE, params=p, logp_out=None, tok_loss_out=None,
+             loss_out=FAKE, dhidden=FAKE, dweight=FAKE, accumulate_dweight=0, workspace=FAKE,
+             ws_bytes=1 << 20, dev_err=None, stream=0)
+    a.update(kw)
+    return L.leap_grpo_lmhead_fwd_bwd(**a)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=-1), L.LEAP_ERR_INVALID_ARG),
+    (dict(V=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(H=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(accumulate_dweight=2), L.LEAP_ERR_INVALID_ARG),
+    (dict(loss_out=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(params=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(hidden=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(w_tok=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(H=48), L.LEAP_ERR_UNSUPPORTED),
+    (dict(V=1 << 20, H=4096), L.LEAP_ERR_UNSUPPORTED),  # W beyond 32-bit offsets
+    (dict(hidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
+    (dict(weight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
+    (dict(dweight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
+    (dict(workspace=None), L.LEAP_ERR_WORKSPACE),
+    (dict(ws_bytes=1024), L.LEAP_ERR_WORKSPACE),
+])
+def test_lmhead_rejects(kw, status):
+    if "ws_bytes" not in kw and "workspace" not in kw:
+        kw["ws_bytes"] = L.leap_lmhead_workspace_size(8, 1000, 64)
+    with pytest.raises(L.LeapError) as e:
+        _lmhead(**kw)
+    assert e.value.status == status
+
+
+def test_lmhead_rejects_params():
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, 9, 1.0)
+    with pytest.raises(L.LeapError) as e:
+        _lmhead(params=p, ws_bytes=L.leap_lmhead_workspace_size(8, 1000, 64))
+    assert e.value.status == L.LEAP_ERR_UNSUPPORTED
+
+
+def test_lmhead_workspace_size():
+    assert L.leap_lmhead_workspace_size(-1, 10, 64) == 0
+    assert L.leap_lmhead_workspace_size(8, 0, 64) == 0
+    small = L.leap_lmhead_workspace_size(8, 1000, 64)
+    assert small > 0 and small % 256 == 0
+    # 16384 x 151936 x 4096: transposes (H*N_pad + H*V_pad bf16), per-tile row
+    # statistics, four per-row vectors and one 8192-column chunk of dZ in two layouts
+    n, v, h = 16384, 151936, 4096
+    v_pad = (v + 255) // 256 * 256
+    want = 2 * h * n + 2 * h * v_pad + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 8192
+    assert abs(L.leap_lmhead_workspace_size(n, v, h) - want) <= 9 * 256

@@ -1,0 +1,163 @@
+"""Parity of the fused LM-head entry point (leap_grpo_lmhead_fwd_bwd) with
+the fp64 oracle on seeded inputs shaped like the LM-head workload (hidden
+~ N(0, 1), weight ~ N(0, 0.02^2), Gumbel-max tokens).
+
+Bars: log-probs within 2e-3 absolute, per-token loss within 2e-3 relative,
+total loss within 1e-3 relative; dH and dW entrywise within (2^-8 + 1e-4)
+of the oracle's |dZ| |W| and |dZ|^T |H| (dZ is rounded to bf16 before the
+gradient products, which moves every term by at most 2^-8 of itself, and the
+fp32 softmax adds about 1e-5); excluded rows give exactly zero gradient
+rows.  At the full 16384 x 151936 x 4096 shape the
+oracle scores 64 sampled rows (log-prob, loss, dH); dW there is cross-checked
+against the logits-resident kernel on bf16 logits plus a torch GEMM (a looser
+bar, since those logits are rounded to bf16)."""
+import numpy as np
+import pytest
+
+import oracle
+from tests import _gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+def _kw(kl_type=0, inv_temp=1.0, kl_coef=0.01):
+    return dict(eps_lo=0.2, eps_hi=0.2, kl_coef=kl_coef, kl_type=kl_type, inv_temp=inv_temp)
+
+
+def _compare(inp, gpu, kw, bad_expected=0, what=""):
+    o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
+                      inp["w"], **kw)
+    V = inp["wt"].shape[0]
+    y, w = inp["y"], inp["w"]
+    valid = (w != 0) & (y >= 0) & (y < V)
+    assert gpu["bad"] == o["bad"] == bad_expected, (gpu["bad"], o["bad"])
+    err = np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0)
+    U.log(f"  {what} logp max err {err:.3e}")
+    assert err < 2e-3
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
+    Hf, Wf = U.bf16_f64(inp["h_u16"]), U.bf16_f64(inp["w_u16"])
+    aZ = np.abs(o["dZ"])
+    if gpu["dH"] is not None:
+        U.check_grad(gpu["dH"], o["dH"], aZ @ np.abs(Wf), f"{what} dH")
+        assert np.all(gpu["dH"][~valid] == 0.0)
+    if gpu["dW"] is not None:
+        U.check_grad(gpu["dW"], o["dW"], aZ.T @ np.abs(Hf), f"{what} dW")
+    return o
+
+
+def test_lmhead_reduced_shape_full_parity():
+    N, V, H = 1024, 32768, 512
+    U.log(f"lmhead reduced N={N} V={V} H={H} seed=1005")
+    inp = U.lmhead_inputs(1005, N, V, H, bad_rows=(17,))
+    gpu = U.run_lmhead(inp, **_kw())
+    _compare(inp, gpu, _kw(), bad_expected=1, what="reduced")
+
+
+@pytest.mark.parametrize("N,V,H,inv_temp,kl_type", [
+    (300, 1000, 96, 0.8, 1),      # ragged rows and vocabulary, one chunk
+    (257, 8492, 64, 1.0, 2),      # two chunks, the last one 512 wide with 300 live columns
+    (1, 300, 32, 1.0, 0),         # a single row
+    (513, 16640, 128, 1.25, 0),   # three chunks, the last one 256 wide
+])
+def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
+    U.log(f"lmhead ragged N={N} V={V} H={H} T^-1={inv_temp} kl={kl_type}")
+    inp = U.lmhead_inputs(2000 + N, N, V, H, inv_temp=inv_temp)
+    kw = _kw(kl_type=kl_type, inv_temp=inv_temp, kl_coef=0.05)
+    gpu = U.run_lmhead(inp, **kw)
+    _compare(inp, gpu, kw, what=f"N={N} V={V}")
+
+
+def test_lmhead_accumulate_and_optional_gradients():
+    N, V, H = 300, 1000, 96
+    U.log(f"lmhead options N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(3001, N, V, H)
+    kw = _kw()
+    full = U.run_lmhead(inp, **kw)
+    o = _compare(inp, full, kw, what="options")
+    init = np.random.default_rng(5).normal(0, 1, (V, H)).astype(np.float32)
+    acc = U.run_lmhead(inp, accumulate=1, dW_init=init, **kw)
+    np.testing.assert_array_equal(acc["dW"], init + full["dW"])  # one fp32 add per entry
+    only_h = U.run_lmhead(inp, want_dW=False, **kw)
+    np.testing.assert_array_equal(only_h["dH"], full["dH"])
+    only_w = U.run_lmhead(inp, want_dH=False, **kw)
+    np.testing.assert_array_equal(only_w["dW"], full["dW"])
+    fwd = U.run_lmhead(inp, want_dH=False, want_dW=False, **kw)
+    np.testing.assert_array_equal(fwd["logp"], full["logp"])
+    assert fwd["loss"] == full["loss"]
+    assert abs(full["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7
+
+
+def test_lmhead_empty_batch():
+    import torch
+    from paper_2608_01804_amd import leap as L
+    V, H = 1000, 64
+    U.log("lmhead N=0")
+    hid = torch.zeros((1, H), dtype=torch.bfloat16, device=U.dev())
+    wt = torch.zeros((V, H), dtype=torch.bfloat16, device=U.dev())
+    loss = torch.full((1,), float("nan"), dtype=torch.float32, device=U.dev())
+    ws_bytes = L.leap_lmhead_workspace_size(0, V, H)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=U.dev())
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, 0, 1.0)
+    one_f = torch.zeros(1, dtype=torch.float32, device=U.dev())
+    one_i = torch.zeros(1, dtype=torch.int32, device=U.dev())
+    for accumulate in (0, 1):
+        dW = torch.full((V, H), 3.0, dtype=torch.float32, device=U.dev())
+        L.leap_grpo_lmhead_fwd_bwd(hid, wt, 0, V, H, one_i, one_f, one_f, one_f, one_f, p, None,
+                                   None, loss, None, dW, accumulate, ws, ws_bytes)
+        torch.cuda.synchronize()
+        assert loss.item() == 0.0
+        assert torch.all(dW == (3.0 if accumulate else 0.0)).item()
+
+
+def test_lmhead_full_shape_sampled_rows():
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N, V, H = 16384, 151936, 4096
+    U.log(f"lmhead full N={N} V={V} H={H}: inputs")
+    inp = U.lmhead_inputs(1005, N, V, H, cur="torch", bad_rows=(5,))
+    kw = _kw()
+    U.log("  fused call")
+    gpu = U.run_lmhead(inp, to_host=False, **kw)
+    assert gpu["bad"] == 1
+    rng = np.random.default_rng(1005)
+    rows = np.unique(np.concatenate([[0, 5, N - 1], rng.choice(N, 61, replace=False)]))
+    U.log(f"  oracle on {rows.size} rows")
+    o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
+                      inp["w"], rows=rows, **kw)
+    y, w = inp["y"][rows], inp["w"][rows]
+    valid = (w != 0) & (y < V)
+    err = np.max(np.abs(gpu["logp"][rows][valid] - o["logp"][valid]))
+    U.log(f"  sampled logp max err {err:.3e}")
+    assert err < 2e-3
+    np.testing.assert_allclose(gpu["tok_loss"][rows][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    dH = gpu["dH"][torch.from_numpy(rows).to(U.dev())].cpu().numpy()
+    Wf = U.bf16_f64(inp["w_u16"])
+    U.check_grad(dH, o["dH"], np.abs(o["dZ"]) @ np.abs(Wf), "full sampled dH")
+    del Wf
+    assert np.isfinite(gpu["loss"])
+
+    # dW over every row: cross-check against the logits-resident kernel on
+    # bf16 logits formed by torch, and a torch fp32 GEMM.
+    U.log("  cross-check of dW via bf16 logits")
+    hid, wt = inp["hid"], inp["wt"]
+    lg = torch.empty((N, V), dtype=torch.bfloat16, device=U.dev())
+    wf = wt.float()
+    for r0 in range(0, N, 1024):
+        lg[r0:r0 + 1024] = (hid[r0:r0 + 1024].float() @ wf.T).to(torch.bfloat16)
+    del wf
+    ref = U.run_grpo(lg, V, inp["y"], inp["old"], inp["ref"], inp["adv"], inp["w"], inplace=True, **kw)
+    lp_err = np.max(np.abs(ref["logp"] - gpu["logp"]))
+    U.log(f"  logp vs bf16-logits path: max diff {lp_err:.3e}")
+    assert lp_err < 5e-2
+    hf = hid.float()
+    worst = 0.0
+    for v0 in range(0, V, 8192):
+        d = lg[:, v0:v0 + 8192].float()
+        dw_x = d.T @ hf
+        bound = d.abs().T @ hf.abs()
+        diff = (gpu["dW"][v0:v0 + 8192] - dw_x).abs()
+        worst = max(worst, float((diff / bound.clamp(min=1e-30)).max().item()))
+        assert torch.all(diff <= 0.03 * bound + 1e-9).item(), v0
+    U.log(f"  dW vs bf16-logits path: max diff/bound {worst:.3e}")
