@@ -267,7 +267,7 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  * ids (counted in *dev_err, excluded).
  *
  * hidden_bf16 [N][H] bf16, weight_bf16 [V][H] bf16, both row-major, 16-byte
- *              aligned.  H % 32 == 0 (else LEAP_ERR_UNSUPPORTED).
+ *              aligned.  H % 64 == 0 (else LEAP_ERR_UNSUPPORTED).
  * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
  * logp_out, tok_loss_out  float [N], nullable.  loss_out float [1], required.
  * dhidden    float [N][H], overwritten; NULL skips it.

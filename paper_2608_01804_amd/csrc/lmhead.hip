@@ -482,7 +482,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
         return LEAP_ERR_INVALID_ARG;
     if (pp.kl_type != LEAP_KL_K3 && pp.kl_type != LEAP_KL_K1 && pp.kl_type != LEAP_KL_K2)
         return LEAP_ERR_UNSUPPORTED;
-    if (H % 32 != 0) return LEAP_ERR_UNSUPPORTED;
+    if (H % 64 != 0) return LEAP_ERR_UNSUPPORTED;  // the GEMM core takes k-tiles of 64
     const Dims d = dims_of(N, V, H);
     if (!shapes_fit(d)) return LEAP_ERR_UNSUPPORTED;
     if (N > 0) {

@@ -231,6 +231,7 @@ def _lmhead(**kw):
     (dict(hidden=None), L.LEAP_ERR_INVALID_ARG),
     (dict(w_tok=None), L.LEAP_ERR_INVALID_ARG),
     (dict(H=48), L.LEAP_ERR_UNSUPPORTED),
+    (dict(H=96), L.LEAP_ERR_UNSUPPORTED),  # k-tiles of 64
     (dict(V=1 << 20, H=4096), L.LEAP_ERR_UNSUPPORTED),  # W beyond 32-bit offsets
     (dict(hidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(weight=FAKE + 2), L.LEAP_ERR_MISALIGNED),

@@ -56,9 +56,9 @@ def test_lmhead_reduced_shape_full_parity():
 
 
 @pytest.mark.parametrize("N,V,H,inv_temp,kl_type", [
-    (300, 1000, 96, 0.8, 1),      # ragged rows and vocabulary, one chunk
+    (300, 1000, 128, 0.8, 1),     # ragged rows and vocabulary, one chunk
     (257, 8492, 64, 1.0, 2),      # two chunks, the last one 512 wide with 300 live columns
-    (1, 300, 32, 1.0, 0),         # a single row
+    (1, 300, 64, 1.0, 0),         # a single row, one k-tile
     (513, 16640, 128, 1.25, 0),   # three chunks, the last one 256 wide
 ])
 def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
@@ -70,7 +70,7 @@ def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
 
 
 def test_lmhead_accumulate_and_optional_gradients():
-    N, V, H = 300, 1000, 96
+    N, V, H = 300, 1000, 192
     U.log(f"lmhead options N={N} V={V} H={H}")
     inp = U.lmhead_inputs(3001, N, V, H)
     kw = _kw()
