@@ -4,9 +4,10 @@
 // gradients dH = dZ W and dW = dZ^T H, where dZ = d(sum_k w_k l_k)/dz.
 //
 // Steps of one call, all on the caller's stream:
-//  1. H and W are transposed once into the workspace (Ht [H][N_pad], Wt
-//     [H][V_pad], zero padded), because every GEMM below runs on one NT core
-//     whose operands are both contiguous along the contraction index.
+//  1. H and W are transposed once into the workspace (Ht [H][N_pad]; Wt
+//     chunk-major, [chunk][H][8192], so its rows are 16 KiB apart; both zero
+//     padded), because every GEMM below runs on one NT core whose operands
+//     are both contiguous along the contraction index.
 //  2. Stats GEMM  Z = H W^T on MFMA.  Its epilogue turns every row of a
 //     256 x 256 tile into a partial (max, sum 2^(z c - max)) in base-2 units
 //     (c = log2(e) / T) and picks out the rollout token's logit.
@@ -36,7 +37,10 @@ using row::row_live;
 using row::u32x4;
 using row::wave_ms_reduce;
 
-constexpr int kChunkCols = 8192;  // vocabulary columns per backward chunk
+#ifndef LEAP_LM_CHUNK
+#define LEAP_LM_CHUNK 8192
+#endif
+constexpr int kChunkCols = LEAP_LM_CHUNK;  // vocabulary columns per backward chunk
 constexpr int kTile = gemm::kBM;  // 256: rows and columns of a GEMM tile
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -383,7 +387,7 @@ struct StoreF32Epi {
 // ---------------------------------------------------------------------------
 struct Dims {
     int64_t N, N_pad;
-    int V, V_pad, H, H_pad, tiles_v, Vc;
+    int V, V_pad, H, H_pad, tiles_v, Vc, n_chunks;
 };
 
 Dims dims_of(int64_t N, int V, int H) {
@@ -396,6 +400,7 @@ Dims dims_of(int64_t N, int V, int H) {
     d.H_pad = static_cast<int>(round_up(H, kTile));
     d.tiles_v = d.V_pad / kTile;
     d.Vc = d.V_pad < kChunkCols ? d.V_pad : kChunkCols;
+    d.n_chunks = (d.V_pad + d.Vc - 1) / d.Vc;
     return d;
 }
 
@@ -412,7 +417,7 @@ Layout layout_of(const Dims& d) {
         return at;
     };
     L.ht = take(static_cast<size_t>(d.H) * d.N_pad * 2);
-    L.wt = take(static_cast<size_t>(d.H) * d.V_pad * 2);
+    L.wt = take(static_cast<size_t>(d.n_chunks) * d.H * d.Vc * 2);
     L.part = take(static_cast<size_t>(d.N_pad) * d.tiles_v * sizeof(float2));
     L.zy = take(static_cast<size_t>(d.N_pad) * 4);
     L.lse2 = take(static_cast<size_t>(d.N_pad) * 4);
@@ -436,7 +441,7 @@ bool shapes_fit(const Dims& d) {
            fits32(d.Vc, d.N_pad) &&      // dZt [chunk][N_pad]
            fits32(d.H_pad, d.N_pad) &&   // Ht  [H][N_pad]
            fits32(d.N_pad, d.Vc) &&      // dZ  [N_pad][chunk]
-           fits32(d.H_pad, d.V_pad);     // Wt  [H][V_pad]
+           fits32(d.H_pad, d.Vc);        // Wt  [H][chunk] per chunk
 }
 
 uint32_t extent32(uint64_t bytes) {
@@ -535,10 +540,15 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
         if ((st = launch_status()) != LEAP_OK) return st;
     }
     if (dhidden) {
-        hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.V_pad / kTr), (H + kTr - 1) / kTr),
-                           dim3(256), 0, stream, Wm, static_cast<int64_t>(V), H,
-                           static_cast<int64_t>(H), wt, static_cast<int64_t>(d.V_pad));
-        if ((st = launch_status()) != LEAP_OK) return st;
+        for (int c = 0; c < d.n_chunks; ++c) {
+            const int c0 = c * d.Vc;
+            const int rows = (V - c0) < d.Vc ? (V - c0) : d.Vc;
+            hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.Vc / kTr), (H + kTr - 1) / kTr),
+                               dim3(256), 0, stream, Wm + static_cast<int64_t>(c0) * H,
+                               static_cast<int64_t>(rows), H, static_cast<int64_t>(H),
+                               wt + static_cast<int64_t>(c) * H * d.Vc, static_cast<int64_t>(d.Vc));
+            if ((st = launch_status()) != LEAP_OK) return st;
+        }
     }
 
     // 2. row statistics and the token logit
@@ -582,10 +592,11 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
         }
         if (dhidden) {
             const uint64_t ab = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
-            const uint64_t bb = static_cast<uint64_t>(H) * d.V_pad * 2 - static_cast<uint64_t>(c0) * 2;
-            st = c0 > 0 ? gemm_nt(dz, d.Vc, ab, wt + c0, d.V_pad, bb, vl, N, H,
+            const uint64_t bb = static_cast<uint64_t>(H) * d.Vc * 2;
+            const uint16_t* wc = wt + static_cast<int64_t>(c0 / d.Vc) * H * d.Vc;
+            st = c0 > 0 ? gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
                                   StoreF32Epi<true>{dhidden, H, N, H}, stream)
-                        : gemm_nt(dz, d.Vc, ab, wt + c0, d.V_pad, bb, vl, N, H,
+                        : gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
                                   StoreF32Epi<false>{dhidden, H, N, H}, stream);
             if (st != LEAP_OK) return st;
         }

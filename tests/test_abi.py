@@ -259,9 +259,11 @@ def test_lmhead_workspace_size():
     assert L.leap_lmhead_workspace_size(8, 0, 64) == 0
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
-    # 16384 x 151936 x 4096: transposes (H*N_pad + H*V_pad bf16), per-tile row
+    # 16384 x 151936 x 4096: transposes (H*N_pad, and H*8192 per vocabulary
+    # chunk, bf16), per-tile row
     # statistics, four per-row vectors and one 8192-column chunk of dZ in two layouts
     n, v, h = 16384, 151936, 4096
     v_pad = (v + 255) // 256 * 256
-    want = 2 * h * n + 2 * h * v_pad + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 8192
+    chunks = -(-v_pad // 8192)
+    want = 2 * h * n + 2 * h * 8192 * chunks + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 8192
     assert abs(L.leap_lmhead_workspace_size(n, v, h) - want) <= 9 * 256
