@@ -19,6 +19,8 @@ over ctypes with numpy arrays.  Functions and the passages they follow:
 * ``logprob_rows``     -- forward-only log-probabilities (old / reference).
 * ``lmhead``           -- the same per-token objective on logits z = H W^T
   (fused LM head), with dH = dZ W and dW = dZ^T H.
+* ``vocab_shard_stats`` -- one vocabulary shard's share of a row's
+  log-softmax normaliser (max and base-2 sum) and of its token logit.
 """
 from __future__ import annotations
 
@@ -241,6 +243,37 @@ def lmhead(hidden, weight, token_ids, old_logp, ref_logp, adv, w, eps_lo=0.2, ep
             dW = dZ.T @ Hm
     return {"logp": r["logp"], "tok_loss": r["tok_loss"], "loss": r["loss"], "dZ": dZ, "dH": dH,
             "dW": dW, "bad": r["bad"]}
+
+
+def vocab_shard_stats(logits, vocab_start, token_ids, w=None, inv_temp=1.0, V=None):
+    """One vocabulary shard's partial of the log-softmax of Sec. 3.1 (Eq. 3):
+    for each row, with c = log2(e) * inv_temp over the shard's columns
+    x[0..V-1] (global ids vocab_start + j): m2 = c * max_j x_j, s = sum_j
+    2^(c x_j - m2); owned = 1 and zy = x[y - vocab_start] when the row's token
+    y lies in the shard, else 0.  Rows with w == 0 (if w is given) or all -inf
+    give m2 = -inf, s = 0.  ``logits`` is float64 or bf16 bit patterns
+    [N, ld].  Returns float64 arrays (m2, s, zy, owned)."""
+    x = _bf16_to_f64(logits)
+    N, ld = x.shape
+    V = ld if V is None else int(V)
+    x = x[:, :V]
+    c = np.log2(np.e) * float(inv_temp)
+    yl = np.asarray(token_ids, np.int64) - int(vocab_start)
+    owned = ((yl >= 0) & (yl < V)).astype(np.float64)
+    m2 = np.full(N, -np.inf)
+    s = np.zeros(N)
+    zy = np.zeros(N)
+    for k in range(N):
+        if owned[k]:
+            zy[k] = x[k, yl[k]]
+        if w is not None and w[k] == 0:
+            continue
+        mx = np.max(x[k])
+        if mx == -np.inf:
+            continue
+        m2[k] = c * mx
+        s[k] = np.sum(np.exp2(c * x[k] - m2[k]))
+    return m2, s, zy, owned
 
 
 def tau_from_pass_rate(G: int, lo: Fraction, lo_strict: bool, hi: Fraction, hi_strict: bool):
