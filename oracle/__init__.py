@@ -250,8 +250,9 @@ def vocab_shard_stats(logits, vocab_start, token_ids, w=None, inv_temp=1.0, V=No
     for each row, with c = log2(e) * inv_temp over the shard's columns
     x[0..V-1] (global ids vocab_start + j): m2 = c * max_j x_j, s = sum_j
     2^(c x_j - m2); owned = 1 and zy = x[y - vocab_start] when the row's token
-    y lies in the shard, else 0.  Rows with w == 0 (if w is given) or all -inf
-    give m2 = -inf, s = 0.  ``logits`` is float64 or bf16 bit patterns
+    y lies in the shard, else 0.  Rows with w == 0 (if w is given) are not
+    read (m2 = -inf, s = 0, zy = 0; owned still reported); all -inf rows give
+    m2 = -inf, s = 0.  ``logits`` is float64 or bf16 bit patterns
     [N, ld].  Returns float64 arrays (m2, s, zy, owned)."""
     x = _bf16_to_f64(logits)
     N, ld = x.shape
@@ -264,10 +265,10 @@ def vocab_shard_stats(logits, vocab_start, token_ids, w=None, inv_temp=1.0, V=No
     s = np.zeros(N)
     zy = np.zeros(N)
     for k in range(N):
+        if w is not None and w[k] == 0:
+            continue  # an excluded row is not read: zy stays 0
         if owned[k]:
             zy[k] = x[k, yl[k]]
-        if w is not None and w[k] == 0:
-            continue
         mx = np.max(x[k])
         if mx == -np.inf:
             continue

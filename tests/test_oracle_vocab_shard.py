@@ -39,7 +39,7 @@ def test_excluded_and_all_minus_inf_rows():
     x = np.array([[1.0, 2.0, 3.0], [-np.inf, -np.inf, -np.inf], [0.5, 0.5, 0.5]])
     y = np.array([1, 0, 5], np.int32)
     m2, s, zy, owned = oracle.vocab_shard_stats(x, 0, y, w=np.array([0.0, 1.0, 1.0]))
-    assert m2[0] == -np.inf and s[0] == 0 and owned[0] == 1 and zy[0] == 2.0
+    assert m2[0] == -np.inf and s[0] == 0 and owned[0] == 1 and zy[0] == 0.0  # not read
     assert m2[1] == -np.inf and s[1] == 0
     assert owned[2] == 0 and zy[2] == 0
     # a uniform row: s = V exactly
