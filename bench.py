@@ -231,6 +231,64 @@ def cpu_baseline(s, seconds: float):
 MFMA_BF16_PEAK = 2.5e15  # MI355X dense bf16 matrix-core peak, flop/s
 
 
+def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
+    """The vocabulary-parallel entry points at one shard's real shape: the
+    first microbatch's rows, the first V / n_shards columns of the resident
+    logits (row stride V), n_shards partials for the merge (shard 0's own and
+    copies that own no token).  HIP events on the launch stream; median."""
+    V, R = s["V"], s["R"]
+    vs = V // n_shards
+    lg = s["logits"][:R]
+    dl = s["dlogits"][:R]
+    tok, w = s["tok"][:R], s["w_tok"][:R]
+    dev = lg.device
+    parts = torch.empty((n_shards, R, 4), dtype=torch.float32, device=dev)
+    state = torch.empty((R, 2), dtype=torch.float32, device=dev)
+    logp = torch.empty(R, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    ws_bytes = L.leap_vocab_merge_workspace_size(R)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return float(np.median(ms)) / 1e3
+
+    t_stats = timed(lambda: L.leap_vocab_shard_stats(lg, V, R, vs, 0, tok, w, 1.0, parts[0]))
+    parts[1:] = parts[0]
+    parts[1:, :, 3] = 0.0  # copies own no token
+    parts[1:, :, 2] = 0.0
+    owned0 = parts[0, :, 3].clone()
+    parts[0, :, 3] = 1.0  # every row's token counted once (timing only)
+    t_merge = timed(lambda: L.leap_vocab_merge_objective(
+        parts, n_shards, R, V, tok, s["old"][:R], s["ref"][:R], s["adv_tok"][:R], w, s["params"],
+        logp, None, loss, state, ws, ws_bytes, err))
+    parts[0, :, 3] = owned0
+    t_bwd = timed(lambda: L.leap_vocab_shard_bwd(lg, V, R, vs, 0, tok, state, 1.0, dl))
+    nv = int((w != 0).sum().item())
+    stats_bytes = nv * (2 * vs + 8) + R * 24
+    bwd_bytes = nv * (4 * vs + 12) + (R - nv) * (2 * vs + 12)
+    log(f"[bench] vocab shard {R} x {vs}: stats {t_stats * 1e6:.1f} us "
+        f"({stats_bytes / t_stats / 1e9:.0f} GB/s), merge of {n_shards} {t_merge * 1e6:.1f} us, "
+        f"bwd {t_bwd * 1e6:.1f} us ({bwd_bytes / t_bwd / 1e9:.0f} GB/s)")
+    return {"workload": f"one vocabulary shard: first microbatch ({R} rows, {nv} live) x "
+                        f"{vs} columns (V/{n_shards}), row stride {V}",
+            "stats_us": t_stats * 1e6, "stats_GBps": stats_bytes / t_stats / 1e9,
+            "merge_us": t_merge * 1e6, "bwd_us": t_bwd * 1e6, "bwd_GBps": bwd_bytes / t_bwd / 1e9,
+            "stats_frac": stats_bytes / t_stats / HBM_PEAK, "bwd_frac": bwd_bytes / t_bwd / HBM_PEAK}
+
+
 def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
     """fp32 log-softmax of hidden weight^T at y with torch, a block of rows at
     a time: input preparation for the old / reference log-probabilities."""
@@ -331,13 +389,17 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    # ~3 s of the real step: a fresh device settles its clocks over the first
+    # seconds of sustained traffic (the first process on a new box measured
+    # ~5% slower with 3 warm-up steps)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="mid", choices=["mid", "full"])
     ap.add_argument("--seed", type=int, default=1002)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lmhead-reps", type=int, default=5,
                     help="timed calls of the fused LM-head variant (0 skips it)")
+    ap.add_argument("--no-shard", action="store_true", help="skip the vocabulary-shard leg")
     ap.add_argument("--lmhead-only", action="store_true",
                     help="run only the fused LM-head leg and print its JSON object")
     args = ap.parse_args()
@@ -406,6 +468,7 @@ def main():
         log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
         cpu = cpu_baseline(s, args.cpu_seconds)
 
+    shard = shard_leg(L, torch, s) if not args.no_shard else None
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
     if args.lmhead_reps > 0:
@@ -438,6 +501,7 @@ def main():
                      "frac_of_probe_copy": achieved / 1e9 / probe["copy_GBps"]},
         "cpu_baseline": cpu,
         "lmhead": lm,
+        "vocab_shard": shard,
     }
     print(json.dumps(out), flush=True)
 

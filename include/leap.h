@@ -296,6 +296,72 @@ leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight
                                      size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
 
 /*
+ * Vocabulary-parallel form of the per-token objective (Sec. 3.1, Eq. 3 per
+ * token) for logits split by vocabulary across devices (each device holds
+ * columns [vocab_start, vocab_start + V_shard) of every row).  The three
+ * calls are the local halves of one exchange: every shard runs
+ * leap_vocab_shard_stats, the caller gathers the partials of all shards
+ * (e.g. one all-gather of N x 16 bytes per shard), every shard runs
+ * leap_vocab_merge_objective on the gathered partials, then
+ * leap_vocab_shard_bwd for its own slice of dlogits.  The results equal
+ * leap_grpo_logprob_loss_fwd_bwd on the concatenated rows up to fp32
+ * rounding of the log-sum-exp.
+ *
+ * leap_vocab_shard_stats: partial [N][4] float (16-byte aligned), per row
+ *   (m2, s, zy, owned) with c = log2(e) * inv_temperature,
+ *   m2 = c * max_v x_v, s = sum_v 2^(c x_v - m2) over the shard's columns,
+ *   owned = 1 and zy = x[y - vocab_start] when the token y = token_ids[k]
+ *   falls in the shard, else owned = 0, zy = 0.  A row with w_tok[k] == 0
+ *   (w_tok nullable) or whose shard columns are all -inf gives m2 = -inf,
+ *   s = 0 and is not read in the first case.
+ *   logits_bf16 [N][ld] bf16 holding the shard's V_shard columns; alignment
+ *   and range rules as leap_grpo_logprob_loss_fwd_bwd; vocab_start >= 0.
+ */
+leap_status leap_vocab_shard_stats(const void *logits_bf16, int64_t ld, int64_t N, int32_t V_shard,
+                                   int32_t vocab_start, const int32_t *token_ids,
+                                   const float *w_tok, float inv_temperature, float *partial,
+                                   hipStream_t stream);
+
+/* Workspace bytes leap_vocab_merge_objective needs for N rows. */
+size_t leap_vocab_merge_workspace_size(int64_t N);
+
+/*
+ * leap_vocab_merge_objective: partials [n_shards][N][4] float (shard-major,
+ *   16-byte aligned) from leap_vocab_shard_stats of every shard; the row's
+ *   log-sum-exp is merged over shards in index order, then the per-token
+ *   objective of leap_grpo_logprob_loss_fwd_bwd: logp_out, tok_loss_out
+ *   (nullable), loss_out (required, fixed-order sum), and row_state [N][2]
+ *   float (g, lse2 = log2 sum 2^(c x); 8-byte aligned), the input of
+ *   leap_vocab_shard_bwd.  An excluded row gets logp = loss = 0 and
+ *   row_state (0, +inf); a token id outside [0, V_total) with w != 0, a row
+ *   whose token no shard (or more than one shard) reports, or a row of all
+ *   -inf logits also counts in *dev_err.
+ * Errors: LEAP_ERR_INVALID_ARG (N < 0, n_shards < 1, V_total < 1, a
+ * parameter out of range, a required pointer NULL), LEAP_ERR_MISALIGNED,
+ * LEAP_ERR_WORKSPACE, LEAP_ERR_UNSUPPORTED (unknown kl_type).
+ */
+leap_status leap_vocab_merge_objective(const float *partials, int32_t n_shards, int64_t N,
+                                       int32_t V_total, const int32_t *token_ids,
+                                       const float *old_logp, const float *ref_logp,
+                                       const float *adv_tok, const float *w_tok,
+                                       const leap_grpo_params *params, float *logp_out,
+                                       float *tok_loss_out, float *loss_out, float *row_state,
+                                       void *workspace, size_t ws_bytes, int32_t *dev_err,
+                                       hipStream_t stream);
+
+/*
+ * leap_vocab_shard_bwd: dlogits[k][v] = g_k * ([vocab_start + v == y_k] -
+ *   2^(c x[k][v] - lse2_k)) in bf16 (RNE) for the shard's V_shard columns,
+ *   from row_state [N][2] of leap_vocab_merge_objective; a row with g == 0 is
+ *   zero-filled without reading its logits.  dlogits_bf16 [N][ld] may equal
+ *   logits_bf16, must not otherwise overlap it.
+ */
+leap_status leap_vocab_shard_bwd(const void *logits_bf16, int64_t ld, int64_t N, int32_t V_shard,
+                                 int32_t vocab_start, const int32_t *token_ids,
+                                 const float *row_state, float inv_temperature,
+                                 void *dlogits_bf16, hipStream_t stream);
+
+/*
  * Measurement helper, not part of the method: streams device memory with the
  * access shape of the fused kernel (16-byte non-temporal accesses) so the
  * achievable HBM rate of each access mix can be set beside the published

@@ -267,3 +267,29 @@ def test_lmhead_workspace_size():
     chunks = -(-v_pad // 8192)
     want = 2 * h * n + 2 * h * 8192 * chunks + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 8192
     assert abs(L.leap_lmhead_workspace_size(n, v, h) - want) <= 9 * 256
+
+
+def test_vocab_shard_entry_points_reject():
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_stats(FAKE, 1000, 8, 0, 0, FAKE, None, 1.0, FAKE, stream=0)
+    assert e.value.status == L.LEAP_ERR_INVALID_ARG
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_stats(FAKE, 1004, 8, 1000, 0, FAKE, None, 1.0, FAKE, stream=0)
+    assert e.value.status == L.LEAP_ERR_MISALIGNED
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_stats(FAKE, 1000, 8, 1000, -1, FAKE, None, 1.0, FAKE, stream=0)
+    assert e.value.status == L.LEAP_ERR_INVALID_ARG
+    ws = L.leap_vocab_merge_workspace_size(8)
+    assert ws % 256 == 0 and ws >= 32
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_merge_objective(FAKE, 0, 8, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, p, None, None,
+                                     FAKE, FAKE, FAKE, ws, stream=0)
+    assert e.value.status == L.LEAP_ERR_INVALID_ARG
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_merge_objective(FAKE, 2, 8, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, p, None, None,
+                                     FAKE, FAKE, FAKE, 16, stream=0)
+    assert e.value.status == L.LEAP_ERR_WORKSPACE
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_bwd(FAKE, 1000, 8, 1000, 0, FAKE, FAKE, 1.0, FAKE + 2048, stream=0)
+    assert e.value.status == L.LEAP_ERR_INVALID_ARG  # partial overlap with the logits
