@@ -21,6 +21,9 @@ over ctypes with numpy arrays.  Functions and the passages they follow:
   (fused LM head), with dH = dZ W and dW = dZ^T H.
 * ``vocab_shard_stats`` -- one vocabulary shard's share of a row's
   log-softmax normaliser (max and base-2 sum) and of its token logit.
+* ``rollout_stats``    -- the training statistics of the pruning study
+  (activated groups, per-rollout / per-group recovery), turns per pass, and
+  the pass-rate-bucketed advantage-sign composition of rollouts.
 """
 from __future__ import annotations
 
@@ -77,6 +80,8 @@ def _load():
     lib.leap_oracle_grpo_rows_bf16.argtypes = row_args
     lib.leap_oracle_logprob_rows_bf16.restype = i64
     lib.leap_oracle_logprob_rows_bf16.argtypes = [P, i64, i64, i32, P, f64, P]
+    lib.leap_oracle_rollout_stats.restype = i64
+    lib.leap_oracle_rollout_stats.argtypes = [P, P, P, P, i64, i32, i32, i32, P]
     _lib = lib
     return lib
 
@@ -275,6 +280,37 @@ def vocab_shard_stats(logits, vocab_start, token_ids, w=None, inv_temp=1.0, V=No
         m2[k] = c * mx
         s[k] = np.sum(np.exp2(c * x[k] - m2[k]))
     return m2, s, zy, owned
+
+
+STAT_FIELDS = ("groups", "rollouts", "activated_groups", "multi_turn_rollouts",
+               "recovered_rollouts", "debugging_groups", "recovered_groups", "total_turns",
+               "passed_rollouts")
+
+
+def rollout_stats(pass_turn, n_turns, gate, G, M, advantage=None, n_buckets=10):
+    """Counters of ``leap_oracle_rollout_stats`` as a dict (STAT_FIELDS, plus
+    ``composition`` int64 [n_buckets, 3, 2]: outcome immediate / debug-assisted
+    / failure x advantage sign positive / negative), the derived rates
+    (activated fraction, per-rollout and per-group recovery, turns per pass;
+    None where the denominator is 0) and ``bad``."""
+    lib = _load()
+    pt = _c(pass_turn, np.int32)
+    nt = _c(n_turns, np.int32)
+    gt = _c(gate, np.uint8)
+    n_groups = gt.size
+    adv = None if advantage is None else _c(advantage, np.float64)
+    cnt = np.zeros(9 + n_buckets * 6, np.int64)
+    bad = lib.leap_oracle_rollout_stats(_p(pt), _p(nt), _p(gt), _p(adv), n_groups, int(G),
+                                        int(M), int(n_buckets), _p(cnt))
+    out = {k: int(v) for k, v in zip(STAT_FIELDS, cnt[:9])}
+    out["composition"] = cnt[9:].reshape(n_buckets, 3, 2)
+    ratio = lambda a, b: (a / b) if b else None  # noqa: E731
+    out["activated_fraction"] = ratio(out["activated_groups"], out["groups"])
+    out["per_rollout_recovery"] = ratio(out["recovered_rollouts"], out["multi_turn_rollouts"])
+    out["per_group_recovery"] = ratio(out["recovered_groups"], out["debugging_groups"])
+    out["turns_per_pass"] = ratio(out["total_turns"], out["passed_rollouts"])
+    out["bad"] = int(bad)
+    return out
 
 
 def tau_from_pass_rate(G: int, lo: Fraction, lo_strict: bool, hi: Fraction, hi_strict: bool):

@@ -460,3 +460,83 @@ int64_t leap_oracle_logprob_rows_bf16(const uint16_t *logits, int64_t ld,
     }
     return bad;
 }
+
+/*
+ * Training statistics of the method (test infrastructure like the rest).
+ *
+ * Definitions followed:
+ *   - pruning-range study (Sec. 4, the DCP analysis): "activated groups" =
+ *     groups whose gate sends them to multi-turn debugging; "per-rollout
+ *     recovery" = among the trajectories that failed their first turn and
+ *     entered debugging, those that later pass; "per-group recovery" = among
+ *     the groups that ran debugging, those with at least one recovered
+ *     trajectory;
+ *   - method comparison (turn efficiency): total turns used by all samples,
+ *     and passed samples (the ratio is turns per pass);
+ *   - rollout-composition analysis: rollouts with a nonzero advantage,
+ *     bucketed by the observed pass rate of their group, split by outcome
+ *     (immediate pass, debug-assisted pass, failure) and advantage sign.
+ *
+ * counters[0..8]: groups, rollouts, activated groups, multi-turn
+ * trajectories, recovered trajectories, debugging groups, recovered groups,
+ * total turns, passed rollouts; then comp[b][o][s] (b < n_buckets, o in 0..2,
+ * s: 0 positive, 1 negative) at counters[9 + (b*3 + o)*2 + s].  The bucket
+ * of a group with n_pass passes is floor(n_pass * n_buckets / G), the top
+ * bucket also holding n_pass = G.  A rollout with pass_turn outside 0..M or
+ * n_turns < 1 is skipped everywhere and counted in the return value.
+ * advantage may be NULL (no composition).
+ */
+int64_t leap_oracle_rollout_stats(const int32_t *pass_turn, const int32_t *n_turns,
+                                  const uint8_t *gate, const double *advantage,
+                                  int64_t n_groups, int32_t G, int32_t M, int32_t n_buckets,
+                                  int64_t *counters)
+{
+    int64_t bad = 0;
+    const int64_t n_counters = 9 + (int64_t)n_buckets * 6;
+    for (int64_t k = 0; k < n_counters; ++k) counters[k] = 0;
+    counters[0] = n_groups;
+    counters[1] = n_groups * (int64_t)G;
+    for (int64_t g = 0; g < n_groups; ++g) {
+        const int64_t base = g * (int64_t)G;
+        const int activated = gate[g] != 0;
+        int64_t n_pass = 0, n_multi = 0, n_recovered = 0;
+        for (int32_t i = 0; i < G; ++i) {
+            const int32_t m = pass_turn[base + i];
+            const int32_t T = n_turns[base + i];
+            if (m < 0 || m > M || T < 1) {
+                ++bad;
+                continue;
+            }
+            counters[7] += T;
+            if (m >= 1) ++n_pass;
+            if (activated && m != 1) {  /* first turn failed: debugging ran */
+                ++n_multi;
+                if (m >= 2) ++n_recovered;
+            }
+        }
+        counters[8] += n_pass;
+        if (activated) {
+            ++counters[2];
+            counters[3] += n_multi;
+            counters[4] += n_recovered;
+            if (n_multi > 0) {
+                ++counters[5];
+                if (n_recovered > 0) ++counters[6];
+            }
+        }
+        if (advantage == NULL || n_buckets < 1) continue;
+        int64_t b = n_pass * (int64_t)n_buckets / G;
+        if (b > n_buckets - 1) b = n_buckets - 1;
+        for (int32_t i = 0; i < G; ++i) {
+            const int32_t m = pass_turn[base + i];
+            const int32_t T = n_turns[base + i];
+            if (m < 0 || m > M || T < 1) continue;
+            const double a = advantage[base + i];
+            if (a == 0.0 || a != a) continue;
+            const int o = (m == 1) ? 0 : (m >= 2 ? 1 : 2);
+            const int s = a > 0.0 ? 0 : 1;
+            ++counters[9 + (b * 3 + o) * 2 + s];
+        }
+    }
+    return bad;
+}
