@@ -303,6 +303,34 @@ def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
     return out
 
 
+def stats_leg(L, torch, s, n_buckets: int = 10, reps: int = 20):
+    """The step's training statistics (activated groups, recovery rates,
+    turns per pass, advantage-sign composition) from its own gate, outcomes
+    and advantages, with the call's median time."""
+    ro = s["ro"]
+    G, M = s["G"], s["M"]
+    n_groups = ro.n_rollouts // G
+    cnt = torch.empty(9 + 6 * n_buckets, dtype=torch.int64, device=s["gate"].device)
+    stream = torch.cuda.current_stream()
+    ms = []
+    for _ in range(reps + 1):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        L.leap_rollout_stats(s["pass_turn"], s["n_turns"], s["gate"], s["adv_roll"], n_groups, G, M,
+                             n_buckets, cnt, s["err"])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    out = L.rollout_stats_summary(cnt.cpu().numpy(), n_buckets)
+    out["call_us"] = float(np.median(ms[1:])) * 1e3
+    out["n_buckets"] = n_buckets
+    log(f"[bench] rollout stats: activated {out['activated_fraction']:.3f}, per-rollout recovery "
+        f"{out['per_rollout_recovery']}, per-group recovery {out['per_group_recovery']}, "
+        f"turns/pass {out['turns_per_pass']:.3f} ({out['call_us']:.1f} us)")
+    return out
+
+
 def lmhead_leg(L, torch, dev, seed: int, reps: int):
     """The fused LM-head variant on one 16384-row microbatch of the LM-head
     workload (hidden [16384 x 4096] ~ N(0,1), weight [151936 x 4096] ~
@@ -469,6 +497,7 @@ def main():
         cpu = cpu_baseline(s, args.cpu_seconds)
 
     shard = shard_leg(L, torch, s) if not args.no_shard else None
+    rstats = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
     if args.lmhead_reps > 0:
@@ -502,6 +531,7 @@ def main():
         "cpu_baseline": cpu,
         "lmhead": lm,
         "vocab_shard": shard,
+        "rollout_stats": rstats,
     }
     print(json.dumps(out), flush=True)
 

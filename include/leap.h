@@ -362,6 +362,38 @@ leap_status leap_vocab_shard_bwd(const void *logits_bf16, int64_t ld, int64_t N,
                                  void *dlogits_bf16, hipStream_t stream);
 
 /*
+ * Training statistics of one step's rollouts, as the paper defines them
+ * (Sec. 4): the pruning-range study's activated groups (gate = 1),
+ * per-rollout recovery (trajectories of activated groups whose first turn
+ * failed, and of those the ones that passed on a later turn) and per-group
+ * recovery (activated groups that ran at least one such trajectory, and of
+ * those the ones with at least one recovery); the turn efficiency (total
+ * turns of all rollouts over passed rollouts); and the rollout-composition
+ * analysis: rollouts with a nonzero advantage, by the observed pass rate of
+ * their group (bucket floor(n_pass * n_buckets / G), the top bucket also
+ * holding n_pass = G), outcome (immediate pass, debug-assisted pass,
+ * failure) and advantage sign.
+ *
+ * pass_turn, n_turns  int32 [n_groups*G] (0 = never passed, else the turn of
+ *   first pass; T_i turns generated).  gate uint8 [n_groups].
+ * advantage float [n_groups*G], nullable (no composition then).
+ * counters int64 [9 + 6*n_buckets], 8-byte aligned, overwritten:
+ *   [0] groups [1] rollouts [2] activated groups [3] multi-turn trajectories
+ *   [4] recovered trajectories [5] debugging groups [6] recovered groups
+ *   [7] total turns [8] passed rollouts, then [9 + (b*3 + o)*2 + s] for
+ *   bucket b, outcome o (0 immediate, 1 debug-assisted, 2 failure), sign s
+ *   (0 positive, 1 negative).  Integer counts: exact, order independent.
+ * A rollout with pass_turn outside 0..M or n_turns < 1 is skipped and counts
+ * in *dev_err.
+ * Errors: LEAP_ERR_INVALID_ARG for n_groups < 0, G outside 1..1024, M < 1,
+ * n_buckets outside 1..256, a required pointer NULL; LEAP_ERR_MISALIGNED.
+ */
+leap_status leap_rollout_stats(const int32_t *pass_turn, const int32_t *n_turns,
+                               const uint8_t *gate, const float *advantage, int64_t n_groups,
+                               int32_t G, int32_t M, int32_t n_buckets, int64_t *counters,
+                               int32_t *dev_err, hipStream_t stream);
+
+/*
  * Measurement helper, not part of the method: streams device memory with the
  * access shape of the fused kernel (16-byte non-temporal accesses) so the
  * achievable HBM rate of each access mix can be set beside the published

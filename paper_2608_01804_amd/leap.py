@@ -43,6 +43,7 @@ EXPORTED = (
     "leap_vocab_merge_workspace_size",
     "leap_vocab_merge_objective",
     "leap_vocab_shard_bwd",
+    "leap_rollout_stats",
     "leap_probe_hbm",
 )
 
@@ -113,6 +114,8 @@ def lib() -> ctypes.CDLL:
                                              ctypes.c_size_t, P, P]
     L.leap_vocab_shard_bwd.restype = ctypes.c_int
     L.leap_vocab_shard_bwd.argtypes = [P, i64, i64, i32, i32, P, P, f32, P, P]
+    L.leap_rollout_stats.restype = ctypes.c_int
+    L.leap_rollout_stats.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P]
     L.leap_probe_hbm.restype = ctypes.c_int
     L.leap_probe_hbm.argtypes = [P, P, ctypes.c_size_t, i32, P]
     _lib = L
@@ -303,6 +306,36 @@ def leap_vocab_shard_bwd(logits, ld, N, V_shard, vocab_start, token_ids, row_sta
         _ptr(token_ids, "int32", "token_ids"), _ptr(row_state, "float32", "row_state"),
         float(inv_temperature), _ptr(dlogits, "bfloat16", "dlogits"), _stream(stream))
     _check(st, "leap_vocab_shard_bwd")
+
+
+def leap_rollout_stats(pass_turn, n_turns, gate, advantage, n_groups, G, M, n_buckets, counters,
+                       dev_err=None, stream=None) -> None:
+    st = lib().leap_rollout_stats(
+        _ptr(pass_turn, "int32", "pass_turn"), _ptr(n_turns, "int32", "n_turns"),
+        _ptr(gate, "uint8", "gate"), _ptr(advantage, "float32", "advantage"), int(n_groups),
+        int(G), int(M), int(n_buckets), _ptr(counters, "int64", "counters"),
+        _ptr(dev_err, "int32", "dev_err"), _stream(stream))
+    _check(st, "leap_rollout_stats")
+
+
+STAT_FIELDS = ("groups", "rollouts", "activated_groups", "multi_turn_rollouts",
+               "recovered_rollouts", "debugging_groups", "recovered_groups", "total_turns",
+               "passed_rollouts")
+
+
+def rollout_stats_summary(counters, n_buckets):
+    """Named counters and derived rates from the int64 counter array that
+    leap_rollout_stats wrote (host-side arithmetic on its output only)."""
+    c = [int(v) for v in counters]
+    out = dict(zip(STAT_FIELDS, c[:9]))
+    out["composition"] = [[c[9 + (b * 3 + o) * 2: 9 + (b * 3 + o) * 2 + 2] for o in range(3)]
+                          for b in range(n_buckets)]
+    ratio = lambda a, b: (a / b) if b else None  # noqa: E731
+    out["activated_fraction"] = ratio(out["activated_groups"], out["groups"])
+    out["per_rollout_recovery"] = ratio(out["recovered_rollouts"], out["multi_turn_rollouts"])
+    out["per_group_recovery"] = ratio(out["recovered_groups"], out["debugging_groups"])
+    out["turns_per_pass"] = ratio(out["total_turns"], out["passed_rollouts"])
+    return out
 
 
 def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:

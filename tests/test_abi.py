@@ -293,3 +293,31 @@ def test_vocab_shard_entry_points_reject():
     with pytest.raises(L.LeapError) as e:
         L.leap_vocab_shard_bwd(FAKE, 1000, 8, 1000, 0, FAKE, FAKE, 1.0, FAKE + 2048, stream=0)
     assert e.value.status == L.LEAP_ERR_INVALID_ARG  # partial overlap with the logits
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_groups=-1), L.LEAP_ERR_INVALID_ARG),
+    (dict(G=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(G=1025), L.LEAP_ERR_INVALID_ARG),
+    (dict(M=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(n_buckets=0), L.LEAP_ERR_INVALID_ARG),
+    (dict(n_buckets=257), L.LEAP_ERR_INVALID_ARG),
+    (dict(counters=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(gate=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(counters=FAKE + 4), L.LEAP_ERR_MISALIGNED),
+])
+def test_rollout_stats_rejects(kw, status):
+    a = dict(pass_turn=FAKE, n_turns=FAKE, gate=FAKE, advantage=None, n_groups=4, G=8, M=2,
+             n_buckets=10, counters=FAKE, dev_err=None, stream=0)
+    a.update(kw)
+    with pytest.raises(L.LeapError) as e:
+        L.leap_rollout_stats(**a)
+    assert e.value.status == status
+
+
+def test_rollout_stats_summary_is_host_arithmetic_on_counters():
+    c = [4, 16, 3, 7, 2, 2, 1, 29, 9] + [0] * 24
+    c[9 + (3 * 3 + 0) * 2 + 0] = 1
+    s = L.rollout_stats_summary(c, 4)
+    assert s["activated_fraction"] == 0.75 and s["per_group_recovery"] == 0.5
+    assert s["turns_per_pass"] == 29 / 9 and s["composition"][3][0] == [1, 0]
