@@ -5,7 +5,7 @@
 //
 // Steps of one call, all on the caller's stream:
 //  1. H and W are transposed once into the workspace (Ht [H][N_pad]; Wt
-//     chunk-major, [chunk][H][8192], so its rows are 16 KiB apart; both zero
+//     chunk-major, [chunk][H][16384], so its rows are 32 KiB apart; both zero
 //     padded), because every GEMM below runs on one NT core whose operands
 //     are both contiguous along the contraction index.
 //  2. Stats GEMM  Z = H W^T on MFMA.  Its epilogue turns every row of a
@@ -15,7 +15,7 @@
 //     into the log-sum-exp and evaluates the same per-token objective as the
 //     logits-resident kernel (log-prob, ratio, surrogate, KL, loss and
 //     g = w dloss/dlogp / T).  A fixed-order reduction sums the loss.
-//  4. Per vocabulary chunk of up to 8192 columns: the Z tiles are recomputed
+//  4. Per vocabulary chunk of up to 16384 columns: the Z tiles are recomputed
 //     and the epilogue writes dZ = g (onehot - p) in bf16, row-major
 //     [N_pad][chunk] and transposed [chunk][N_pad]; then dW[chunk] = dZ^T H
 //     and dH (+)= dZ W[chunk] run as two more GEMMs with fp32 epilogues.
@@ -38,7 +38,7 @@ using row::u32x4;
 using row::wave_ms_reduce;
 
 #ifndef LEAP_LM_CHUNK
-#define LEAP_LM_CHUNK 8192
+#define LEAP_LM_CHUNK 16384
 #endif
 constexpr int kChunkCols = LEAP_LM_CHUNK;  // vocabulary columns per backward chunk
 constexpr int kTile = gemm::kBM;  // 256: rows and columns of a GEMM tile

@@ -259,13 +259,13 @@ def test_lmhead_workspace_size():
     assert L.leap_lmhead_workspace_size(8, 0, 64) == 0
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
-    # 16384 x 151936 x 4096: transposes (H*N_pad, and H*8192 per vocabulary
+    # 16384 x 151936 x 4096: transposes (H*N_pad, and H*16384 per vocabulary
     # chunk, bf16), per-tile row
-    # statistics, four per-row vectors and one 8192-column chunk of dZ in two layouts
+    # statistics, four per-row vectors and one 16384-column chunk of dZ in two layouts
     n, v, h = 16384, 151936, 4096
     v_pad = (v + 255) // 256 * 256
-    chunks = -(-v_pad // 8192)
-    want = 2 * h * n + 2 * h * 8192 * chunks + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 8192
+    chunks = -(-v_pad // 16384)
+    want = 2 * h * n + 2 * h * 16384 * chunks + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 16384
     assert abs(L.leap_lmhead_workspace_size(n, v, h) - want) <= 9 * 256
 
 

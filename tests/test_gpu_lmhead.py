@@ -57,9 +57,10 @@ def test_lmhead_reduced_shape_full_parity():
 
 @pytest.mark.parametrize("N,V,H,inv_temp,kl_type", [
     (300, 1000, 128, 0.8, 1),     # ragged rows and vocabulary, one chunk
-    (257, 8492, 64, 1.0, 2),      # two chunks, the last one 512 wide with 300 live columns
+    (257, 8492, 64, 1.0, 2),      # one chunk, 8704 wide with 8492 live columns
     (1, 300, 64, 1.0, 0),         # a single row, one k-tile
-    (513, 16640, 128, 1.25, 0),   # three chunks, the last one 256 wide
+    (513, 16640, 128, 1.25, 0),   # two 16384-column chunks, the last one 256 wide
+    (129, 33000, 64, 1.0, 1),     # three chunks, the last 256 wide with 232 live columns
 ])
 def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
     U.log(f"lmhead ragged N={N} V={V} H={H} T^-1={inv_temp} kl={kl_type}")
