@@ -6,17 +6,19 @@
 //    grid, each wave a 128 x 128 block of 4 x 4 v_mfma_f32_32x32x16_bf16
 //    tiles (256 fp32 accumulators per lane, one wave per SIMD).
 //  * Operand k-tiles go straight from HBM to LDS (buffer_load_dwordx4 ... lds,
-//    no VGPR staging) into two stages of 64 KiB; each row's 128-byte
-//    k-segment is one cache line fetched by one instruction.  The compiler
-//    does not track these LDS writes, so each wave waits on its own vmcnt
-//    before the stage barrier.
-//  * A k-tile is four k = 16 sub-steps; the fragments of the next sub-step
-//    (across the barrier, the next k-tile's first) are read from LDS while
-//    the current 16 MFMAs run, one read per two MFMAs, and the next k-tile's
-//    loads are spread one per MFMA after the barrier.  The per-CU vector
-//    memory path (about 32 bytes per clock) is what a 256 x 256 bf16 tile
-//    needs at the full MFMA rate, so keeping loads in flight under the MFMAs
-//    is what sets the achieved rate.
+//    no VGPR staging); each row's 128-byte k-segment is one cache line
+//    fetched by one instruction.  LDS holds two A slots and three B slots of
+//    32 KiB (160 KiB): A k-tiles are loaded one k-tile ahead, B k-tiles two.
+//    The compiler does not track these LDS writes, so each wave waits on its
+//    own vmcnt before the stage barrier.
+//  * The per-CU vector memory path moves about 32 bytes per clock, which is
+//    what a 256 x 256 bf16 tile consumes at the full MFMA rate, and a wave
+//    whose load cannot be accepted stalls its MFMA stream too.  So the 16
+//    loads of a k-tile are spread one per four MFMAs over the whole k-tile
+//    (second half of A(kt+1), then B(kt+2), then after the barrier the first
+//    half of A(kt+2)), and the fragments of the next k = 16 sub-step are read
+//    from LDS two per four MFMAs, in fenced groups of
+//    [2 MFMA | load | 2 LDS reads + 2 MFMA].
 //  * LDS rows are 128 bytes (64 bf16); the 16-byte chunk c of row r sits at
 //    position c ^ ((r >> 1) & 7), so the 16-row MFMA fragment reads hit
 //    distinct banks, and every load instruction fills 1 KiB contiguously.
@@ -41,11 +43,11 @@ typedef uint32_t u32x4g __attribute__((ext_vector_type(4)));
 constexpr int kBM = 256;
 constexpr int kBN = 256;
 constexpr int kBK = 64;
-constexpr int kStages = 2;
+constexpr int kASlots = 2;  // A k-tiles in LDS
+constexpr int kBSlots = 3;  // B k-tiles in LDS
 constexpr int kThreads = 256;
 constexpr int kTileBytes = kBM * kBK * 2;        // one operand k-tile in LDS (32 KiB)
-constexpr int kStageBytes = 2 * kTileBytes;      // A and B
-constexpr int kLdsBytes = kStages * kStageBytes;  // 128 KiB
+constexpr int kLdsBytes = (kASlots + kBSlots) * kTileBytes;  // 160 KiB
 // Word 3 of a raw gfx9 buffer descriptor (32-bit data format, no swizzle).
 constexpr int kGemmBufferFlags = 0x00020000;
 constexpr int kXcds = 8;
@@ -141,8 +143,9 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(A), 0, a_bytes, kGemmBufferFlags);
     const __amdgpu_buffer_rsrc_t rb =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(B), 0, b_bytes, kGemmBufferFlags);
-    // zero extent: loads through it fetch nothing and deliver zeros
-    const __amdgpu_buffer_rsrc_t r0 =
+    // zero extent: loads through it fetch nothing and deliver zeros; used for
+    // the slots past the last k-tile so every path issues the same stream
+    const __amdgpu_buffer_rsrc_t rz =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(A), 0, 0, kGemmBufferFlags);
     // DMA mapping: instruction q (0..7) of wave w fills rows (8w + q)*8 .. +7
     // of a 256-row operand tile (1 KiB, LDS-contiguous); lane l writes row
@@ -155,100 +158,102 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
         voff_a[q] = static_cast<uint32_t>((static_cast<int64_t>(tm) * kBM + r) * lda * 2 + c * 16);
         voff_b[q] = static_cast<uint32_t>((static_cast<int64_t>(tn) * kBN + r) * ldb * 2 + c * 16);
     }
-    // Loads of k-tile kt into stage `stage`; live == false sends the same
-    // instructions through the zero-extent descriptor (no memory traffic),
-    // which keeps the instruction stream identical on every path.
-    auto issue = [&](int kt, int stage, bool live) {
-        uint8_t* st = smem + stage * kStageBytes;
-        const int koff = kt * kBK * 2;
-        const __amdgpu_buffer_rsrc_t sa = live ? ra : r0;
-        const __amdgpu_buffer_rsrc_t sb = live ? rb : r0;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                sa, (__attribute__((address_space(3))) void*)(st + (wave * 8 + q) * 1024), 16,
-                voff_a[q], koff, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                sb, (__attribute__((address_space(3))) void*)(st + kTileBytes + (wave * 8 + q) * 1024),
-                16, voff_b[q], koff, 0, 0);
-        }
+    const int KT = K / kBK;
+    // load q of A k-tile kt into its slot kt % 2 (zeros past the last k-tile)
+    auto dma_a = [&](int kt, int q) {
+        const bool live = kt < KT;
+        uint8_t* st = smem + (kt & 1) * kTileBytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            live ? ra : rz, (__attribute__((address_space(3))) void*)(st + (wave * 8 + q) * 1024), 16,
+            voff_a[q], (live ? kt : 0) * kBK * 2, 0, 0);
     };
-    auto read = [&](int stage, int s, bf16x8(&af)[4], bf16x8(&bf)[4]) {
-        // the previous sub-step's fragments landed during the MFMAs since
-        // they were read; waiting here keeps at most 8 LDS reads in flight
-        wait_lgkmcnt0();
-        const uint8_t* sa = smem + stage * kStageBytes;
-        const uint8_t* sb = sa + kTileBytes;
+    // load q of B k-tile kt into B slot `slot` (== kt % 3)
+    auto dma_b = [&](int kt, int slot, int q) {
+        const bool live = kt < KT;
+        uint8_t* st = smem + (kASlots + slot) * kTileBytes;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            live ? rb : rz, (__attribute__((address_space(3))) void*)(st + (wave * 8 + q) * 1024), 16,
+            voff_b[q], (live ? kt : 0) * kBK * 2, 0, 0);
+    };
+    // fragment f of sub-step s (f < 4: A rows block f; else B columns block f - 4)
+    auto read1 = [&](int as, int bsl, int s, int f, bf16x8(&af)[4], bf16x8(&bf)[4]) {
         const int c = 2 * s + (lane >> 5);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            af[i] = *reinterpret_cast<const bf16x8*>(sa + lds_off(wm * 128 + i * 32 + (lane & 31), c));
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            bf[j] = *reinterpret_cast<const bf16x8*>(sb + lds_off(wn * 128 + j * 32 + (lane & 31), c));
-    };
-    auto mma = [&](const bf16x8(&af)[4], const bf16x8(&bf)[4]) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-    };
-    // one LDS read per two MFMAs
-    auto spread_reads = [&]() {
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+        if (f < 4) {
+            const uint8_t* sa = smem + as * kTileBytes;
+            af[f] = *reinterpret_cast<const bf16x8*>(sa + lds_off(wm * 128 + f * 32 + (lane & 31), c));
+        } else {
+            const uint8_t* sb = smem + (kASlots + bsl) * kTileBytes;
+            bf[f - 4] = *reinterpret_cast<const bf16x8*>(sb + lds_off(wn * 128 + (f - 4) * 32 + (lane & 31), c));
         }
-        __builtin_amdgcn_sched_barrier(0);
+    };
+    // The 16 MFMAs of one sub-step on (xa, xb); meanwhile the fragments of
+    // the next sub-step s into (ya, yb) (s < 0: none) and the four loads
+    // dma(0..3), in four fenced groups [2 MFMA | load | 2 reads + 2 MFMA].
+    // The wait first: the fragments in use were read a sub-step ago.
+    auto batch = [&](const bf16x8(&xa)[4], const bf16x8(&xb)[4], int as, int bsl, int s,
+                     bf16x8(&ya)[4], bf16x8(&yb)[4], auto&& dma) {
+        wait_lgkmcnt0();
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                acc[g][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[g], xb[u], acc[g][u], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            dma(g);
+            __builtin_amdgcn_sched_barrier(0);
+            if (s >= 0) {
+                read1(as, bsl, s, 2 * g, ya, yb);
+                read1(as, bsl, s, 2 * g + 1, ya, yb);
+            }
+#pragma unroll
+            for (int u = 2; u < 4; ++u)
+                acc[g][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[g], xb[u], acc[g][u], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
 
-    // k-tile kt lives in stage kt % 2; k-tile kt + 2 refills stage kt % 2
-    // after the barrier that ends k-tile kt.
-    const int KT = K / kBK;
-    issue(0, 0, true);
-    issue(KT > 1 ? 1 : 0, 1, KT > 1);
-    wait_vmcnt<16>();
+    // A k-tile t in A slot t % 2, B k-tile t in B slot t % 3.  Per k-tile kt:
+    // batch 1 loads the second half of A(kt+1), batches 2-3 load B(kt+2),
+    // batch 4 (after the barrier) loads the first half of A(kt+2).
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_a(0, q);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_b(0, 0, q);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_b(1, 1, q);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dma_a(1, q);
+    wait_vmcnt<12>();  // A(0), B(0) landed; B(1) and half of A(1) may fly
     stage_barrier();
     bf16x8 a0[4], b0[4], a1[4], b1[4];
-    read(0, 0, a0, b0);
-    for (int kt = 0; kt + 1 < KT; ++kt) {
-        const int cur = kt & 1;
-        read(cur, 1, a1, b1);
-        mma(a0, b0);
-        spread_reads();
-        read(cur, 2, a0, b0);
-        mma(a1, b1);
-        spread_reads();
-        read(cur, 3, a1, b1);
-        mma(a0, b0);
-        spread_reads();
-        // k-tile kt + 1 has landed everywhere and stage kt % 2 is free
-        wait_vmcnt<0>();
-        stage_barrier();
-        read(cur ^ 1, 0, a0, b0);
-        issue(kt + 2 < KT ? kt + 2 : 0, cur, kt + 2 < KT);
-        mma(a1, b1);
+    wait_lgkmcnt0();
 #pragma unroll
-        for (int g = 0; g < 16; ++g) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read (LDS DMA)
-        }
-        __builtin_amdgcn_sched_barrier(0);
+    for (int f = 0; f < 8; ++f) read1(0, 0, 0, f, a0, b0);
+    int bs = 0;  // B slot of k-tile kt
+    for (int kt = 0; kt + 1 < KT; ++kt) {
+        const int as = kt & 1;
+        const int b2 = bs == 0 ? 2 : bs - 1;  // slot of B(kt+2) == slot of B(kt-1)
+        const int bn = bs == 2 ? 0 : bs + 1;
+        batch(a0, b0, as, bs, 1, a1, b1, [&](int g) { dma_a(kt + 1, 4 + g); });
+        batch(a1, b1, as, bs, 2, a0, b0, [&](int g) { dma_b(kt + 2, b2, g); });
+        batch(a0, b0, as, bs, 3, a1, b1, [&](int g) { dma_b(kt + 2, b2, 4 + g); });
+        // A(kt+1) and B(kt+1) have landed (only B(kt+2) may still fly); after
+        // the barrier A slot kt % 2 and B slot kt % 3 are free
+        wait_vmcnt<8>();
+        stage_barrier();
+        batch(a1, b1, as ^ 1, bn, 0, a0, b0, [&](int g) { dma_a(kt + 2, g); });
+        bs = bn;
     }
     {
-        const int cur = (KT - 1) & 1;
-        read(cur, 1, a1, b1);
-        mma(a0, b0);
-        read(cur, 2, a0, b0);
-        mma(a1, b1);
-        read(cur, 3, a1, b1);
-        mma(a0, b0);
-        mma(a1, b1);
+        const int as = (KT - 1) & 1;
+        auto none = [&](int) {};
+        batch(a0, b0, as, bs, 1, a1, b1, none);
+        batch(a1, b1, as, bs, 2, a0, b0, none);
+        batch(a0, b0, as, bs, 3, a1, b1, none);
+        batch(a1, b1, as, bs, -1, a0, b0, none);
     }
-    // the zero-filling loads of the last slot have landed, every wave is
-    // past its LDS reads: the epilogue may reuse the LDS
+    // the zero-filling loads of the slots past the end have landed and every
+    // wave is past its LDS reads: the epilogue may reuse the LDS
     wait_vmcnt<0>();
     stage_barrier();
 }
