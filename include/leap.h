@@ -270,8 +270,8 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  *              aligned.  H % 64 == 0 (else LEAP_ERR_UNSUPPORTED).
  * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
  * logp_out, tok_loss_out  float [N], nullable.  loss_out float [1], required.
- * dhidden    float [N][H], overwritten; NULL skips it.
- * dweight    float [V][H]; overwritten (accumulate_dweight = 0) or added to
+ * dhidden    float [N][H], 16-byte aligned, overwritten; NULL skips it.
+ * dweight    float [V][H], 16-byte aligned; overwritten (accumulate_dweight = 0) or added to
  *            (accumulate_dweight = 1); NULL skips it.  With both gradients
  *            NULL only the forward outputs are computed.
  * workspace  device buffer of >= leap_lmhead_workspace_size(N, V, H) bytes,

@@ -354,8 +354,10 @@ struct DzEpi {
     }
 };
 
-// fp32 result tile into C[rows][cols] (leading dimension ldc): stored, or
-// added to what C holds.
+// fp32 result tile into C[rows][cols] (leading dimension ldc, 16-byte aligned
+// rows): stored, or added to what C holds.  The 4 x 4 transpose inside each
+// lane quad gives every lane 4 consecutive columns of one row, so each store
+// (and each load of the accumulating form) moves 16 bytes per lane.
 template <bool ACCUMULATE>
 struct StoreF32Epi {
     float* C;
@@ -364,18 +366,31 @@ struct StoreF32Epi {
     int cols;
 
     __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t*) const {
-        const int lane = t.lane;
+        const int lane = t.lane, half = (lane >> 5) & 1;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int n = t.col0() + j * 32 + (lane & 31);
+                const int n0 = t.col0() + j * 32 + ((lane & 31) & ~3);  // the quad's first column
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int64_t m = t.row0() + i * 32 + acc_row(r, lane);
-                    if (m < rows && n < cols) {
-                        float* p = C + m * ldc + n;
-                        *p = ACCUMULATE ? *p + acc[i][j][r] : acc[i][j][r];
+                for (int q = 0; q < 4; ++q) {
+                    float d[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                  acc[i][j][4 * q + 3]};
+                    quad_transpose(d, lane);
+                    const int64_t m = t.row0() + i * 32 + q * 8 + half * 4 + (lane & 3);
+                    if (m >= rows) continue;
+                    float* p = C + m * ldc + n0;
+                    if (n0 + 3 < cols) {
+                        float4 v = make_float4(d[0], d[1], d[2], d[3]);
+                        if (ACCUMULATE) {
+                            const float4 o = *reinterpret_cast<const float4*>(p);
+                            v.x += o.x, v.y += o.y, v.z += o.z, v.w += o.w;
+                        }
+                        *reinterpret_cast<float4*>(p) = v;
+                    } else {
+#pragma unroll
+                        for (int b = 0; b < 4; ++b)
+                            if (n0 + b < cols) p[b] = ACCUMULATE ? p[b] + d[b] : d[b];
                     }
                 }
             }
@@ -496,9 +511,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
             return LEAP_ERR_INVALID_ARG;
         if (!aligned16(hidden_bf16) || !aligned16(weight_bf16)) return LEAP_ERR_MISALIGNED;
     }
-    if ((reinterpret_cast<uintptr_t>(dhidden) & 3u) != 0 ||
-        (reinterpret_cast<uintptr_t>(dweight) & 3u) != 0)
-        return LEAP_ERR_MISALIGNED;
+    if (!aligned16(dhidden) || !aligned16(dweight)) return LEAP_ERR_MISALIGNED;
     const Layout L = layout_of(d);
     if (!workspace || ws_bytes < L.total) return LEAP_ERR_WORKSPACE;
     if (!aligned16(workspace)) return LEAP_ERR_MISALIGNED;

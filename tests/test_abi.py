@@ -236,6 +236,7 @@ def _lmhead(**kw):
     (dict(hidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(weight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
     (dict(dweight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
+    (dict(dhidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(workspace=None), L.LEAP_ERR_WORKSPACE),
     (dict(ws_bytes=1024), L.LEAP_ERR_WORKSPACE),
 ])
