@@ -256,10 +256,14 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 
 // ---------------------------------------------------------------------------
 // dZ epilogue: dz = g (onehot - 2^(z c - lse2)), zero past V, rounded to
-// bf16.  Register groups r = 4q..4q+3 of a lane are 4 consecutive rows of one
-// column: they go to the transposed copy as one 8-byte store, and after a
-// 4 x 4 transpose inside each lane quad (two DPP exchanges) each lane holds 4
-// consecutive columns of one row for the row-major copy.
+// bf16, stored twice with 16-byte stores.  Register group q (regs 4q..4q+3)
+// of a lane holds rows q*8 + h*4 + 0..3 (h = lane / 32) of its column.
+//  * Transposed copy: the two half-waves swap groups (xor 32), so a lane of
+//    h = 0 holds rows 0-7 and 16-23 of its column, h = 1 rows 8-15 and
+//    24-31: two runs of 8 bf16.
+//  * Row-major copy: a 4 x 4 transpose inside each lane quad (two DPP
+//    exchanges) gives a lane 4 columns of one row; neighbouring quads then
+//    swap groups (xor 4), so a lane holds 8 consecutive columns of one row.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -287,6 +291,10 @@ __device__ __forceinline__ void quad_transpose(float (&d)[4], int lane) {
     } else {
         d[2] = r0, d[3] = r1;
     }
+}
+
+__device__ __forceinline__ uint2 xor_lanes(uint2 v, int mask) {
+    return make_uint2(__shfl_xor(v.x, mask, kWave), __shfl_xor(v.y, mask, kWave));
 }
 
 struct DzEpi {
@@ -321,32 +329,62 @@ struct DzEpi {
             }
         }
         __syncthreads();
-        const int lane = t.lane, l32 = lane & 31, half = lane >> 5;
+        const int lane = t.lane, l32 = lane & 31, h = lane >> 5;
+        const bool qodd = ((l32 >> 2) & 1) != 0;  // odd lane quad
         const int vw = t.col0();  // chunk-local column of the wave's block
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
+            const int rb = t.wm * 128 + i * 32;  // tile row of the block
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int v = vw + j * 32 + l32;
                 const bool colok = c0 + v < V;
+                float d[4][4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int rq = t.wm * 128 + i * 32 + q * 8 + half * 4;  // tile row of e = 0
-                    float d[4];
+                for (int q = 0; q < 4; ++q)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float pz = __builtin_amdgcn_exp2f(acc[i][j][4 * q + e] * c2 - s_l[rq + e]);
-                        const float dd = s_g[rq + e] * ((v == s_y[rq + e] ? 1.0f : 0.0f) - pz);
-                        d[e] = colok ? dd : 0.0f;
+                        const int rr = rb + q * 8 + h * 4 + e;
+                        const float pz = __builtin_amdgcn_exp2f(acc[i][j][4 * q + e] * c2 - s_l[rr]);
+                        const float dd = s_g[rr] * ((v == s_y[rr] ? 1.0f : 0.0f) - pz);
+                        d[q][e] = colok ? dd : 0.0f;
                     }
-                    if (dzt) {
-                        uint2 w2 = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
-                        *reinterpret_cast<uint2*>(dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rq) = w2;
+                if (dzt) {
+                    uint2 P[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        P[q] = make_uint2(pack_bf16(d[q][0], d[q][1]), pack_bf16(d[q][2], d[q][3]));
+                    const uint2 ra = xor_lanes(h ? P[0] : P[1], 32);
+                    const uint2 rc = xor_lanes(h ? P[2] : P[3], 32);
+                    u32x4 lo, hi;
+                    if (h == 0) {  // rows 0-7 and 16-23
+                        lo = u32x4{P[0].x, P[0].y, ra.x, ra.y};
+                        hi = u32x4{P[2].x, P[2].y, rc.x, rc.y};
+                    } else {       // rows 8-15 and 24-31
+                        lo = u32x4{ra.x, ra.y, P[1].x, P[1].y};
+                        hi = u32x4{rc.x, rc.y, P[3].x, P[3].y};
                     }
-                    if (dz) {
-                        quad_transpose(d, lane);
-                        uint2 w2 = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
-                        *reinterpret_cast<uint2*>(dz + (row0 + rq + (lane & 3)) * ld_dz + (v & ~3)) = w2;
+                    uint16_t* col = dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rb + h * 8;
+                    *reinterpret_cast<u32x4*>(col) = lo;
+                    *reinterpret_cast<u32x4*>(col + 16) = hi;
+                }
+                if (dz) {
+                    uint2 Z[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        quad_transpose(d[q], lane);  // row q*8 + h*4 + lane%4, columns 4Q..4Q+3
+                        Z[q] = make_uint2(pack_bf16(d[q][0], d[q][1]), pack_bf16(d[q][2], d[q][3]));
+                    }
+                    const int vq = vw + j * 32 + (l32 & ~7);  // first column of the quad pair
+#pragma unroll
+                    for (int pr = 0; pr < 2; ++pr) {  // group pairs (0, 1) and (2, 3)
+                        const uint2 mine_even = Z[2 * pr], mine_odd = Z[2 * pr + 1];
+                        const uint2 r = xor_lanes(qodd ? mine_even : mine_odd, 4);
+                        // even quad: row of group 2pr, columns vq..vq+7; odd quad: group 2pr+1
+                        const u32x4 out = qodd ? u32x4{r.x, r.y, mine_odd.x, mine_odd.y}
+                                               : u32x4{mine_even.x, mine_even.y, r.x, r.y};
+                        const int rr = rb + (2 * pr + (qodd ? 1 : 0)) * 8 + h * 4 + (lane & 3);
+                        *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + vq) = out;
                     }
                 }
             }
