@@ -27,7 +27,8 @@ namespace leap {
 namespace {
 
 using gemm::acc_row;
-using gemm::f32x16;
+using gemm::acc_col;
+using gemm::f32x4;
 using gemm::Tile;
 using obj::Params;
 using obj::RowOut;
@@ -93,14 +94,15 @@ __global__ __launch_bounds__(256) void fill_zero_f32_kernel(float* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Stats epilogue.  Accumulator register r of lane l in 32 x 32 block (i, j)
-// of a wave holds row i*32 + acc_row(r, l), column j*32 + l%32, so the 32
-// lanes of each half-wave share 16 rows per block i.  Each lane first folds
-// its 4 columns, then the half-wave does a reduce-scatter: at every step a
-// lane keeps half of its (max, sum) pairs, sends the other half to its
-// partner and merges what it receives, so after xor 16, 8, 4, 2 and a final
-// xor 1 exchange every lane pair holds one row's pair over 128 columns.
-// The two waves covering the same rows merge through LDS.
+// Stats epilogue.  Accumulator register r of lane l in 16 x 16 block (i, j)
+// of a wave holds row 16 i + 4 (l / 16) + r, column 16 j + l % 16, so the 16
+// lanes with the same l / 16 share those rows.  Per group of four row blocks
+// each lane first folds its 8 columns of each of its 16 rows, then the 16
+// lanes do a reduce-scatter: at every step a lane keeps half of its (max,
+// sum) pairs, sends the other half to its partner and merges what it
+// receives, so after xor 8, 4, 2, 1 lane l holds the pair of one row over the
+// wave's 128 columns (the row of pair index l % 16).  The two waves covering
+// the same rows merge through LDS.
 // ---------------------------------------------------------------------------
 template <int HALF>
 __device__ __forceinline__ void scatter_step(float (&m)[16], float (&s)[16], int lane, int b) {
@@ -127,7 +129,7 @@ struct StatsEpi {
     int V, tiles_v;
     float c2;  // log2(e) / T
 
-    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t* smem) const {
+    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
         int* s_y = reinterpret_cast<int*>(smem);
         float2* s_ms = reinterpret_cast<float2*>(smem + kTile * sizeof(int));
         const int tid = threadIdx.x;
@@ -138,60 +140,60 @@ struct StatsEpi {
             s_y[tid] = (y >= 0 && y < V) ? y : -1;
         }
         __syncthreads();
-        const int lane = t.lane, l32 = lane & 31;
+        const int lane = t.lane, c = lane & 15, h = lane >> 4;
         const int col0 = t.col0();
-        bool colok[4];
+        bool colok[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) colok[j] = col0 + j * 32 + l32 < V;
+        for (int j = 0; j < 8; ++j) colok[j] = col0 + j * 16 + c < V;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int G = 0; G < 2; ++G) {  // row blocks 4G .. 4G+3; pair k = 4 (i - 4G) + r
             float m[16], s[16];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float z[4];
-                float mx = -INFINITY;
+            for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    z[j] = colok[j] ? acc[i][j][r] * c2 : -INFINITY;
-                    mx = fmaxf(mx, z[j]);
-                }
-                float sum = 0.0f;
-                if (mx != -INFINITY) {
+                for (int r = 0; r < 4; ++r) {
+                    const int i = 4 * G + ii;
+                    float z[8];
+                    float mx = -INFINITY;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) sum += __builtin_amdgcn_exp2f(z[j] - mx);
+                    for (int j = 0; j < 8; ++j) {
+                        z[j] = colok[j] ? acc[i][j][r] * c2 : -INFINITY;
+                        mx = fmaxf(mx, z[j]);
+                    }
+                    float sum = 0.0f;
+                    if (mx != -INFINITY) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) sum += __builtin_amdgcn_exp2f(z[j] - mx);
+                    }
+                    m[4 * ii + r] = mx;
+                    s[4 * ii + r] = sum;
                 }
-                m[r] = mx;
-                s[r] = sum;
-            }
             // The token's logit: exactly one lane of the grid holds each row's.
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int rw = t.wm * 128 + i * 32 + acc_row(r, lane);
-                const int y = s_y[rw];
-                const int rel = y - col0;
-                if (y >= 0 && rel >= 0 && rel < 128 && (rel & 31) == l32) {
-                    const int jj = rel >> 5;
-                    float v = acc[i][0][r];
-                    v = jj == 1 ? acc[i][1][r] : v;
-                    v = jj == 2 ? acc[i][2][r] : v;
-                    v = jj == 3 ? acc[i][3][r] : v;
-                    zy[row0 + rw] = v;
+            for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = 4 * G + ii;
+                    const int rw = t.wm * 128 + i * 16 + acc_row(r, lane);
+                    const int y = s_y[rw];
+                    const int rel = y - col0;
+                    if (y >= 0 && rel >= 0 && rel < 128 && (rel & 15) == c) {
+                        const int jj = rel >> 4;
+                        float v = acc[i][0][r];
+#pragma unroll
+                        for (int q = 1; q < 8; ++q) v = jj == q ? acc[i][q][r] : v;
+                        zy[row0 + rw] = v;
+                    }
                 }
-            }
-            scatter_step<8>(m, s, lane, 16);
-            scatter_step<4>(m, s, lane, 8);
-            scatter_step<2>(m, s, lane, 4);
-            scatter_step<1>(m, s, lane, 2);
+            scatter_step<8>(m, s, lane, 8);
+            scatter_step<4>(m, s, lane, 4);
+            scatter_step<2>(m, s, lane, 2);
+            scatter_step<1>(m, s, lane, 1);
             {
-                const float rm = __shfl_xor(m[0], 1, kWave);
-                const float rs = __shfl_xor(s[0], 1, kWave);
-                ms_merge(m[0], s[0], rm, rs);
-            }
-            if ((lane & 1) == 0) {
-                const int rw = t.wm * 128 + i * 32 + acc_row((l32 >> 1) & 15, lane);
+                const int rw = t.wm * 128 + (4 * G + (c >> 2)) * 16 + acc_row(c & 3, lane);
                 s_ms[t.wn * kTile + rw] = make_float2(m[0], s[0]);
             }
-            // keep the next block's accumulators in AGPRs until they are used
+            // keep the next group's accumulators in AGPRs until they are used
             __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();
@@ -256,14 +258,16 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 
 // ---------------------------------------------------------------------------
 // dZ epilogue: dz = g (onehot - 2^(z c - lse2)), zero past V, rounded to
-// bf16, stored twice with 16-byte stores.  Register group q (regs 4q..4q+3)
-// of a lane holds rows q*8 + h*4 + 0..3 (h = lane / 32) of its column.
-//  * Transposed copy: the two half-waves swap groups (xor 32), so a lane of
-//    h = 0 holds rows 0-7 and 16-23 of its column, h = 1 rows 8-15 and
-//    24-31: two runs of 8 bf16.
+// bf16, stored twice with 16-byte stores.  A lane holds rows 4h .. 4h+3
+// (h = lane / 16) of column l % 16 of each 16 x 16 block; blocks are taken
+// in column pairs (j, j+1).
+//  * Transposed copy: lanes l and l ^ 16 (h even / odd) swap one block each,
+//    so the even lane holds rows 4h .. 4h+7 of its column in block j and the
+//    odd lane rows 4h-4 .. 4h+3 in block j+1: one run of 8 bf16 each.
 //  * Row-major copy: a 4 x 4 transpose inside each lane quad (two DPP
-//    exchanges) gives a lane 4 columns of one row; neighbouring quads then
-//    swap groups (xor 4), so a lane holds 8 consecutive columns of one row.
+//    exchanges) gives a lane 4 columns of one row; lanes l and l ^ 4
+//    (neighbouring quads) then swap one block each, so a lane holds 8
+//    consecutive columns of one row.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -309,7 +313,7 @@ struct DzEpi {
     int V, c0;  // vocabulary size, first column of the chunk
     float c2;
 
-    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t* smem) const {
+    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
         float* s_l = reinterpret_cast<float*>(smem);
         float* s_g = s_l + kTile;
         int* s_y = reinterpret_cast<int*>(s_g + kTile);
@@ -329,63 +333,54 @@ struct DzEpi {
             }
         }
         __syncthreads();
-        const int lane = t.lane, l32 = lane & 31, h = lane >> 5;
-        const bool qodd = ((l32 >> 2) & 1) != 0;  // odd lane quad
+        const int lane = t.lane, c = lane & 15, h = lane >> 4;
+        const bool hodd = (h & 1) != 0;
+        const int k = c >> 2;              // lane quad within the 16 columns
+        const bool qodd = (k & 1) != 0;
         const int vw = t.col0();  // chunk-local column of the wave's block
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int rb = t.wm * 128 + i * 32;  // tile row of the block
+        for (int i = 0; i < 8; ++i) {
+            const int rb = t.wm * 128 + i * 16;  // tile row of the block
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int v = vw + j * 32 + l32;
-                const bool colok = c0 + v < V;
-                float d[4][4];
+            for (int jp = 0; jp < 4; ++jp) {
+                float d[2][4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
+                for (int e = 0; e < 2; ++e) {
+                    const int v = vw + (2 * jp + e) * 16 + c;
+                    const bool colok = c0 + v < V;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int rr = rb + q * 8 + h * 4 + e;
-                        const float pz = __builtin_amdgcn_exp2f(acc[i][j][4 * q + e] * c2 - s_l[rr]);
+                    for (int r = 0; r < 4; ++r) {
+                        const int rr = rb + acc_row(r, lane);
+                        const float pz = __builtin_amdgcn_exp2f(acc[i][2 * jp + e][r] * c2 - s_l[rr]);
                         const float dd = s_g[rr] * ((v == s_y[rr] ? 1.0f : 0.0f) - pz);
-                        d[q][e] = colok ? dd : 0.0f;
+                        d[e][r] = colok ? dd : 0.0f;
                     }
+                }
                 if (dzt) {
-                    uint2 P[4];
+                    uint2 P[2];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        P[q] = make_uint2(pack_bf16(d[q][0], d[q][1]), pack_bf16(d[q][2], d[q][3]));
-                    const uint2 ra = xor_lanes(h ? P[0] : P[1], 32);
-                    const uint2 rc = xor_lanes(h ? P[2] : P[3], 32);
-                    u32x4 lo, hi;
-                    if (h == 0) {  // rows 0-7 and 16-23
-                        lo = u32x4{P[0].x, P[0].y, ra.x, ra.y};
-                        hi = u32x4{P[2].x, P[2].y, rc.x, rc.y};
-                    } else {       // rows 8-15 and 24-31
-                        lo = u32x4{ra.x, ra.y, P[1].x, P[1].y};
-                        hi = u32x4{rc.x, rc.y, P[3].x, P[3].y};
-                    }
-                    uint16_t* col = dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rb + h * 8;
-                    *reinterpret_cast<u32x4*>(col) = lo;
-                    *reinterpret_cast<u32x4*>(col + 16) = hi;
+                    for (int e = 0; e < 2; ++e)
+                        P[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
+                    const uint2 rv = xor_lanes(hodd ? P[0] : P[1], 16);
+                    const u32x4 out = hodd ? u32x4{rv.x, rv.y, P[1].x, P[1].y}
+                                           : u32x4{P[0].x, P[0].y, rv.x, rv.y};
+                    const int v = vw + (2 * jp + (hodd ? 1 : 0)) * 16 + c;
+                    const int rs = rb + 4 * (h & ~1);  // first of the 8 rows
+                    *reinterpret_cast<u32x4*>(dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rs) = out;
                 }
                 if (dz) {
-                    uint2 Z[4];
+                    uint2 Z[2];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        quad_transpose(d[q], lane);  // row q*8 + h*4 + lane%4, columns 4Q..4Q+3
-                        Z[q] = make_uint2(pack_bf16(d[q][0], d[q][1]), pack_bf16(d[q][2], d[q][3]));
+                    for (int e = 0; e < 2; ++e) {
+                        quad_transpose(d[e], lane);  // row 4h + lane%4, columns 4k .. 4k+3
+                        Z[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
                     }
-                    const int vq = vw + j * 32 + (l32 & ~7);  // first column of the quad pair
-#pragma unroll
-                    for (int pr = 0; pr < 2; ++pr) {  // group pairs (0, 1) and (2, 3)
-                        const uint2 mine_even = Z[2 * pr], mine_odd = Z[2 * pr + 1];
-                        const uint2 r = xor_lanes(qodd ? mine_even : mine_odd, 4);
-                        // even quad: row of group 2pr, columns vq..vq+7; odd quad: group 2pr+1
-                        const u32x4 out = qodd ? u32x4{r.x, r.y, mine_odd.x, mine_odd.y}
-                                               : u32x4{mine_even.x, mine_even.y, r.x, r.y};
-                        const int rr = rb + (2 * pr + (qodd ? 1 : 0)) * 8 + h * 4 + (lane & 3);
-                        *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + vq) = out;
-                    }
+                    const uint2 rv = xor_lanes(qodd ? Z[0] : Z[1], 4);
+                    const u32x4 out = qodd ? u32x4{rv.x, rv.y, Z[1].x, Z[1].y}
+                                           : u32x4{Z[0].x, Z[0].y, rv.x, rv.y};
+                    const int v = vw + (2 * jp + (qodd ? 1 : 0)) * 16 + 4 * (k & ~1);
+                    const int rr = rb + 4 * h + (lane & 3);
+                    *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v) = out;
                 }
             }
         }
@@ -403,35 +398,32 @@ struct StoreF32Epi {
     int64_t rows;
     int cols;
 
-    __device__ void operator()(f32x16 (&acc)[4][4], const Tile& t, uint8_t*) const {
-        const int lane = t.lane, half = (lane >> 5) & 1;
+    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t*) const {
+        const int lane = t.lane;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 8; ++i) {
+            const int64_t m = t.row0() + i * 16 + acc_row(lane & 3, lane);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int n0 = t.col0() + j * 32 + ((lane & 31) & ~3);  // the quad's first column
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float d[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                  acc[i][j][4 * q + 3]};
-                    quad_transpose(d, lane);
-                    const int64_t m = t.row0() + i * 32 + q * 8 + half * 4 + (lane & 3);
-                    if (m >= rows) continue;
-                    float* p = C + m * ldc + n0;
-                    if (n0 + 3 < cols) {
-                        float4 v = make_float4(d[0], d[1], d[2], d[3]);
-                        if (ACCUMULATE) {
-                            const float4 o = *reinterpret_cast<const float4*>(p);
-                            v.x += o.x, v.y += o.y, v.z += o.z, v.w += o.w;
-                        }
-                        *reinterpret_cast<float4*>(p) = v;
-                    } else {
-#pragma unroll
-                        for (int b = 0; b < 4; ++b)
-                            if (n0 + b < cols) p[b] = ACCUMULATE ? p[b] + d[b] : d[b];
+            for (int j = 0; j < 8; ++j) {
+                float d[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+                quad_transpose(d, lane);  // row 4h + lane%4, columns of the lane quad
+                const int n0 = t.col0() + j * 16 + (acc_col(lane) & ~3);
+                if (m >= rows) continue;
+                float* p = C + m * ldc + n0;
+                if (n0 + 3 < cols) {
+                    float4 v = make_float4(d[0], d[1], d[2], d[3]);
+                    if (ACCUMULATE) {
+                        const float4 o = *reinterpret_cast<const float4*>(p);
+                        v.x += o.x, v.y += o.y, v.z += o.z, v.w += o.w;
                     }
+                    *reinterpret_cast<float4*>(p) = v;
+                } else {
+#pragma unroll
+                    for (int b = 0; b < 4; ++b)
+                        if (n0 + b < cols) p[b] = ACCUMULATE ? p[b] + d[b] : d[b];
                 }
             }
+        }
     }
 };
 

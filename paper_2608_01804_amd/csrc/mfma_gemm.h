@@ -3,34 +3,39 @@
 // the result handed to an epilogue functor instead of being stored.
 //
 //  * Workgroup tile 256 x 256, k-tiles of 64, 256 lanes = 4 waves in a 2 x 2
-//    grid, each wave a 128 x 128 block of 4 x 4 v_mfma_f32_32x32x16_bf16
-//    tiles (256 fp32 accumulators per lane, one wave per SIMD).
+//    grid, each wave a 128 x 128 block of 8 x 8 v_mfma_f32_16x16x32_bf16
+//    tiles (256 fp32 accumulators per lane, one wave per SIMD).  Under the
+//    chip's power limit this shape runs at a higher clock than 32x32x16 for
+//    the same work (half the accumulator traffic per flop).
 //  * Operand k-tiles go straight from HBM to LDS (buffer_load_dwordx4 ... lds,
 //    no VGPR staging); each row's 128-byte k-segment is one cache line
 //    fetched by one instruction.  LDS holds two A slots and three B slots of
 //    32 KiB (160 KiB): A k-tiles are loaded one k-tile ahead, B k-tiles two.
 //    The compiler does not track these LDS writes, so each wave waits on its
 //    own vmcnt before the stage barrier.
-//  * The per-CU vector memory path moves about 32 bytes per clock, which is
-//    what a 256 x 256 bf16 tile consumes at the full MFMA rate, and a wave
-//    whose load cannot be accepted stalls its MFMA stream too.  So the 16
-//    loads of a k-tile are spread one per four MFMAs over the whole k-tile
-//    (second half of A(kt+1), then B(kt+2), then after the barrier the first
-//    half of A(kt+2)), and the fragments of the next k = 16 sub-step are read
-//    from LDS two per four MFMAs, in fenced groups of
-//    [2 MFMA | load | 2 LDS reads + 2 MFMA].
+//  * A k-tile is two k = 32 steps of 64 MFMAs.  The stage barrier sits
+//    between them: step 0 streams in B(kt+2) and reads the step-1 fragments
+//    of the same slots; after the barrier, step 1 streams A(kt+2) into the
+//    A slot just freed and reads the step-0 fragments of k-tile kt+1.  Within
+//    a step the 8 x 8 blocks run row by row: one load per row, the next
+//    step's B fragments in rows 0-3 (into the second B register set), and the
+//    next A fragment of row i right after row i, into the registers row i
+//    has just finished with.
 //  * LDS rows are 128 bytes (64 bf16); the 16-byte chunk c of row r sits at
-//    position c ^ ((r >> 1) & 7), so the 16-row MFMA fragment reads hit
-//    distinct banks, and every load instruction fills 1 KiB contiguously.
-//  * The wave index is made wave-uniform (readfirstlane) so every LDS
-//    destination of the loads is computed in scalar registers and written to
-//    M0 directly; a per-load v_readfirstlane into M0 stalls the MFMA stream.
+//    position c ^ ((r >> 1) & 7), so the 16-row fragment reads hit distinct
+//    banks and every load instruction fills 1 KiB contiguously.  The swizzle
+//    term does not depend on the 16-row block, so the 8 fragment reads of a
+//    step use one base register and immediate offsets.
+//  * The wave index and the LDS slot bases are wave-uniform scalars
+//    (readfirstlane): the loads' LDS destinations go to M0 from scalar
+//    registers, and no vector address arithmetic sits between the MFMAs.
 //  * Tiles are numbered so the workgroups one XCD runs at once form a compact
 //    GROUP x (32 / GROUP) patch (see tile_of_block).
 //
-// Operand fragments of v_mfma_f32_32x32x16_bf16 (lane l of 64): A row l%32
-// with k = 8*(l/32) .. +7; B column l%32 with the same k; accumulator
-// register r holds C[row (r/4)*8 + (l/32)*4 + r%4][column l%32].
+// v_mfma_f32_16x16x32_bf16 (lane l of 64): A row l%16 with k = 8*(l/16) .. +7;
+// B column l%16 with the same k; accumulator register r holds
+// C[row 4*(l/16) + r][column l%16].  So acc[i][j][r] of lane l is
+// C[row0 + 16 i + 4 (l / 16) + r][col0 + 16 j + l % 16] of the wave's block.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -40,8 +45,7 @@ namespace leap {
 namespace gemm {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4g __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256;
 constexpr int kBN = 256;
@@ -58,9 +62,6 @@ constexpr int kXcds = 8;
 #define LEAP_GEMM_GROUP_M 4
 #endif
 constexpr int kGroupM = LEAP_GEMM_GROUP_M;
-
-// Byte offset of chunk c (16 bytes) of row r inside an LDS operand tile.
-__device__ __forceinline__ int lds_off(int r, int c) { return (r << 7) + ((c ^ ((r >> 1) & 7)) << 4); }
 
 // s_waitcnt on vmcnt <= n only (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
 // expcnt and lgkmcnt left at their "no wait" maxima).
@@ -80,9 +81,9 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("s_barrier" ::: "memory");
 }
 
-// Row and column of accumulator register r of lane l inside a 32 x 32 tile.
-__device__ __forceinline__ int acc_row(int r, int lane) { return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3); }
-__device__ __forceinline__ int acc_col(int lane) { return lane & 31; }
+// Row and column of accumulator register r of lane l inside a 16 x 16 block.
+__device__ __forceinline__ int acc_row(int r, int lane) { return ((lane >> 4) << 2) + r; }
+__device__ __forceinline__ int acc_col(int lane) { return lane & 15; }
 
 struct Tile {
     int tm, tn;  // tile coordinates
@@ -122,7 +123,7 @@ inline int gemm_grid(int tiles_m, int tiles_n) {
     return per * kXcds;
 }
 
-// The k-loop; leaves the wave's 4 x 4 accumulator tiles in acc.  Requires
+// The k-loop; leaves the wave's 8 x 8 accumulator blocks in acc.  Requires
 // K % 64 == 0, lda and ldb multiples of 8, and every row offset the tiles
 // reach ((tiles * 256) * ld * 2 bytes) below 4 GiB; a_bytes / b_bytes are the
 // readable extents (rows past them read as 0).  On return every load has
@@ -131,19 +132,16 @@ inline int gemm_grid(int tiles_m, int tiles_n) {
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t lda,
                                          uint32_t a_bytes, const uint16_t* __restrict__ B,
                                          int64_t ldb, uint32_t b_bytes, int K, int tm, int tn,
-                                         uint8_t* smem, f32x16 (&acc)[4][4]) {
+                                         uint8_t* smem, f32x4 (&acc)[8][8]) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    // wave-uniform by construction; readfirstlane lets the compiler keep
-    // the LDS destinations of the loads (M0) in scalar registers instead of
-    // a v_readfirstlane per load, which costs ~12% of the MFMA issue rate
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{};
 
     const __amdgpu_buffer_rsrc_t ra =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(A), 0, a_bytes, kGemmBufferFlags);
@@ -181,46 +179,51 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
             live ? rb : rz, (__attribute__((address_space(3))) void*)(st + (wave * 8 + q) * 1024), 16,
             voff_b[q], (live ? kt : 0) * kBK * 2, 0, 0);
     };
-    // fragment f of sub-step s (f < 4: A rows block f; else B columns block f - 4)
-    auto read1 = [&](int as, int bsl, int s, int f, bf16x8(&af)[4], bf16x8(&bf)[4]) {
-        const int c = 2 * s + (lane >> 5);
-        if (f < 4) {
-            const uint8_t* sa = smem + as * kTileBytes;
-            af[f] = *reinterpret_cast<const bf16x8*>(sa + lds_off(wm * 128 + f * 32 + (lane & 31), c));
-        } else {
-            const uint8_t* sb = smem + (kASlots + bsl) * kTileBytes;
-            bf[f - 4] = *reinterpret_cast<const bf16x8*>(sb + lds_off(wn * 128 + (f - 4) * 32 + (lane & 31), c));
-        }
-    };
-    // The 16 MFMAs of one sub-step on (xa, xb); meanwhile the fragments of
-    // the next sub-step s into (ya, yb) (s < 0: none) and the four loads
-    // dma(0..3), in four fenced groups [2 MFMA | load | 2 reads + 2 MFMA].
-    // The wait first: the fragments in use were read a sub-step ago.
-    auto batch = [&](const bf16x8(&xa)[4], const bf16x8(&xb)[4], int as, int bsl, int s,
-                     bf16x8(&ya)[4], bf16x8(&yb)[4], auto&& dma) {
-        wait_lgkmcnt0();
+    // Fragment f of step s: row wm*128 + 16f + l%16 (A) or wn*128 + 16f + l%16
+    // (B), chunk 4s + l/16.  The swizzle term ((row >> 1) & 7) is the same for
+    // every f, so fragment f sits f * 2048 bytes past fragment 0.
+    const int lr = lane & 15, lc = lane >> 4;
+    uint32_t lane_a[2], lane_b[2];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+    for (int s = 0; s < 2; ++s) {
+        const int pos = ((4 * s + lc) ^ ((lr >> 1) & 7)) << 4;
+        lane_a[s] = static_cast<uint32_t>((wm * 128 + lr) * 128 + pos);
+        lane_b[s] = static_cast<uint32_t>((wn * 128 + lr) * 128 + pos);
+    }
+    bf16x8 fa[8], fb0[8], fb1[8];
+    // One k = 32 step: 64 MFMAs on (fa, xb), row by row over the 8 x 8
+    // blocks.  Meanwhile the fragments of step s of the slots (as, bsl) (s < 0:
+    // none): B into yb during rows 0-3, A block i into fa right after row i;
+    // and the loads dma(i), one per row, after the row's second MFMA.
+    auto step = [&](const bf16x8(&xb)[8], bf16x8(&yb)[8], int as, int bsl, int s, auto&& dma) {
+        // slot bases as opaque scalars: one vector add per step, and the 8
+        // reads per operand then use immediate offsets
+        const uint32_t a_base = __builtin_amdgcn_readfirstlane(as * kTileBytes);
+        const uint32_t b_base = __builtin_amdgcn_readfirstlane((kASlots + bsl) * kTileBytes);
+        const uint8_t* pa = smem + (a_base + lane_a[s < 0 ? 0 : s]);
+        const uint8_t* pb = smem + (b_base + lane_b[s < 0 ? 0 : s]);
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
-                acc[g][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[g], xb[u], acc[g][u], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            dma(g);
-            __builtin_amdgcn_sched_barrier(0);
-            if (s >= 0) {
-                read1(as, bsl, s, 2 * g, ya, yb);
-                read1(as, bsl, s, 2 * g + 1, ya, yb);
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], xb[j], acc[i][j], 0, 0, 0);
+                if (j == 1) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    dma(i);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (s >= 0 && i < 4) {
+                        yb[2 * i] = *reinterpret_cast<const bf16x8*>(pb + (2 * i) * 2048);
+                        yb[2 * i + 1] = *reinterpret_cast<const bf16x8*>(pb + (2 * i + 1) * 2048);
+                    }
+                }
             }
-#pragma unroll
-            for (int u = 2; u < 4; ++u)
-                acc[g][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[g], xb[u], acc[g][u], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (s >= 0) fa[i] = *reinterpret_cast<const bf16x8*>(pa + i * 2048);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
 
-    // A k-tile t in A slot t % 2, B k-tile t in B slot t % 3.  Per k-tile kt:
-    // batch 1 loads the second half of A(kt+1), batches 2-3 load B(kt+2),
-    // batch 4 (after the barrier) loads the first half of A(kt+2).
+    // A k-tile t in A slot t % 2, B k-tile t in B slot t % 3.
 #pragma unroll
     for (int q = 0; q < 8; ++q) dma_a(0, q);
 #pragma unroll
@@ -228,35 +231,38 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
 #pragma unroll
     for (int q = 0; q < 8; ++q) dma_b(1, 1, q);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) dma_a(1, q);
-    wait_vmcnt<12>();  // A(0), B(0) landed; B(1) and half of A(1) may fly
+    for (int q = 0; q < 8; ++q) dma_a(1, q);
+    wait_vmcnt<16>();  // A(0), B(0) landed; B(1) and A(1) may fly
     stage_barrier();
-    bf16x8 a0[4], b0[4], a1[4], b1[4];
-    wait_lgkmcnt0();
+    {
+        const uint8_t* pa = smem + lane_a[0];
+        const uint8_t* pb = smem + kASlots * kTileBytes + lane_b[0];
 #pragma unroll
-    for (int f = 0; f < 8; ++f) read1(0, 0, 0, f, a0, b0);
+        for (int f = 0; f < 8; ++f) {
+            fa[f] = *reinterpret_cast<const bf16x8*>(pa + f * 2048);
+            fb0[f] = *reinterpret_cast<const bf16x8*>(pb + f * 2048);
+        }
+    }
     int bs = 0;  // B slot of k-tile kt
     for (int kt = 0; kt + 1 < KT; ++kt) {
         const int as = kt & 1;
         const int b2 = bs == 0 ? 2 : bs - 1;  // slot of B(kt+2) == slot of B(kt-1)
         const int bn = bs == 2 ? 0 : bs + 1;
-        batch(a0, b0, as, bs, 1, a1, b1, [&](int g) { dma_a(kt + 1, 4 + g); });
-        batch(a1, b1, as, bs, 2, a0, b0, [&](int g) { dma_b(kt + 2, b2, g); });
-        batch(a0, b0, as, bs, 3, a1, b1, [&](int g) { dma_b(kt + 2, b2, 4 + g); });
-        // A(kt+1) and B(kt+1) have landed (only B(kt+2) may still fly); after
-        // the barrier A slot kt % 2 and B slot kt % 3 are free
+        // step 0: step-1 fragments of the same slots; B(kt+2) streams in
+        step(fb0, fb1, as, bs, 1, [&](int i) { dma_b(kt + 2, b2, i); });
+        // k-tile kt+1 has landed (only B(kt+2) may still fly); after the
+        // barrier A slot kt % 2 and B slot kt % 3 are free
         wait_vmcnt<8>();
         stage_barrier();
-        batch(a1, b1, as ^ 1, bn, 0, a0, b0, [&](int g) { dma_a(kt + 2, g); });
+        // step 1: step-0 fragments of k-tile kt+1; A(kt+2) into A slot kt % 2
+        step(fb1, fb0, as ^ 1, bn, 0, [&](int i) { dma_a(kt + 2, i); });
         bs = bn;
     }
     {
         const int as = (KT - 1) & 1;
         auto none = [&](int) {};
-        batch(a0, b0, as, bs, 1, a1, b1, none);
-        batch(a1, b1, as, bs, 2, a0, b0, none);
-        batch(a0, b0, as, bs, 3, a1, b1, none);
-        batch(a1, b1, as, bs, -1, a0, b0, none);
+        step(fb0, fb1, as, bs, 1, none);
+        step(fb1, fb0, as, bs, -1, none);
     }
     // the zero-filling loads of the slots past the end have landed and every
     // wave is past its LDS reads: the epilogue may reuse the LDS
@@ -274,7 +280,7 @@ gemm_nt_kernel(const uint16_t* __restrict__ A, int64_t lda, uint32_t a_bytes,
     __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
     int tm, tn;
     if (!tile_of_block<kGroupM>(tiles_m, tiles_n, tm, tn)) return;
-    f32x16 acc[4][4];
+    f32x4 acc[8][8];
     mainloop(A, lda, a_bytes, B, ldb, b_bytes, K, tm, tn, smem, acc);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     Tile t{tm, tn, wave >> 1, wave & 1, static_cast<int>(threadIdx.x & 63)};
