@@ -46,6 +46,11 @@ constexpr int kTile = gemm::kBM;  // 256: rows and columns of a GEMM tile
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
+
 // ---------------------------------------------------------------------------
 // Transpose with zero padding: dst[c][r] = src[r][c] for r < R, and 0 for
 // R <= r < ld_dst, for every c < C.  64 x 64 tiles through LDS; C % 8 == 0.
@@ -297,9 +302,19 @@ __device__ __forceinline__ void quad_transpose(float (&d)[4], int lane) {
     }
 }
 
-__device__ __forceinline__ uint2 xor_lanes(uint2 v, int mask) {
-    return make_uint2(__shfl_xor(v.x, mask, kWave), __shfl_xor(v.y, mask, kWave));
+// DPP row rotates inside each 16-lane row: lane i gets lane (i - 4) mod 16
+// (ror 4) or lane (i + 4) mod 16 (ror 12).
+__device__ __forceinline__ uint32_t dpp_row_ror4(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x124, 0xF, 0xF, false));
 }
+__device__ __forceinline__ uint32_t dpp_row_ror12(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x12C, 0xF, 0xF, false));
+}
+
+constexpr int kStageRow = 128 * 2 + 16;            // bytes per staged column (128 rows + pad)
+constexpr int kStageWave = 128 * kStageRow;          // 34816 bytes per wave
+constexpr int kStageBase = 4096;                     // after the per-row arrays (3 KiB)
+static_assert(kStageBase + 4 * kStageWave <= gemm::kLdsBytes, "dZ staging exceeds the GEMM's LDS");
 
 struct DzEpi {
     const int32_t* token_ids;
@@ -317,6 +332,10 @@ struct DzEpi {
         float* s_l = reinterpret_cast<float*>(smem);
         float* s_g = s_l + kTile;
         int* s_y = reinterpret_cast<int*>(s_g + kTile);
+        // per-wave staging area for the transposed copy: 128 columns x 128
+        // rows of bf16, rows padded to 272 bytes so that 16 lanes writing 16
+        // bytes each to 16 consecutive columns hit distinct banks
+        uint8_t* stage = smem + kStageBase + (t.wm * 2 + t.wn) * kStageWave;
         const int tid = threadIdx.x;
         const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
         {
@@ -338,50 +357,80 @@ struct DzEpi {
         const int k = c >> 2;              // lane quad within the 16 columns
         const bool qodd = (k & 1) != 0;
         const int vw = t.col0();  // chunk-local column of the wave's block
+        // Every column of the wave's block inside the vocabulary (all but the
+        // last tile of the vocabulary): no per-element range select.
+        auto tile_body = [&](auto full) {
+            constexpr bool kFull = decltype(full)::value;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int rb = t.wm * 128 + i * 16;  // tile row of the block
+            for (int i = 0; i < 8; ++i) {
+                const int rb = t.wm * 128 + i * 16;  // tile row of the block
 #pragma unroll
-            for (int jp = 0; jp < 4; ++jp) {
-                float d[2][4];
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const int v = vw + (2 * jp + e) * 16 + c;
-                    const bool colok = c0 + v < V;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int rr = rb + acc_row(r, lane);
-                        const float pz = __builtin_amdgcn_exp2f(acc[i][2 * jp + e][r] * c2 - s_l[rr]);
-                        const float dd = s_g[rr] * ((v == s_y[rr] ? 1.0f : 0.0f) - pz);
-                        d[e][r] = colok ? dd : 0.0f;
-                    }
-                }
-                if (dzt) {
-                    uint2 P[2];
-#pragma unroll
-                    for (int e = 0; e < 2; ++e)
-                        P[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
-                    const uint2 rv = xor_lanes(hodd ? P[0] : P[1], 16);
-                    const u32x4 out = hodd ? u32x4{rv.x, rv.y, P[1].x, P[1].y}
-                                           : u32x4{P[0].x, P[0].y, rv.x, rv.y};
-                    const int v = vw + (2 * jp + (hodd ? 1 : 0)) * 16 + c;
-                    const int rs = rb + 4 * (h & ~1);  // first of the 8 rows
-                    *reinterpret_cast<u32x4*>(dzt + static_cast<int64_t>(v) * ld_dzt + row0 + rs) = out;
-                }
-                if (dz) {
-                    uint2 Z[2];
+                for (int jp = 0; jp < 4; ++jp) {
+                    float d[2][4];
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
-                        quad_transpose(d[e], lane);  // row 4h + lane%4, columns 4k .. 4k+3
-                        Z[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
+                        const int v = vw + (2 * jp + e) * 16 + c;
+                        const bool colok = kFull || c0 + v < V;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int rr = rb + acc_row(r, lane);
+                            const float gr = s_g[rr];
+                            const float pz = __builtin_amdgcn_exp2f(acc[i][2 * jp + e][r] * c2 - s_l[rr]);
+                            const float dd = fmaf(-gr, pz, v == s_y[rr] ? gr : 0.0f);  // g (onehot - p)
+                            d[e][r] = colok ? dd : 0.0f;
+                        }
                     }
-                    const uint2 rv = xor_lanes(qodd ? Z[0] : Z[1], 4);
-                    const u32x4 out = qodd ? u32x4{rv.x, rv.y, Z[1].x, Z[1].y}
-                                           : u32x4{Z[0].x, Z[0].y, rv.x, rv.y};
-                    const int v = vw + (2 * jp + (qodd ? 1 : 0)) * 16 + 4 * (k & ~1);
-                    const int rr = rb + 4 * h + (lane & 3);
-                    *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v) = out;
+                    if (dzt) {
+                        // v_permlane16_swap trades the odd 16-lane rows of its
+                        // first operand for the even rows of its second: an even-h
+                        // lane gets its partner's block-j0 rows, an odd-h lane its
+                        // partner's block-j1 rows, with no selects.  The 8 rows
+                        // go to the wave's column-major staging area.
+                        const uint32_t p0x = pack_bf16(d[0][0], d[0][1]), p0y = pack_bf16(d[0][2], d[0][3]);
+                        const uint32_t p1x = pack_bf16(d[1][0], d[1][1]), p1y = pack_bf16(d[1][2], d[1][3]);
+                        const auto sx = __builtin_amdgcn_permlane16_swap(p0x, p1x, false, false);
+                        const auto sy = __builtin_amdgcn_permlane16_swap(p0y, p1y, false, false);
+                        const int vl = (2 * jp + (hodd ? 1 : 0)) * 16 + c;  // column in the wave block
+                        const int nl = i * 16 + 4 * (h & ~1);               // first of the 8 rows
+                        *reinterpret_cast<u32x4*>(stage + vl * kStageRow + nl * 2) = u32x4{sx[0], sy[0], sx[1], sy[1]};
+                    }
+                    if (dz) {
+                        uint2 Z[2];
+#pragma unroll
+                        for (int e = 0; e < 2; ++e) {
+                            quad_transpose(d[e], lane);  // row 4h + lane%4, columns 4k .. 4k+3
+                            Z[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
+                        }
+                        // lane quads k and k^1 swap one block: DPP row rotates by
+                        // 12 (from lane + 4) and 4 (from lane - 4) within the row
+                        const uint2 snd = qodd ? Z[0] : Z[1];
+                        const uint2 from_hi = make_uint2(dpp_row_ror12(snd.x), dpp_row_ror12(snd.y));
+                        const uint2 from_lo = make_uint2(dpp_row_ror4(snd.x), dpp_row_ror4(snd.y));
+                        const u32x4 out = qodd ? u32x4{from_lo.x, from_lo.y, Z[1].x, Z[1].y}
+                                               : u32x4{Z[0].x, Z[0].y, from_hi.x, from_hi.y};
+                        const int v = vw + (2 * jp + (qodd ? 1 : 0)) * 16 + 4 * (k & ~1);
+                        const int rr = rb + 4 * h + (lane & 3);
+                        *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v) = out;
+                    }
                 }
+            }
+        };
+        if (c0 + vw + 128 <= V)
+            tile_body(Flag<true>{});
+        else
+            tile_body(Flag<false>{});
+        if (dzt) {
+            // the wave's own staging area: its LDS writes are complete once
+            // its lgkmcnt drains; then 16 lanes write 256 contiguous bytes of
+            // one dZ^T row (column v) per store
+            __builtin_amdgcn_s_waitcnt(0xf | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
+            const int nl = (lane & 15) * 8;
+            uint16_t* dst = dzt + static_cast<int64_t>(vw) * ld_dzt + row0 + t.wm * 128 + nl;
+#pragma unroll 8
+            for (int q = 0; q < 32; ++q) {
+                const int vl = 4 * q + (lane >> 4);
+                const u32x4 x = *reinterpret_cast<const u32x4*>(stage + vl * kStageRow + nl * 2);
+                *reinterpret_cast<u32x4*>(dst + static_cast<int64_t>(vl) * ld_dzt) = x;
             }
         }
     }
