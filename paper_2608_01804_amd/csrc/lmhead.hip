@@ -145,7 +145,7 @@ struct StatsEpi {
             s_y[tid] = (y >= 0 && y < V) ? y : -1;
         }
         __syncthreads();
-        const int lane = t.lane, c = lane & 15, h = lane >> 4;
+        const int lane = t.lane, c = lane & 15;
         const int col0 = t.col0();
         bool colok[8];
 #pragma unroll
@@ -263,16 +263,19 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 
 // ---------------------------------------------------------------------------
 // dZ epilogue: dz = g (onehot - 2^(z c - lse2)), zero past V, rounded to
-// bf16, stored twice with 16-byte stores.  A lane holds rows 4h .. 4h+3
-// (h = lane / 16) of column l % 16 of each 16 x 16 block; blocks are taken
-// in column pairs (j, j+1).
-//  * Transposed copy: lanes l and l ^ 16 (h even / odd) swap one block each,
-//    so the even lane holds rows 4h .. 4h+7 of its column in block j and the
-//    odd lane rows 4h-4 .. 4h+3 in block j+1: one run of 8 bf16 each.
+// bf16, stored twice with 16-byte non-temporal stores (the copies are read
+// back only by the next two GEMMs, after they have left the caches anyway).
+// A lane holds rows 4h .. 4h+3 (h = lane / 16) of column l % 16 of each
+// 16 x 16 block; blocks are taken in column pairs (j, j+1).
+//  * Transposed copy: lanes l and l ^ 16 (h even / odd) swap one block each
+//    (v_permlane16_swap), so the even lane holds rows 4h .. 4h+7 of its
+//    column in block j and the odd lane rows 4h-4 .. 4h+3 in block j+1; the
+//    runs go to a per-wave LDS staging area and are written back so that
+//    16 lanes cover the wave's 128 rows (256 bytes) of one dZ^T row.
 //  * Row-major copy: a 4 x 4 transpose inside each lane quad (two DPP
 //    exchanges) gives a lane 4 columns of one row; lanes l and l ^ 4
-//    (neighbouring quads) then swap one block each, so a lane holds 8
-//    consecutive columns of one row.
+//    (neighbouring quads) then swap one block each (DPP row rotates), so a
+//    lane holds 8 consecutive columns of one row.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -410,7 +413,7 @@ struct DzEpi {
                                                : u32x4{Z[0].x, Z[0].y, from_hi.x, from_hi.y};
                         const int v = vw + (2 * jp + (qodd ? 1 : 0)) * 16 + 4 * (k & ~1);
                         const int rr = rb + 4 * h + (lane & 3);
-                        *reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v) = out;
+                        __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v));
                     }
                 }
             }
@@ -430,7 +433,7 @@ struct DzEpi {
             for (int q = 0; q < 32; ++q) {
                 const int vl = 4 * q + (lane >> 4);
                 const u32x4 x = *reinterpret_cast<const u32x4*>(stage + vl * kStageRow + nl * 2);
-                *reinterpret_cast<u32x4*>(dst + static_cast<int64_t>(vl) * ld_dzt) = x;
+                __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(dst + static_cast<int64_t>(vl) * ld_dzt));
             }
         }
     }
@@ -439,7 +442,9 @@ struct DzEpi {
 // fp32 result tile into C[rows][cols] (leading dimension ldc, 16-byte aligned
 // rows): stored, or added to what C holds.  The 4 x 4 transpose inside each
 // lane quad gives every lane 4 consecutive columns of one row, so each store
-// (and each load of the accumulating form) moves 16 bytes per lane.
+// (and each load of the accumulating form) moves 16 bytes per lane; the
+// stores are non-temporal (the result is not read again by this call, or
+// only by the next chunk's accumulation).
 template <bool ACCUMULATE>
 struct StoreF32Epi {
     float* C;
@@ -465,7 +470,7 @@ struct StoreF32Epi {
                         const float4 o = *reinterpret_cast<const float4*>(p);
                         v.x += o.x, v.y += o.y, v.z += o.z, v.w += o.w;
                     }
-                    *reinterpret_cast<float4*>(p) = v;
+                    __builtin_nontemporal_store(f32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4*>(p));
                 } else {
 #pragma unroll
                     for (int b = 0; b < 4; ++b)
