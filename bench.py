@@ -413,6 +413,35 @@ def lmhead_leg(L, torch, dev, seed: int, reps: int):
                          "executed_frac": executed / t / MFMA_BF16_PEAK}}
 
 
+def blas_reference(torch, dev):
+    """Context only, not part of the path: torch's bf16 matmul (hipBLASLt) on
+    the shapes of the fused LM head's four GEMM passes, as plain products
+    with a bf16 result and no epilogue work.  Median of 3 timed calls."""
+    shapes = {"stats (H W^T)": (16384, 151936, 4096), "dZ chunk": (16384, 16384, 4096),
+              "dW chunk": (16384, 4096, 16384), "dH chunk": (16384, 4096, 16384)}
+    out = {}
+    for name, (m, n, k) in shapes.items():
+        a = torch.randn(m, k, device=dev, dtype=torch.bfloat16)
+        b = torch.randn(n, k, device=dev, dtype=torch.bfloat16) * 0.02
+        c = a @ b.t()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            c = a @ b.t()
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        t = float(np.median(ms))
+        out[name] = {"M": m, "N": n, "K": k, "ms": t, "TFLOPs": 2.0 * m * n * k / (t * 1e-3) / 1e12}
+        log(f"[bench] torch bf16 matmul {name} {m}x{n}x{k}: {t:.3f} ms, {out[name]['TFLOPs']:.0f} TFLOP/s")
+        del a, b, c
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -430,6 +459,9 @@ def main():
     ap.add_argument("--no-shard", action="store_true", help="skip the vocabulary-shard leg")
     ap.add_argument("--lmhead-only", action="store_true",
                     help="run only the fused LM-head leg and print its JSON object")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="with --lmhead-only: also time torch's bf16 matmul on the same GEMM "
+                         "shapes (context for the GEMM core, not part of the path)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -447,8 +479,10 @@ def main():
         raise SystemExit("the full workload does not fit resident; bench runs 'mid'")
 
     if args.lmhead_only:
-        print(json.dumps({"lmhead": lmhead_leg(L, torch, dev, 1005, max(1, args.lmhead_reps))}),
-              flush=True)
+        out = {"lmhead": lmhead_leg(L, torch, dev, 1005, max(1, args.lmhead_reps))}
+        if args.blas_reference:
+            out["blas_reference"] = blas_reference(torch, dev)
+        print(json.dumps(out), flush=True)
         return
 
     probe = hbm_probe(L, torch, dev)
