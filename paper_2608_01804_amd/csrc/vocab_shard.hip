@@ -206,6 +206,7 @@ __global__ __launch_bounds__(256) void merge_objective_kernel(
 // Shard backward: one workgroup per row.
 // ---------------------------------------------------------------------------
 constexpr int kBwdBlock = 256;
+constexpr int kBwdBatch = 4;
 
 __global__ __launch_bounds__(kBwdBlock) void shard_bwd_kernel(
     const uint16_t* logits, int64_t ld, int V, int vocab_start, const int32_t* __restrict__ token_ids,
@@ -234,29 +235,39 @@ __global__ __launch_bounds__(kBwdBlock) void shard_bwd_kernel(
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(xrow, nchunks * 16);
     const float c2 = kLog2e * inv_temp;
     const int yl = token_ids[row] - vocab_start;
-    for (int c = tid; c < nchunks; c += kBwdBlock) {
-        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, c * 16, 0, kLoadPolicy);
-        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-        float d[8];
+    // kBwdBatch chunks per thread are loaded before any is processed, so the
+    // loads of a batch are in flight together (past the row: zeros)
+    for (int cb = tid; cb < nchunks; cb += kBwdBatch * kBwdBlock) {
+        u32x4 vb[kBwdBatch];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            d[2 * q] = -g * __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -lse2));
-            d[2 * q + 1] = -g * __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -lse2));
-        }
-        const int e0 = c << 3;
-        if (yl >= e0 && yl < e0 + 8) {
+        for (int b = 0; b < kBwdBatch; ++b)
+            vb[b] = __builtin_amdgcn_raw_buffer_load_b128(rs, (cb + b * kBwdBlock) * 16, 0, kLoadPolicy);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (e0 + e == yl) d[e] += g;
-        }
-        if (c < nfull) {
-            const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
-                                       pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
-            __builtin_amdgcn_raw_buffer_store_b128(out, rd, c * 16, 0, kStorePolicy);
-        } else {
+        for (int b = 0; b < kBwdBatch; ++b) {
+            const int c = cb + b * kBwdBlock;
+            if (c >= nchunks) break;
+            const uint32_t wv[4] = {vb[b].x, vb[b].y, vb[b].z, vb[b].w};
+            float d[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (e < (V & 7)) drow[e0 + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+            for (int q = 0; q < 4; ++q) {
+                d[2 * q] = -g * __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -lse2));
+                d[2 * q + 1] = -g * __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -lse2));
+            }
+            const int e0 = c << 3;
+            if (yl >= e0 && yl < e0 + 8) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (e0 + e == yl) d[e] += g;
+            }
+            if (c < nfull) {
+                const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
+                                           pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
+                __builtin_amdgcn_raw_buffer_store_b128(out, rd, c * 16, 0, kStorePolicy);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (e < (V & 7)) drow[e0 + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+            }
         }
     }
 }
