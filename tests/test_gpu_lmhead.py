@@ -61,6 +61,7 @@ def test_lmhead_reduced_shape_full_parity():
     (1, 300, 64, 1.0, 0),         # a single row, one k-tile
     (513, 16640, 128, 1.25, 0),   # two 16384-column chunks, the last one 256 wide
     (129, 33000, 64, 1.0, 1),     # three chunks, the last 256 wide with 232 live columns
+    (70, 700, 192, 1.0, 0),       # three k-tiles along H (odd count > 1), ragged everywhere
 ])
 def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
     U.log(f"lmhead ragged N={N} V={V} H={H} T^-1={inv_temp} kl={kl_type}")
