@@ -235,7 +235,8 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
     """The vocabulary-parallel entry points at one shard's real shape: the
     first microbatch's rows, the first V / n_shards columns of the resident
     logits (row stride V), n_shards partials for the merge (shard 0's own and
-    copies that own no token).  HIP events on the launch stream; median."""
+    copies that own no token).  HIP events on the launch stream around `reps`
+    back-to-back calls (as in a training step), per-call average."""
     V, R = s["V"], s["R"]
     vs = V // n_shards
     lg = s["logits"][:R]
@@ -254,16 +255,14 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
     def timed(fn):
         fn()
         torch.cuda.synchronize()
-        ms = []
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         for _ in range(reps):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
             fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ms.append(e0.elapsed_time(e1))
-        return float(np.median(ms)) / 1e3
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps / 1e3
 
     t_stats = timed(lambda: L.leap_vocab_shard_stats(lg, V, R, vs, 0, tok, w, 1.0, parts[0]))
     parts[1:] = parts[0]
