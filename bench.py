@@ -288,6 +288,35 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
             "stats_frac": stats_bytes / t_stats / HBM_PEAK, "bwd_frac": bwd_bytes / t_bwd / HBM_PEAK}
 
 
+def logprob_leg(L, torch, s, reps: int = 20):
+    """The forward-only log-probability (old-policy / reference passes) on the
+    first microbatch of the resident logits, every row read: HIP events on the
+    launch stream around `reps` back-to-back calls, per-call average."""
+    V, R = s["V"], s["R"]
+    lg, tok = s["logits"][:R], s["tok"][:R]
+    out = torch.empty(R, dtype=torch.float32, device=lg.device)
+    stream = torch.cuda.current_stream()
+
+    def call():
+        L.leap_logprob_fwd(lg, V, R, V, tok, None, 1.0, out, s["err"])
+
+    call()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps / 1e3
+    nbytes = R * (2 * V + 8)
+    log(f"[bench] forward-only log-prob {R} x {V}: {t * 1e6:.1f} us ({nbytes / t / 1e9:.0f} GB/s)")
+    return {"workload": f"forward-only log-prob: first microbatch ({R} rows, all read) x {V}",
+            "call_us": t * 1e6, "GBps": nbytes / t / 1e9, "frac": nbytes / t / HBM_PEAK,
+            "bytes_per_call": nbytes}
+
+
 def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
     """fp32 log-softmax of hidden weight^T at y with torch, a block of rows at
     a time: input preparation for the old / reference log-probabilities."""
@@ -530,6 +559,7 @@ def main():
         cpu = cpu_baseline(s, args.cpu_seconds)
 
     shard = shard_leg(L, torch, s) if not args.no_shard else None
+    fwd = logprob_leg(L, torch, s)
     rstats = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
@@ -564,6 +594,7 @@ def main():
         "cpu_baseline": cpu,
         "lmhead": lm,
         "vocab_shard": shard,
+        "logprob_fwd": fwd,
         "rollout_stats": rstats,
     }
     print(json.dumps(out), flush=True)
