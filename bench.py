@@ -445,8 +445,8 @@ def blas_reference(torch, dev):
     """Context only, not part of the path: torch's bf16 matmul (hipBLASLt) on
     the shapes of the fused LM head's four GEMM passes, as plain products
     with a bf16 result and no epilogue work.  Median of 3 timed calls."""
-    shapes = {"stats (H W^T)": (16384, 151936, 4096), "dZ chunk": (16384, 16384, 4096),
-              "dW chunk": (16384, 4096, 16384), "dH chunk": (16384, 4096, 16384)}
+    shapes = {"stats (H W^T)": (16384, 151936, 4096), "dZ chunk": (16384, 32768, 4096),
+              "dW chunk": (32768, 4096, 16384), "dH chunk": (16384, 4096, 32768)}
     out = {}
     for name, (m, n, k) in shapes.items():
         a = torch.randn(m, k, device=dev, dtype=torch.bfloat16)

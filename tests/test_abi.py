@@ -260,14 +260,24 @@ def test_lmhead_workspace_size():
     assert L.leap_lmhead_workspace_size(8, 0, 64) == 0
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
-    # 16384 x 151936 x 4096: transposes (H*N_pad, and H*16384 per vocabulary
-    # chunk, bf16), per-tile row
-    # statistics, four per-row vectors and one 16384-column chunk of dZ in two layouts
-    n, v, h = 16384, 151936, 4096
-    v_pad = (v + 255) // 256 * 256
-    chunks = -(-v_pad // 16384)
-    want = 2 * h * n + 2 * h * 16384 * chunks + 8 * n * (v_pad // 256) + 4 * 4 * n + 2 * 2 * n * 16384
-    assert abs(L.leap_lmhead_workspace_size(n, v, h) - want) <= 9 * 256
+    # transposes (H*N_pad, and H*chunk per vocabulary chunk, bf16), per-tile
+    # row statistics, four per-row vectors and one chunk of dZ in two layouts;
+    # chunks are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
+    def want(n, v, h):
+        n_pad = (n + 255) // 256 * 256
+        v_pad = (v + 255) // 256 * 256
+        vc = 32768 if n_pad * 32768 * 2 < (1 << 32) - 64 else 16384
+        vc = min(vc, v_pad)
+        chunks = -(-v_pad // vc)
+        return (2 * h * n_pad + 2 * h * vc * chunks + 8 * n_pad * (v_pad // 256) + 4 * 4 * n_pad
+                + 2 * 2 * n_pad * vc)
+
+    for n, v, h in [(16384, 151936, 4096), (65280, 151936, 4096), (65281, 151936, 4096),
+                    (1000, 20000, 512)]:
+        assert abs(L.leap_lmhead_workspace_size(n, v, h) - want(n, v, h)) <= 9 * 256, (n, v, h)
+    # the narrow chunk takes over from N_pad = 65536 (a 4 GiB dZ chunk otherwise)
+    assert (L.leap_lmhead_workspace_size(65281, 151936, 4096)
+            < L.leap_lmhead_workspace_size(65280, 151936, 4096))
 
 
 def test_vocab_shard_entry_points_reject():

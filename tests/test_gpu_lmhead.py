@@ -59,8 +59,9 @@ def test_lmhead_reduced_shape_full_parity():
     (300, 1000, 128, 0.8, 1),     # ragged rows and vocabulary, one chunk
     (257, 8492, 64, 1.0, 2),      # one chunk, 8704 wide with 8492 live columns
     (1, 300, 64, 1.0, 0),         # a single row, one k-tile
-    (513, 16640, 128, 1.25, 0),   # two 16384-column chunks, the last one 256 wide
-    (129, 33000, 64, 1.0, 1),     # three chunks, the last 256 wide with 232 live columns
+    (513, 16640, 128, 1.25, 0),   # one chunk, 65 tiles wide
+    (129, 33000, 64, 1.0, 1),     # two 32768-column chunks, the last 256 wide with 232 live columns
+    (65, 70000, 64, 1.0, 2),      # three chunks (dH accumulated twice), the last 4608 wide
     (70, 700, 192, 1.0, 0),       # three k-tiles along H (odd count > 1), ragged everywhere
 ])
 def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
