@@ -280,8 +280,9 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  *            transposed operands, per-tile row statistics and one vocabulary
  *            chunk of dZ in both layouts.
  * Limits: each operand and workspace matrix below 4 GiB (32-bit offsets in
- * the GEMM core; for H = 4096 that allows V up to about 500000 and N up to
- * about 500000); otherwise LEAP_ERR_UNSUPPORTED.
+ * the GEMM core): for H = 4096, V up to about 520000, and N up to 130816
+ * once V reaches 16384 (a dZ chunk holds N_pad x 16384 bf16; chunks are
+ * 32768 columns for N up to 65280); otherwise LEAP_ERR_UNSUPPORTED.
  * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, H < 1, accumulate_dweight
  * not 0 or 1, a parameter out of range, a required pointer NULL;
  * LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE; LEAP_ERR_UNSUPPORTED.

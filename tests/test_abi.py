@@ -233,6 +233,8 @@ def _lmhead(**kw):
     (dict(H=48), L.LEAP_ERR_UNSUPPORTED),
     (dict(H=96), L.LEAP_ERR_UNSUPPORTED),  # k-tiles of 64
     (dict(V=1 << 20, H=4096), L.LEAP_ERR_UNSUPPORTED),  # W beyond 32-bit offsets
+    (dict(N=131072, V=151936, H=4096), L.LEAP_ERR_UNSUPPORTED),  # one 16384-column dZ chunk past 4 GiB
+    (dict(N=130816, V=151936, H=4096), L.LEAP_ERR_WORKSPACE),  # largest N that fits; only the workspace is short
     (dict(hidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(weight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
     (dict(dweight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
