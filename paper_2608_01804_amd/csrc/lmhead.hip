@@ -5,9 +5,9 @@
 //
 // Steps of one call, all on the caller's stream:
 //  1. H and W are transposed once into the workspace (Ht [H][N_pad]; Wt
-//     chunk-major, [chunk][H][chunk width]; both zero padded), because every
-//     GEMM below runs on one NT core whose operands are both contiguous along
-//     the contraction index.
+//     chunk-major, [chunk][H][chunk width]; both zero padded), because the
+//     GEMM core takes B contiguous along the contraction index (and A either
+//     way: contiguous along it, or k-major through transposing LDS reads).
 //  2. Stats GEMM  Z = H W^T on MFMA.  Its epilogue turns every row of a
 //     256 x 256 tile into a partial (max, sum 2^(z c - max)) in base-2 units
 //     (c = log2(e) / T) and picks out the rollout token's logit.
@@ -17,9 +17,9 @@
 //     g = w dloss/dlogp / T).  A fixed-order reduction sums the loss.
 //  4. Per vocabulary chunk (32768 columns, 16384 for very large N): the Z
 //     tiles are recomputed and the epilogue writes dZ = g (onehot - p) in
-//     bf16, row-major [N_pad][chunk] and transposed [chunk][N_pad]; then
-//     dW[chunk] = dZ^T H and dH (+)= dZ W[chunk] run as two more GEMMs with
-//     fp32 epilogues.
+//     bf16, row-major [N_pad][chunk]; then dW[chunk] = dZ^T H (dZ read
+//     k-major) and dH (+)= dZ W[chunk] run as two more GEMMs with fp32
+//     epilogues.
 // Executed work is 8 N H V flops (the forward GEMM is recomputed once).
 #include "mfma_gemm.h"
 #include "row_common.h"
@@ -266,19 +266,13 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 
 // ---------------------------------------------------------------------------
 // dZ epilogue: dz = g (onehot - 2^(z c - lse2)), zero past V, rounded to
-// bf16, stored twice with 16-byte non-temporal stores (the copies are read
-// back only by the next two GEMMs, after they have left the caches anyway).
-// A lane holds rows 4h .. 4h+3 (h = lane / 16) of column l % 16 of each
-// 16 x 16 block; blocks are taken in column pairs (j, j+1).
-//  * Transposed copy: lanes l and l ^ 16 (h even / odd) swap one block each
-//    (v_permlane16_swap), so the even lane holds rows 4h .. 4h+7 of its
-//    column in block j and the odd lane rows 4h-4 .. 4h+3 in block j+1; the
-//    runs go to a per-wave LDS staging area and are written back so that
-//    16 lanes cover the wave's 128 rows (256 bytes) of one dZ^T row.
-//  * Row-major copy: a 4 x 4 transpose inside each lane quad (two DPP
-//    exchanges) gives a lane 4 columns of one row; lanes l and l ^ 4
-//    (neighbouring quads) then swap one block each (DPP row rotates), so a
-//    lane holds 8 consecutive columns of one row.
+// bf16, stored row-major with 16-byte non-temporal stores (read back only by
+// the next two GEMMs, after it has left the caches anyway).  A lane holds
+// rows 4h .. 4h+3 (h = lane / 16) of column l % 16 of each 16 x 16 block;
+// blocks are taken in column pairs (j, j+1): a 4 x 4 transpose inside each
+// lane quad (two DPP exchanges) gives a lane 4 columns of one row; lanes l
+// and l ^ 4 (neighbouring quads) then swap one block each (DPP row rotates),
+// so a lane holds 8 consecutive columns of one row.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -317,19 +311,12 @@ __device__ __forceinline__ uint32_t dpp_row_ror12(uint32_t v) {
     return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x12C, 0xF, 0xF, false));
 }
 
-constexpr int kStageRow = 128 * 2 + 16;            // bytes per staged column (128 rows + pad)
-constexpr int kStageWave = 128 * kStageRow;          // 34816 bytes per wave
-constexpr int kStageBase = 4096;                     // after the per-row arrays (3 KiB)
-static_assert(kStageBase + 4 * kStageWave <= gemm::kLdsBytes, "dZ staging exceeds the GEMM's LDS");
-
 struct DzEpi {
     const int32_t* token_ids;
     const float* lse2;
     const float* g;
-    uint16_t* dz;   // [N_pad][ld_dz], chunk-local columns; null: not written
+    uint16_t* dz;  // [N_pad][ld_dz], chunk-local columns
     int64_t ld_dz;
-    uint16_t* dzt;  // [chunk][ld_dzt]; null: not written
-    int64_t ld_dzt;
     int64_t N;
     int V, c0;  // vocabulary size, first column of the chunk
     float c2;
@@ -338,10 +325,6 @@ struct DzEpi {
         float* s_l = reinterpret_cast<float*>(smem);
         float* s_g = s_l + kTile;
         int* s_y = reinterpret_cast<int*>(s_g + kTile);
-        // per-wave staging area for the transposed copy: 128 columns x 128
-        // rows of bf16, rows padded to 272 bytes so that 16 lanes writing 16
-        // bytes each to 16 consecutive columns hit distinct banks
-        uint8_t* stage = smem + kStageBase + (t.wm * 2 + t.wn) * kStageWave;
         const int tid = threadIdx.x;
         const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
         {
@@ -359,7 +342,6 @@ struct DzEpi {
         }
         __syncthreads();
         const int lane = t.lane, c = lane & 15, h = lane >> 4;
-        const bool hodd = (h & 1) != 0;
         const int k = c >> 2;              // lane quad within the 16 columns
         const bool qodd = (k & 1) != 0;
         const int vw = t.col0();  // chunk-local column of the wave's block
@@ -386,21 +368,7 @@ struct DzEpi {
                             d[e][r] = colok ? dd : 0.0f;
                         }
                     }
-                    if (dzt) {
-                        // v_permlane16_swap trades the odd 16-lane rows of its
-                        // first operand for the even rows of its second: an even-h
-                        // lane gets its partner's block-j0 rows, an odd-h lane its
-                        // partner's block-j1 rows, with no selects.  The 8 rows
-                        // go to the wave's column-major staging area.
-                        const uint32_t p0x = pack_bf16(d[0][0], d[0][1]), p0y = pack_bf16(d[0][2], d[0][3]);
-                        const uint32_t p1x = pack_bf16(d[1][0], d[1][1]), p1y = pack_bf16(d[1][2], d[1][3]);
-                        const auto sx = __builtin_amdgcn_permlane16_swap(p0x, p1x, false, false);
-                        const auto sy = __builtin_amdgcn_permlane16_swap(p0y, p1y, false, false);
-                        const int vl = (2 * jp + (hodd ? 1 : 0)) * 16 + c;  // column in the wave block
-                        const int nl = i * 16 + 4 * (h & ~1);               // first of the 8 rows
-                        *reinterpret_cast<u32x4*>(stage + vl * kStageRow + nl * 2) = u32x4{sx[0], sy[0], sx[1], sy[1]};
-                    }
-                    if (dz) {
+                    {
                         uint2 Z[2];
 #pragma unroll
                         for (int e = 0; e < 2; ++e) {
@@ -425,20 +393,6 @@ struct DzEpi {
             tile_body(Flag<true>{});
         else
             tile_body(Flag<false>{});
-        if (dzt) {
-            // the wave's own staging area: its LDS writes are complete once
-            // its lgkmcnt drains; then 16 lanes write 256 contiguous bytes of
-            // one dZ^T row (column v) per store
-            __builtin_amdgcn_s_waitcnt(0xf | (0x7 << 4) | (0x3 << 14));  // lgkmcnt(0)
-            const int nl = (lane & 15) * 8;
-            uint16_t* dst = dzt + static_cast<int64_t>(vw) * ld_dzt + row0 + t.wm * 128 + nl;
-#pragma unroll 8
-            for (int q = 0; q < 32; ++q) {
-                const int vl = 4 * q + (lane >> 4);
-                const u32x4 x = *reinterpret_cast<const u32x4*>(stage + vl * kStageRow + nl * 2);
-                __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(dst + static_cast<int64_t>(vl) * ld_dzt));
-            }
-        }
     }
 };
 
@@ -509,7 +463,7 @@ Dims dims_of(int64_t N, int V, int H) {
 }
 
 struct Layout {
-    size_t ht, wt, part, zy, lse2, g, row_loss, dz, dzt, total;
+    size_t ht, wt, part, zy, lse2, g, row_loss, dz, total;
 };
 
 Layout layout_of(const Dims& d) {
@@ -528,7 +482,6 @@ Layout layout_of(const Dims& d) {
     L.g = take(static_cast<size_t>(d.N_pad) * 4);
     L.row_loss = take(static_cast<size_t>(d.N_pad) * 4);
     L.dz = take(static_cast<size_t>(d.N_pad) * d.Vc * 2);
-    L.dzt = take(static_cast<size_t>(d.Vc) * d.N_pad * 2);
     L.total = off;
     return L;
 }
@@ -542,7 +495,6 @@ bool fits32(int64_t rows_padded, int64_t ld) {
 bool shapes_fit(const Dims& d) {
     return fits32(d.N_pad, d.H) &&       // H   [N][H]
            fits32(d.V_pad, d.H) &&       // W   [V][H]
-           fits32(d.Vc, d.N_pad) &&      // dZt [chunk][N_pad]
            fits32(d.H_pad, d.N_pad) &&   // Ht  [H][N_pad]
            fits32(d.N_pad, d.Vc) &&      // dZ  [N_pad][chunk]
            fits32(d.H_pad, d.Vc);        // Wt  [H][chunk] per chunk
@@ -552,13 +504,13 @@ uint32_t extent32(uint64_t bytes) {
     return bytes > 0xffffffffull ? 0xffffffffu : static_cast<uint32_t>(bytes);
 }
 
-template <class Epi>
+template <bool AKM = false, class Epi>
 leap_status gemm_nt(const uint16_t* A, int64_t lda, uint64_t a_bytes, const uint16_t* B, int64_t ldb,
                     uint64_t b_bytes, int K, int64_t M, int64_t Ncols, const Epi& epi,
                     hipStream_t stream) {
     const int tiles_m = static_cast<int>((M + kTile - 1) / kTile);
     const int tiles_n = static_cast<int>((Ncols + kTile - 1) / kTile);
-    hipLaunchKernelGGL(gemm::gemm_nt_kernel<Epi>, dim3(gemm::gemm_grid(tiles_m, tiles_n)),
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<Epi, AKM>), dim3(gemm::gemm_grid(tiles_m, tiles_n)),
                        dim3(gemm::kThreads), 0, stream, A, lda, extent32(a_bytes), B, ldb,
                        extent32(b_bytes), K, tiles_m, tiles_n, epi);
     return launch_status();
@@ -614,7 +566,6 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     float* g = reinterpret_cast<float*>(ws + L.g);
     float* row_loss = reinterpret_cast<float*>(ws + L.row_loss);
     uint16_t* dz = reinterpret_cast<uint16_t*>(ws + L.dz);
-    uint16_t* dzt = reinterpret_cast<uint16_t*>(ws + L.dzt);
     const uint16_t* Hm = static_cast<const uint16_t*>(hidden_bf16);
     const uint16_t* Wm = static_cast<const uint16_t*>(weight_bf16);
     leap_status st;
@@ -672,8 +623,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     for (int c0 = 0; c0 < V; c0 += d.Vc) {
         const int vl = (d.V_pad - c0) < d.Vc ? (d.V_pad - c0) : d.Vc;  // multiple of 256
         {
-            const DzEpi epi{token_ids, lse2, g, dhidden ? dz : nullptr, d.Vc,
-                            dweight ? dzt : nullptr, d.N_pad, N, V, c0, c2};
+            const DzEpi epi{token_ids, lse2, g, dz, d.Vc, N, V, c0, c2};
             const uint64_t wb = static_cast<uint64_t>(V - c0) * H * 2;
             if ((st = gemm_nt(Hm, H, h_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
                               epi, stream)) != LEAP_OK)
@@ -682,14 +632,15 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
         if (dweight) {
             const int64_t rows = (V - c0) < vl ? (V - c0) : vl;
             float* C = dweight + static_cast<int64_t>(c0) * H;
-            const uint64_t ab = static_cast<uint64_t>(vl) * d.N_pad * 2;
+            // A = dZ read k-major: [N_pad][Vc], the chunk's vl columns
+            const uint64_t ab = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
             const uint64_t bb = static_cast<uint64_t>(H) * d.N_pad * 2;
             const int K = static_cast<int>(d.N_pad);
             st = accumulate_dweight
-                     ? gemm_nt(dzt, d.N_pad, ab, ht, d.N_pad, bb, K, vl, H,
-                               StoreF32Epi<true>{C, H, rows, H}, stream)
-                     : gemm_nt(dzt, d.N_pad, ab, ht, d.N_pad, bb, K, vl, H,
-                               StoreF32Epi<false>{C, H, rows, H}, stream);
+                     ? gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
+                                     StoreF32Epi<true>{C, H, rows, H}, stream)
+                     : gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
+                                     StoreF32Epi<false>{C, H, rows, H}, stream);
             if (st != LEAP_OK) return st;
         }
         if (dhidden) {

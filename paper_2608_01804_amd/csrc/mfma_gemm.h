@@ -32,6 +32,14 @@
 //  * Tiles are numbered so the workgroups one XCD runs at once form a compact
 //    GROUP x (32 / GROUP) patch (see tile_of_block).
 //
+//  * A may instead be stored k-major ([K][lda], contiguous along m; AKM): its
+//    k-tile is 64 LDS rows of 512 bytes (256 m), chunk c of row r at
+//    c ^ (2 * ((r & 3) | ((r >> 3 & 1) << 2))), and each A fragment is two
+//    ds_read_b64_tr_b16 (4 k each), which transpose 4 x 4 bf16 blocks
+//    across each 16-lane group on the way out of the LDS.  The swizzle term
+//    does depend on the 16-row block there, so each lane keeps 8 precomputed
+//    fragment addresses.
+//
 // v_mfma_f32_16x16x32_bf16 (lane l of 64): A row l%16 with k = 8*(l/16) .. +7;
 // B column l%16 with the same k; accumulator register r holds
 // C[row 4*(l/16) + r][column l%16].  So acc[i][j][r] of lane l is
@@ -40,6 +48,8 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 namespace leap {
 namespace gemm {
@@ -126,9 +136,38 @@ inline int gemm_grid(int tiles_m, int tiles_n) {
 // The k-loop; leaves the wave's 8 x 8 accumulator blocks in acc.  Requires
 // K % 64 == 0, lda and ldb multiples of 8, and every row offset the tiles
 // reach ((tiles * 256) * ld * 2 bytes) below 4 GiB; a_bytes / b_bytes are the
-// readable extents (rows past them read as 0).  On return every load has
-// landed and every wave is past its last LDS read, so the epilogue may use
-// the LDS.
+// readable extents (rows past them read as 0).  With AKM, A is [K][lda] and
+// every m-tile must lie inside a row (tiles_m * 256 <= lda).  On return every
+// load has landed and every wave is past its last LDS read, so the epilogue
+// may use the LDS.
+//
+// ds_read_b64_tr_b16, per 16-lane group: lane i receives element i % 4 of the
+// 4-element (8-byte) rows that lanes i / 4, i / 4 + 4, i / 4 + 8 and
+// i / 4 + 12 point at, in that order.  With lane 4e + q pointing at k-row
+// k0 + e, columns m0 + 4q .. +3, lane i receives column m0 + i of k-rows
+// k0 .. k0 + 3: the first (or second) half of an MFMA A fragment.
+__device__ __forceinline__ uint32_t akm_swizzle(int r) {
+    return static_cast<uint32_t>(((r & 3) | (((r >> 3) & 1) << 2)) << 1);
+}
+
+// A compile-time int (an LDS slot index known to the unrolled k-loop).
+template <int V>
+struct IntC {
+    static constexpr int value = V;
+};
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ bf16x8 read_a_km(const uint8_t* p) {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * 512));
+    const s16x8 both = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    return __builtin_bit_cast(bf16x8, both);
+}
+
+template <bool AKM>
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t lda,
                                          uint32_t a_bytes, const uint16_t* __restrict__ B,
                                          int64_t ldb, uint32_t b_bytes, int K, int tm, int tn,
@@ -154,14 +193,25 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
     // DMA mapping: instruction q (0..7) of wave w fills rows (8w + q)*8 .. +7
     // of a 256-row operand tile (1 KiB, LDS-contiguous); lane l writes row
     // +l/8 at LDS position l%8, which holds chunk (l%8) ^ ((row >> 1) & 7).
+    // AKM: instruction q fills k-rows 2(8w + q) and +1; lane l writes k-row
+    // +l/32 at position l%32, which holds chunk (l%32) ^ akm_swizzle(row).
     uint32_t voff_a[8], voff_b[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int r = (wave * 8 + q) * 8 + (lane >> 3);
         const int c = (lane & 7) ^ ((r >> 1) & 7);
-        voff_a[q] = static_cast<uint32_t>((static_cast<int64_t>(tm) * kBM + r) * lda * 2 + c * 16);
+        if (AKM) {
+            const int kr = 2 * (wave * 8 + q) + (lane >> 5);
+            const int ca = static_cast<int>((lane & 31) ^ akm_swizzle(kr));
+            voff_a[q] = static_cast<uint32_t>(static_cast<int64_t>(kr) * lda * 2 +
+                                              (static_cast<int64_t>(tm) * kBM + ca * 8) * 2);
+        } else {
+            voff_a[q] = static_cast<uint32_t>((static_cast<int64_t>(tm) * kBM + r) * lda * 2 + c * 16);
+        }
         voff_b[q] = static_cast<uint32_t>((static_cast<int64_t>(tn) * kBN + r) * ldb * 2 + c * 16);
     }
+    // byte offset of A k-tile kt from k-tile 0
+    const uint32_t a_kstep = AKM ? static_cast<uint32_t>(kBK * lda * 2) : kBK * 2;
     const int KT = K / kBK;
     // load q of A k-tile kt into its slot kt % 2 (zeros past the last k-tile)
     auto dma_a = [&](int kt, int q) {
@@ -169,7 +219,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
         uint8_t* st = smem + (kt & 1) * kTileBytes;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             live ? ra : rz, (__attribute__((address_space(3))) void*)(st + (wave * 8 + q) * 1024), 16,
-            voff_a[q], (live ? kt : 0) * kBK * 2, 0, 0);
+            voff_a[q], (live ? kt : 0) * a_kstep, 0, 0);
     };
     // load q of B k-tile kt into B slot `slot` (== kt % 3)
     auto dma_b = [&](int kt, int slot, int q) {
@@ -190,17 +240,39 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
         lane_a[s] = static_cast<uint32_t>((wm * 128 + lr) * 128 + pos);
         lane_b[s] = static_cast<uint32_t>((wn * 128 + lr) * 128 + pos);
     }
+    // AKM fragment f of step s, first half: lane 4e + q of group g points at
+    // k-row 32s + 8g + e, columns wm*128 + 16f + 4q .. +3, i.e. chunk
+    // wm*16 + 2f + q/2 (half q%2), swizzled by akm_swizzle(8g + e); the step
+    // adds 32 rows (16 KiB), the second half 4 rows (2 KiB).
+    uint32_t lane_akm[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        const int e = lr >> 2, q = lr & 3;
+        const int kr = 8 * lc + e;
+        const uint32_t chunk = static_cast<uint32_t>(wm * 16 + 2 * f + (q >> 1)) ^ akm_swizzle(kr);
+        lane_akm[f] = static_cast<uint32_t>(kr * 512) + chunk * 16 + static_cast<uint32_t>((q & 1) * 8);
+    }
+    auto read_a = [&](const uint8_t* slot, int s, int f) -> bf16x8 {
+        if (AKM) return read_a_km(slot + lane_akm[f] + s * 16384);
+        return *reinterpret_cast<const bf16x8*>(slot + lane_a[s] + f * 2048);
+    };
     bf16x8 fa[8], fb0[8], fb1[8];
     // One k = 32 step: 64 MFMAs on (fa, xb), row by row over the 8 x 8
     // blocks.  Meanwhile the fragments of step s of the slots (as, bsl) (s < 0:
     // none): B into yb during rows 0-3, A block i into fa right after row i;
     // and the loads dma(i), one per row, after the row's second MFMA.
-    auto step = [&](const bf16x8(&xb)[8], bf16x8(&yb)[8], int as, int bsl, int s, auto&& dma) {
-        // slot bases as opaque scalars: one vector add per step, and the 8
-        // reads per operand then use immediate offsets
-        const uint32_t a_base = __builtin_amdgcn_readfirstlane(as * kTileBytes);
+    // The A slot is a compile-time IntC inside the unrolled k-loop (its base
+    // folds into the reads' immediate offsets) and a run-time int in the
+    // tail; the B slot is always a run-time int.  Run-time slot bases are
+    // opaque scalars: one vector add per step, and the 8 reads per operand
+    // then use immediate offsets.
+    auto step = [&](const bf16x8(&xb)[8], bf16x8(&yb)[8], auto as, int bsl, int s, auto&& dma) {
+        const uint8_t* pas;
+        if constexpr (std::is_integral<decltype(as)>::value)
+            pas = smem + __builtin_amdgcn_readfirstlane(as * kTileBytes);
+        else
+            pas = smem + decltype(as)::value * kTileBytes;
         const uint32_t b_base = __builtin_amdgcn_readfirstlane((kASlots + bsl) * kTileBytes);
-        const uint8_t* pa = smem + (a_base + lane_a[s < 0 ? 0 : s]);
         const uint8_t* pb = smem + (b_base + lane_b[s < 0 ? 0 : s]);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -218,7 +290,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
-            if (s >= 0) fa[i] = *reinterpret_cast<const bf16x8*>(pa + i * 2048);
+            if (s >= 0) fa[i] = read_a(pas, s, i);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -235,28 +307,41 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
     wait_vmcnt<16>();  // A(0), B(0) landed; B(1) and A(1) may fly
     stage_barrier();
     {
-        const uint8_t* pa = smem + lane_a[0];
         const uint8_t* pb = smem + kASlots * kTileBytes + lane_b[0];
 #pragma unroll
         for (int f = 0; f < 8; ++f) {
-            fa[f] = *reinterpret_cast<const bf16x8*>(pa + f * 2048);
+            fa[f] = read_a(smem, 0, f);
             fb0[f] = *reinterpret_cast<const bf16x8*>(pb + f * 2048);
         }
     }
     int bs = 0;  // B slot of k-tile kt
-    for (int kt = 0; kt + 1 < KT; ++kt) {
-        const int as = kt & 1;
+    // one k-tile kt (not the last); as_a: its A slot kt % 2, an IntC or an int
+    auto ktile = [&](int kt, auto as_a, auto as_b) {
         const int b2 = bs == 0 ? 2 : bs - 1;  // slot of B(kt+2) == slot of B(kt-1)
         const int bn = bs == 2 ? 0 : bs + 1;
         // step 0: step-1 fragments of the same slots; B(kt+2) streams in
-        step(fb0, fb1, as, bs, 1, [&](int i) { dma_b(kt + 2, b2, i); });
+        step(fb0, fb1, as_a, bs, 1, [&](int i) { dma_b(kt + 2, b2, i); });
         // k-tile kt+1 has landed (only B(kt+2) may still fly); after the
         // barrier A slot kt % 2 and B slot kt % 3 are free
         wait_vmcnt<8>();
         stage_barrier();
         // step 1: step-0 fragments of k-tile kt+1; A(kt+2) into A slot kt % 2
-        step(fb1, fb0, as ^ 1, bn, 0, [&](int i) { dma_a(kt + 2, i); });
+        step(fb1, fb0, as_b, bn, 0, [&](int i) { dma_a(kt + 2, i); });
         bs = bn;
+    };
+    int kt = 0;
+    if constexpr (AKM) {
+        // the k-major reads keep run-time slot bases: unrolled, this loop
+        // measured 21% slower
+        for (; kt + 1 < KT; ++kt) ktile(kt, kt & 1, (kt & 1) ^ 1);
+    } else {
+        // unrolled by two: the A slot bases become immediate offsets (2-4%
+        // faster on every NT pass)
+        for (; kt + 2 < KT; kt += 2) {
+            ktile(kt, IntC<0>{}, IntC<1>{});
+            ktile(kt + 1, IntC<1>{}, IntC<0>{});
+        }
+        if (kt + 1 < KT) ktile(kt, IntC<0>{}, IntC<1>{});
     }
     {
         const int as = (KT - 1) & 1;
@@ -270,9 +355,10 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
     stage_barrier();
 }
 
-// One kernel per epilogue.  The epilogue gets the accumulators, the tile and
-// the (idle) LDS buffer; it is called after the last barrier of the k-loop.
-template <class Epi>
+// One kernel per epilogue and A layout.  The epilogue gets the accumulators,
+// the tile and the (idle) LDS buffer; it is called after the last barrier of
+// the k-loop.
+template <class Epi, bool AKM = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 gemm_nt_kernel(const uint16_t* __restrict__ A, int64_t lda, uint32_t a_bytes,
                const uint16_t* __restrict__ B, int64_t ldb, uint32_t b_bytes, int K, int tiles_m,
@@ -281,7 +367,7 @@ gemm_nt_kernel(const uint16_t* __restrict__ A, int64_t lda, uint32_t a_bytes,
     int tm, tn;
     if (!tile_of_block<kGroupM>(tiles_m, tiles_n, tm, tn)) return;
     f32x4 acc[8][8];
-    mainloop(A, lda, a_bytes, B, ldb, b_bytes, K, tm, tn, smem, acc);
+    mainloop<AKM>(A, lda, a_bytes, B, ldb, b_bytes, K, tm, tn, smem, acc);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     Tile t{tm, tn, wave >> 1, wave & 1, static_cast<int>(threadIdx.x & 63)};
     epi(acc, t, smem);

@@ -263,8 +263,8 @@ def test_lmhead_workspace_size():
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
     # transposes (H*N_pad, and H*chunk per vocabulary chunk, bf16), per-tile
-    # row statistics, four per-row vectors and one chunk of dZ in two layouts;
-    # chunks are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
+    # row statistics, four per-row vectors and one bf16 chunk of dZ; chunks
+    # are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
     def want(n, v, h):
         n_pad = (n + 255) // 256 * 256
         v_pad = (v + 255) // 256 * 256
@@ -272,7 +272,7 @@ def test_lmhead_workspace_size():
         vc = min(vc, v_pad)
         chunks = -(-v_pad // vc)
         return (2 * h * n_pad + 2 * h * vc * chunks + 8 * n_pad * (v_pad // 256) + 4 * 4 * n_pad
-                + 2 * 2 * n_pad * vc)
+                + 2 * n_pad * vc)
 
     for n, v, h in [(16384, 151936, 4096), (65280, 151936, 4096), (65281, 151936, 4096),
                     (1000, 20000, 512)]:
