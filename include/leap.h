@@ -278,7 +278,7 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  *            16-byte aligned, scratch for this call only (calls sharing one
  *            workspace must be ordered on one stream).  It holds the
  *            transposed operands, per-tile row statistics and one vocabulary
- *            chunk of dZ in both layouts.
+ *            chunk of dZ (bf16, row-major).
  * Limits: each operand and workspace matrix below 4 GiB (32-bit offsets in
  * the GEMM core): for H = 4096, V up to about 520000, and N up to 130816
  * once V reaches 16384 (a dZ chunk holds N_pad x 16384 bf16; chunks are
