@@ -33,6 +33,8 @@ using gemm::f32x4;
 using gemm::Tile;
 using obj::Params;
 using obj::RowOut;
+using row::bf_hi;
+using row::bf_lo;
 using row::ms_merge;
 using row::pack_bf16;
 using row::row_live;
@@ -108,54 +110,74 @@ __global__ __launch_bounds__(256) void fill_zero_f32_kernel(float* __restrict__ 
 // each lane first folds its 8 columns of each of its 16 rows, then the 16
 // lanes do a reduce-scatter: at every step a lane keeps half of its (max,
 // sum) pairs, sends the other half to its partner and merges what it
-// receives, so after xor 8, 4, 2, 1 lane l holds the pair of one row over the
-// wave's 128 columns (the row of pair index l % 16).  The two waves covering
-// the same rows merge through LDS.
+// receives.  The partners are DPP lane moves inside each 16-lane row: mirror
+// (lane i and 15 - i), half mirror (i and 7 - i within 8), then the quad
+// swaps (xor 2, xor 1); the lane of each pair with bit 3, 2, 1, 0 set keeps
+// the upper half, so after the four steps lane l holds the pair of one row
+// over the wave's 128 columns (the row of pair index l % 16).  The two waves
+// covering the same rows merge through LDS.  The rollout token's logit is
+// not taken here (the combine kernel forms it as a dot product).
 // ---------------------------------------------------------------------------
-template <int HALF>
-__device__ __forceinline__ void scatter_step(float (&m)[16], float (&s)[16], int lane, int b) {
-    const bool up = (lane & b) != 0;
+// (max, sum) merge without a branch: an empty side (-inf, 0) contributes
+// exp2(-inf) = 0, and two empty sides give (-inf, 0).
+__device__ __forceinline__ void ms_merge_sel(float& m, float& s, float m2, float s2) {
+    const float M = fmaxf(m, m2);
+    const float Ms = M == -INFINITY ? 0.0f : M;
+    s = s * __builtin_amdgcn_exp2f(m - Ms) + s2 * __builtin_amdgcn_exp2f(m2 - Ms);
+    m = M;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2, 3, 0, 1]
+constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1, 0, 3, 2]
+
+// One reduce-scatter step over HALF pairs; the partner of lane i (by the DPP
+// move CTRL) differs from it in bit log2(HALF) and agrees in the higher ones.
+template <int HALF, int CTRL>
+__device__ __forceinline__ void scatter_step(float (&m)[16], float (&s)[16], int lane) {
+    const bool up = (lane & HALF) != 0;
 #pragma unroll
     for (int k = 0; k < HALF; ++k) {
         const float sm = up ? m[k] : m[k + HALF];
         const float ss = up ? s[k] : s[k + HALF];
         float km = up ? m[k + HALF] : m[k];
         float ks = up ? s[k + HALF] : s[k];
-        const float rm = __shfl_xor(sm, b, kWave);
-        const float rs = __shfl_xor(ss, b, kWave);
-        ms_merge(km, ks, rm, rs);
+        const float rm = dpp_f32<CTRL>(sm);
+        const float rs = dpp_f32<CTRL>(ss);
+        ms_merge_sel(km, ks, rm, rs);
         m[k] = km;
         s[k] = ks;
     }
 }
 
 struct StatsEpi {
-    const int32_t* token_ids;
     float2* part;  // [N][tiles_v] (max, sum) in base-2 units
-    float* zy;     // [N] logit of the rollout token (unscaled)
     int64_t N;
     int V, tiles_v;
     float c2;  // log2(e) / T
 
     __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
-        int* s_y = reinterpret_cast<int*>(smem);
-        float2* s_ms = reinterpret_cast<float2*>(smem + kTile * sizeof(int));
+        // the k-loop's last barrier has every wave past its LDS reads
+        float2* s_ms = reinterpret_cast<float2*>(smem);
         const int tid = threadIdx.x;
         const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
-        {
-            const int64_t r = row0 + tid;
-            const int y = r < N ? token_ids[r] : -1;
-            s_y[tid] = (y >= 0 && y < V) ? y : -1;
-        }
-        __syncthreads();
         const int lane = t.lane, c = lane & 15;
         const int col0 = t.col0();
+        // Columns past V (only in the last vocabulary tile) count as -inf.
+        // The max is taken on the raw accumulators (c2 > 0 keeps the order,
+        // and rounding is monotonic, so m * c2 is the max of the scaled
+        // values) and each term is one fma: 2^(z c2 - m c2).
         bool colok[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) colok[j] = col0 + j * 16 + c < V;
-#pragma unroll
-        for (int G = 0; G < 2; ++G) {  // row blocks 4G .. 4G+3; pair k = 4 (i - 4G) + r
-            float m[16], s[16];
+        const bool full = col0 + 128 <= V;
+        auto fold = [&](float (&m)[16], float (&s)[16], int G, auto full_c) {
+            constexpr bool kFull = decltype(full_c)::value;
 #pragma unroll
             for (int ii = 0; ii < 4; ++ii)
 #pragma unroll
@@ -165,38 +187,29 @@ struct StatsEpi {
                     float mx = -INFINITY;
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        z[j] = colok[j] ? acc[i][j][r] * c2 : -INFINITY;
+                        z[j] = (kFull || colok[j]) ? acc[i][j][r] : -INFINITY;
                         mx = fmaxf(mx, z[j]);
                     }
+                    const float m2 = mx * c2;  // -inf for an empty row part
+                    const float nm = m2 == -INFINITY ? 0.0f : -m2;
                     float sum = 0.0f;
-                    if (mx != -INFINITY) {
 #pragma unroll
-                        for (int j = 0; j < 8; ++j) sum += __builtin_amdgcn_exp2f(z[j] - mx);
-                    }
-                    m[4 * ii + r] = mx;
+                    for (int j = 0; j < 8; ++j) sum += __builtin_amdgcn_exp2f(fmaf(z[j], c2, nm));
+                    m[4 * ii + r] = m2;
                     s[4 * ii + r] = sum;
                 }
-            // The token's logit: exactly one lane of the grid holds each row's.
+        };
 #pragma unroll
-            for (int ii = 0; ii < 4; ++ii)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int i = 4 * G + ii;
-                    const int rw = t.wm * 128 + i * 16 + acc_row(r, lane);
-                    const int y = s_y[rw];
-                    const int rel = y - col0;
-                    if (y >= 0 && rel >= 0 && rel < 128 && (rel & 15) == c) {
-                        const int jj = rel >> 4;
-                        float v = acc[i][0][r];
-#pragma unroll
-                        for (int q = 1; q < 8; ++q) v = jj == q ? acc[i][q][r] : v;
-                        zy[row0 + rw] = v;
-                    }
-                }
-            scatter_step<8>(m, s, lane, 8);
-            scatter_step<4>(m, s, lane, 4);
-            scatter_step<2>(m, s, lane, 2);
-            scatter_step<1>(m, s, lane, 1);
+        for (int G = 0; G < 2; ++G) {  // row blocks 4G .. 4G+3; pair k = 4 (i - 4G) + r
+            float m[16], s[16];
+            if (full)
+                fold(m, s, G, Flag<true>{});
+            else
+                fold(m, s, G, Flag<false>{});
+            scatter_step<8, kDppRowMirror>(m, s, lane);
+            scatter_step<4, kDppRowHalfMirror>(m, s, lane);
+            scatter_step<2, kDppQuadXor2>(m, s, lane);
+            scatter_step<1, kDppQuadXor1>(m, s, lane);
             {
                 const int rw = t.wm * 128 + (4 * G + (c >> 2)) * 16 + acc_row(c & 3, lane);
                 s_ms[t.wn * kTile + rw] = make_float2(m[0], s[0]);
@@ -217,7 +230,8 @@ struct StatsEpi {
 // Combine: one wave per row.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void lm_combine_kernel(
-    const float2* __restrict__ part, int tiles_v, const float* __restrict__ zy, int64_t N,
+    const float2* __restrict__ part, int tiles_v, const uint16_t* __restrict__ hidden,
+    const uint16_t* __restrict__ weight, int H, int64_t N,
     int64_t n_rows, int V, const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
     const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
     const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
@@ -243,6 +257,27 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
         }
         return;
     }
+    // the rollout token's logit z_y = H[row] . W[y]: fp32 products of the
+    // bf16 operands, lanes over 16-byte chunks (H % 64 == 0), a fixed-order
+    // wave sum
+    float zy = 0.0f;
+    {
+        const u32x4* hr = reinterpret_cast<const u32x4*>(hidden + row * H);
+        const u32x4* wr = reinterpret_cast<const u32x4*>(weight + static_cast<int64_t>(y) * H);
+        for (int c = lane; c < H / 8; c += kWave) {
+            const u32x4 a = hr[c], b = wr[c];
+            zy = fmaf(bf_lo(a.x), bf_lo(b.x), zy);
+            zy = fmaf(bf_hi(a.x), bf_hi(b.x), zy);
+            zy = fmaf(bf_lo(a.y), bf_lo(b.y), zy);
+            zy = fmaf(bf_hi(a.y), bf_hi(b.y), zy);
+            zy = fmaf(bf_lo(a.z), bf_lo(b.z), zy);
+            zy = fmaf(bf_hi(a.z), bf_hi(b.z), zy);
+            zy = fmaf(bf_lo(a.w), bf_lo(b.w), zy);
+            zy = fmaf(bf_hi(a.w), bf_hi(b.w), zy);
+        }
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) zy += __shfl_xor(zy, o, kWave);
+    }
     float m = -INFINITY, s = 0.0f;
     for (int t = lane; t < tiles_v; t += kWave) {
         const float2 q = part[row * tiles_v + t];
@@ -258,7 +293,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
         return;
     }
     const float lse2 = m + __builtin_amdgcn_logf(s);
-    const RowOut o = obj::row_epilogue(lse2, zy[row], old_logp[row], ref_logp[row], adv_tok[row], w, p);
+    const RowOut o = obj::row_epilogue(lse2, zy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
     obj::write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
     g_out[row] = o.g;
     lse2_out[row] = lse2;
@@ -463,7 +498,7 @@ Dims dims_of(int64_t N, int V, int H) {
 }
 
 struct Layout {
-    size_t ht, wt, part, zy, lse2, g, row_loss, dz, total;
+    size_t ht, wt, part, lse2, g, row_loss, dz, total;
 };
 
 Layout layout_of(const Dims& d) {
@@ -477,7 +512,6 @@ Layout layout_of(const Dims& d) {
     L.ht = take(static_cast<size_t>(d.H) * d.N_pad * 2);
     L.wt = take(static_cast<size_t>(d.n_chunks) * d.H * d.Vc * 2);
     L.part = take(static_cast<size_t>(d.N_pad) * d.tiles_v * sizeof(float2));
-    L.zy = take(static_cast<size_t>(d.N_pad) * 4);
     L.lse2 = take(static_cast<size_t>(d.N_pad) * 4);
     L.g = take(static_cast<size_t>(d.N_pad) * 4);
     L.row_loss = take(static_cast<size_t>(d.N_pad) * 4);
@@ -561,7 +595,6 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     uint16_t* ht = reinterpret_cast<uint16_t*>(ws + L.ht);
     uint16_t* wt = reinterpret_cast<uint16_t*>(ws + L.wt);
     float2* part = reinterpret_cast<float2*>(ws + L.part);
-    float* zy = reinterpret_cast<float*>(ws + L.zy);
     float* lse2 = reinterpret_cast<float*>(ws + L.lse2);
     float* g = reinterpret_cast<float*>(ws + L.g);
     float* row_loss = reinterpret_cast<float*>(ws + L.row_loss);
@@ -606,12 +639,12 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
 
     // 2. row statistics and the token logit
     {
-        const StatsEpi epi{token_ids, part, zy, N, V, d.tiles_v, c2};
+        const StatsEpi epi{part, N, V, d.tiles_v, c2};
         if ((st = gemm_nt(Hm, H, h_bytes, Wm, H, w_bytes, H, N, V, epi, stream)) != LEAP_OK) return st;
     }
     // 3. per-token objective
     hipLaunchKernelGGL(lm_combine_kernel, dim3(static_cast<unsigned>(d.N_pad / 4)), dim3(256), 0,
-                       stream, part, d.tiles_v, zy, N, d.N_pad, V, token_ids, old_logp, ref_logp,
+                       stream, part, d.tiles_v, Hm, Wm, H, N, d.N_pad, V, token_ids, old_logp, ref_logp,
                        adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
     if ((st = launch_status()) != LEAP_OK) return st;
     hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
