@@ -263,7 +263,7 @@ def test_lmhead_workspace_size():
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
     # transposes (H*N_pad, and H*chunk per vocabulary chunk, bf16), per-tile
-    # row statistics, four per-row vectors and one bf16 chunk of dZ; chunks
+    # row statistics, three per-row vectors and one bf16 chunk of dZ; chunks
     # are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
     def want(n, v, h):
         n_pad = (n + 255) // 256 * 256
@@ -271,7 +271,7 @@ def test_lmhead_workspace_size():
         vc = 32768 if n_pad * 32768 * 2 < (1 << 32) - 64 else 16384
         vc = min(vc, v_pad)
         chunks = -(-v_pad // vc)
-        return (2 * h * n_pad + 2 * h * vc * chunks + 8 * n_pad * (v_pad // 256) + 4 * 4 * n_pad
+        return (2 * h * n_pad + 2 * h * vc * chunks + 8 * n_pad * (v_pad // 256) + 3 * 4 * n_pad
                 + 2 * n_pad * vc)
 
     for n, v, h in [(16384, 151936, 4096), (65280, 151936, 4096), (65281, 151936, 4096),
