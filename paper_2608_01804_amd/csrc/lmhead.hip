@@ -161,7 +161,7 @@ struct StatsEpi {
     int V, tiles_v;
     float c2;  // log2(e) / T
 
-    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
+    __device__ __forceinline__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
         // the k-loop's last barrier has every wave past its LDS reads
         float2* s_ms = reinterpret_cast<float2*>(smem);
         const int tid = threadIdx.x;
@@ -304,10 +304,13 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 // bf16, stored row-major with 16-byte non-temporal stores (read back only by
 // the next two GEMMs, after it has left the caches anyway).  A lane holds
 // rows 4h .. 4h+3 (h = lane / 16) of column l % 16 of each 16 x 16 block;
-// blocks are taken in column pairs (j, j+1): a 4 x 4 transpose inside each
-// lane quad (two DPP exchanges) gives a lane 4 columns of one row; lanes l
-// and l ^ 4 (neighbouring quads) then swap one block each (DPP row rotates),
-// so a lane holds 8 consecutive columns of one row.
+// blocks are taken in column pairs (j, j+1) and transposed through a
+// per-wave LDS area: each lane writes the 4 rows of its column of both
+// blocks (8 bytes each), then two ds_read_b64_tr_b16 hand lane 4q + p of
+// group h row 4h + p, columns 8q .. 8q+7 of the pair (the read pointer of
+// lane j is column 8 (j % 4) + j / 4, then 4 columns on).  Every element is
+// first -g p; the one lane of the grid that stores a row's token column
+// then adds g to it (in fp32 from the rounded value: within 2^-8 |g|).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -337,13 +340,24 @@ __device__ __forceinline__ void quad_transpose(float (&d)[4], int lane) {
     }
 }
 
-// DPP row rotates inside each 16-lane row: lane i gets lane (i - 4) mod 16
-// (ror 4) or lane (i + 4) mod 16 (ror 12).
-__device__ __forceinline__ uint32_t dpp_row_ror4(uint32_t v) {
-    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x124, 0xF, 0xF, false));
+constexpr int kDzStageBase = 4096;  // after the per-row arrays (3 KiB)
+constexpr int kDzStageBuf = 1024;   // [h][32 columns][4 rows] bf16
+static_assert(kDzStageBase + 4 * 2 * kDzStageBuf <= gemm::kLdsBytes, "dZ staging exceeds the LDS");
+
+__device__ __forceinline__ uint2 read_tr16(const uint8_t* p) {
+    typedef __attribute__((address_space(3))) gemm::s16x4 lds_s16x4;
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p)));
 }
-__device__ __forceinline__ uint32_t dpp_row_ror12(uint32_t v) {
-    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x12C, 0xF, 0xF, false));
+
+// Add g to element e (0..7) of 8 packed bf16, through fp32.
+__device__ __forceinline__ u32x4 add_to_element(u32x4 x, int e, float gv) {
+    const int wi = e >> 1;
+    const bool hi = (e & 1) != 0;
+    uint32_t w = wi == 0 ? x.x : wi == 1 ? x.y : wi == 2 ? x.z : x.w;
+    const uint32_t bits = hi ? (w >> 16) : (w & 0xffffu);
+    const uint32_t nb = pack_bf16(__uint_as_float(bits << 16) + gv, 0.0f) & 0xffffu;
+    w = hi ? ((w & 0xffffu) | (nb << 16)) : ((w & 0xffff0000u) | nb);
+    return u32x4{wi == 0 ? w : x.x, wi == 1 ? w : x.y, wi == 2 ? w : x.z, wi == 3 ? w : x.w};
 }
 
 struct DzEpi {
@@ -356,7 +370,7 @@ struct DzEpi {
     int V, c0;  // vocabulary size, first column of the chunk
     float c2;
 
-    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
+    __device__ __forceinline__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t* smem) const {
         float* s_l = reinterpret_cast<float*>(smem);
         float* s_g = s_l + kTile;
         int* s_y = reinterpret_cast<int*>(s_g + kTile);
@@ -377,9 +391,11 @@ struct DzEpi {
         }
         __syncthreads();
         const int lane = t.lane, c = lane & 15, h = lane >> 4;
-        const int k = c >> 2;              // lane quad within the 16 columns
-        const bool qodd = (k & 1) != 0;
-        const int vw = t.col0();  // chunk-local column of the wave's block
+        const int q = c >> 2, p = c & 3;  // the lane stores row 4h + p, columns 8q .. 8q+7
+        const int vw = t.col0();          // chunk-local column of the wave's block
+        uint8_t* stage = smem + kDzStageBase + (t.wm * 2 + t.wn) * 2 * kDzStageBuf;
+        const int wr = (h * 32 + c) * 8;
+        const int rd = (h * 32 + 8 * p + q) * 8;
         // Every column of the wave's block inside the vocabulary (all but the
         // last tile of the vocabulary): no per-element range select.
         auto tile_body = [&](auto full) {
@@ -387,40 +403,39 @@ struct DzEpi {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int rb = t.wm * 128 + i * 16;  // tile row of the block
+                const int rs = rb + 4 * h + p;       // the row this lane stores
+                const int ys = s_y[rs];
+                const float gs = s_g[rs];
+                // the lane's 4 rows: read once (the staging writes below
+                // would otherwise force re-reads)
+                float lr[4], ngr[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    lr[r] = s_l[rb + acc_row(r, lane)];
+                    ngr[r] = -s_g[rb + acc_row(r, lane)];
+                }
 #pragma unroll
                 for (int jp = 0; jp < 4; ++jp) {
-                    float d[2][4];
+                    uint8_t* buf = stage + (jp & 1) * kDzStageBuf;
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         const int v = vw + (2 * jp + e) * 16 + c;
                         const bool colok = kFull || c0 + v < V;
+                        float d[4];
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            const int rr = rb + acc_row(r, lane);
-                            const float gr = s_g[rr];
-                            const float pz = __builtin_amdgcn_exp2f(acc[i][2 * jp + e][r] * c2 - s_l[rr]);
-                            const float dd = fmaf(-gr, pz, v == s_y[rr] ? gr : 0.0f);  // g (onehot - p)
-                            d[e][r] = colok ? dd : 0.0f;
+                            const float pz = __builtin_amdgcn_exp2f(acc[i][2 * jp + e][r] * c2 - lr[r]);
+                            d[r] = colok ? fmaf(ngr[r], pz, 0.0f) : 0.0f;  // -g p, +0 for g = 0
                         }
+                        *reinterpret_cast<uint2*>(buf + wr + e * 128) =
+                            make_uint2(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]));
                     }
-                    {
-                        uint2 Z[2];
-#pragma unroll
-                        for (int e = 0; e < 2; ++e) {
-                            quad_transpose(d[e], lane);  // row 4h + lane%4, columns 4k .. 4k+3
-                            Z[e] = make_uint2(pack_bf16(d[e][0], d[e][1]), pack_bf16(d[e][2], d[e][3]));
-                        }
-                        // lane quads k and k^1 swap one block: DPP row rotates by
-                        // 12 (from lane + 4) and 4 (from lane - 4) within the row
-                        const uint2 snd = qodd ? Z[0] : Z[1];
-                        const uint2 from_hi = make_uint2(dpp_row_ror12(snd.x), dpp_row_ror12(snd.y));
-                        const uint2 from_lo = make_uint2(dpp_row_ror4(snd.x), dpp_row_ror4(snd.y));
-                        const u32x4 out = qodd ? u32x4{from_lo.x, from_lo.y, Z[1].x, Z[1].y}
-                                               : u32x4{Z[0].x, Z[0].y, from_hi.x, from_hi.y};
-                        const int v = vw + (2 * jp + (qodd ? 1 : 0)) * 16 + 4 * (k & ~1);
-                        const int rr = rb + 4 * h + (lane & 3);
-                        __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dz + (row0 + rr) * ld_dz + v));
-                    }
+                    const uint2 lo = read_tr16(buf + rd), hi = read_tr16(buf + rd + 32);
+                    u32x4 out = u32x4{lo.x, lo.y, hi.x, hi.y};
+                    const int v0 = vw + 32 * jp + 8 * q;
+                    const int off = ys - v0;  // the row's token column (chunk-local, -1: none)
+                    if (static_cast<unsigned>(off) < 8u) out = add_to_element(out, off, gs);
+                    __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dz + (row0 + rs) * ld_dz + v0));
                 }
             }
         };
@@ -444,7 +459,7 @@ struct StoreF32Epi {
     int64_t rows;
     int cols;
 
-    __device__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t*) const {
+    __device__ __forceinline__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t*) const {
         const int lane = t.lane;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
