@@ -29,6 +29,8 @@
 //  * The wave index and the LDS slot bases are wave-uniform scalars
 //    (readfirstlane): the loads' LDS destinations go to M0 from scalar
 //    registers, and no vector address arithmetic sits between the MFMAs.
+//    The k-loop runs two k-tiles per iteration, so the A slot base is a
+//    compile-time part of the fragment reads' immediate offsets.
 //  * Tiles are numbered so the workgroups one XCD runs at once form a compact
 //    GROUP x (32 / GROUP) patch (see tile_of_block).
 //
@@ -38,7 +40,8 @@
 //    ds_read_b64_tr_b16 (4 k each), which transpose 4 x 4 bf16 blocks
 //    across each 16-lane group on the way out of the LDS.  The swizzle term
 //    does depend on the 16-row block there, so each lane keeps 8 precomputed
-//    fragment addresses.
+//    fragment addresses, and the k-loop stays rolled (unrolled, the compiler
+//    moved the accumulators between AGPRs every iteration).
 //
 // v_mfma_f32_16x16x32_bf16 (lane l of 64): A row l%16 with k = 8*(l/16) .. +7;
 // B column l%16 with the same k; accumulator register r holds
