@@ -48,6 +48,19 @@ def k4_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def settle(torch, fn, ms: float = 300.0) -> None:
+    """Run fn back to back for about `ms` milliseconds before a timed region.
+    After idle time or a run of short kernels the device takes tens of
+    milliseconds to bring its clocks back up (the forward-only leg timed
+    right after the shard leg measured 455 us against 384 us once settled),
+    and a short timed region would include that ramp."""
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+
+
 def row_bytes(V: int, valid: bool) -> int:
     """Algorithmic HBM bytes of one row of the fused kernel.
     valid row : read 2V (logits) + 20 (token id, old, ref, adv, w)
@@ -171,6 +184,7 @@ def hbm_probe(L, torch, dev, gib: int = 4, reps: int = 5):
     b = torch.empty_like(a)
     out = {}
     for mode, name, moved in ((0, "copy", 2 * n), (1, "read", n), (2, "write", n)):
+        settle(torch, lambda: L.leap_probe_hbm(a, b, n, mode))
         ts = []
         for _ in range(reps):
             e0 = torch.cuda.Event(enable_timing=True)
@@ -253,8 +267,7 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
     stream = torch.cuda.current_stream()
 
     def timed(fn):
-        fn()
-        torch.cuda.synchronize()
+        settle(torch, fn)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -300,8 +313,7 @@ def logprob_leg(L, torch, s, reps: int = 20):
     def call():
         L.leap_logprob_fwd(lg, V, R, V, tok, None, 1.0, out, s["err"])
 
-    call()
-    torch.cuda.synchronize()
+    settle(torch, call)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -407,8 +419,7 @@ def lmhead_leg(L, torch, dev, seed: int, reps: int):
         L.leap_grpo_lmhead_fwd_bwd(hid, wt, R, V, H, y, old, ref, adv_tok, w_tok, p, logp, None,
                                    loss, dH, dW, 0, ws, ws_bytes, err)
 
-    call()
-    torch.cuda.synchronize()
+    settle(torch, call)
     stream = torch.cuda.current_stream()
     ms = []
     for _ in range(reps):
