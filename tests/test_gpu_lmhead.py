@@ -72,6 +72,29 @@ def test_lmhead_ragged_shapes(N, V, H, inv_temp, kl_type):
     _compare(inp, gpu, kw, what=f"N={N} V={V}")
 
 
+def test_lmhead_edge_tokens():
+    # Rollout tokens on the column edges of the dZ pass: the first column, the
+    # 8- and 128-column edges of a lane's and a wave's store, tile (256) and
+    # chunk (32768) boundaries, and the first and last live column of the
+    # partial last tile (V - 1).  Each of these rows has its token column
+    # written by a different lane position of the transposed store.
+    N, V, H = 64, 70000, 64
+    U.log(f"lmhead edge tokens N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(4001, N, V, H)
+    edges = [0, 7, 8, 127, 128, 255, 256, 32767, 32768, 65535, 65536, 69887, 69888, 69999]
+    y = inp["y"].copy()
+    y[:len(edges)] = edges
+    w = inp["w"].copy()
+    w[:len(edges)] = 1.0 / N
+    z = np.zeros(N)
+    c = oracle.lmhead(inp["h_u16"], inp["w_u16"], y, z, z, z, np.ones(N), want_grads=False)["logp"]
+    n_old, n_ref = np.random.default_rng(4001).normal(0.0, 0.05, (2, N))
+    inp.update(y=y, w=w, old=(c + n_old).astype(np.float32), ref=(c + 2 * n_ref).astype(np.float32))
+    kw = _kw()
+    gpu = U.run_lmhead(inp, **kw)
+    _compare(inp, gpu, kw, what="edge tokens")
+
+
 def test_lmhead_accumulate_and_optional_gradients():
     N, V, H = 300, 1000, 192
     U.log(f"lmhead options N={N} V={V} H={H}")
