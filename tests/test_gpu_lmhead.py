@@ -137,17 +137,14 @@ def test_lmhead_empty_batch():
         assert torch.all(dW == (3.0 if accumulate else 0.0)).item()
 
 
-def test_lmhead_full_shape_sampled_rows():
+def _sampled_rows_and_dw_check(inp, gpu, kw, seed, what):
+    """Oracle on 64 sampled rows (log-prob, loss, dH), then dW over every row
+    against the logits-resident kernel on torch-formed bf16 logits and a
+    torch fp32 GEMM (those logits are rounded to bf16, hence the looser bar)."""
     import torch
-    from paper_2608_01804_amd import leap as L
-    N, V, H = 16384, 151936, 4096
-    U.log(f"lmhead full N={N} V={V} H={H}: inputs")
-    inp = U.lmhead_inputs(1005, N, V, H, cur="torch", bad_rows=(5,))
-    kw = _kw()
-    U.log("  fused call")
-    gpu = U.run_lmhead(inp, to_host=False, **kw)
-    assert gpu["bad"] == 1
-    rng = np.random.default_rng(1005)
+    N, H = inp["hid"].shape
+    V = inp["wt"].shape[0]
+    rng = np.random.default_rng(seed)
     rows = np.unique(np.concatenate([[0, 5, N - 1], rng.choice(N, 61, replace=False)]))
     U.log(f"  oracle on {rows.size} rows")
     o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
@@ -160,12 +157,10 @@ def test_lmhead_full_shape_sampled_rows():
     np.testing.assert_allclose(gpu["tok_loss"][rows][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
     dH = gpu["dH"][torch.from_numpy(rows).to(U.dev())].cpu().numpy()
     Wf = U.bf16_f64(inp["w_u16"])
-    U.check_grad(dH, o["dH"], np.abs(o["dZ"]) @ np.abs(Wf), "full sampled dH")
+    U.check_grad(dH, o["dH"], np.abs(o["dZ"]) @ np.abs(Wf), f"{what} sampled dH")
     del Wf
     assert np.isfinite(gpu["loss"])
 
-    # dW over every row: cross-check against the logits-resident kernel on
-    # bf16 logits formed by torch, and a torch fp32 GEMM.
     U.log("  cross-check of dW via bf16 logits")
     hid, wt = inp["hid"], inp["wt"]
     lg = torch.empty((N, V), dtype=torch.bfloat16, device=U.dev())
@@ -187,3 +182,28 @@ def test_lmhead_full_shape_sampled_rows():
         worst = max(worst, float((diff / bound.clamp(min=1e-30)).max().item()))
         assert torch.all(diff <= 0.03 * bound + 1e-9).item(), v0
     U.log(f"  dW vs bf16-logits path: max diff/bound {worst:.3e}")
+
+
+def test_lmhead_narrow_chunks():
+    # N_pad = 65536: a 32768-column dZ chunk would pass the GEMM core's 4 GiB
+    # operand offsets, so the call takes 16384-column chunks (two at V =
+    # 20000, the second 3840 wide) and the k-major dW pass runs K = 65536.
+    N, V, H = 65281, 20000, 64
+    U.log(f"lmhead narrow chunks N={N} V={V} H={H}: inputs")
+    inp = U.lmhead_inputs(5001, N, V, H, cur="torch", bad_rows=(5,))
+    kw = _kw()
+    U.log("  fused call")
+    gpu = U.run_lmhead(inp, to_host=False, **kw)
+    assert gpu["bad"] == 1
+    _sampled_rows_and_dw_check(inp, gpu, kw, 5001, "narrow")
+
+
+def test_lmhead_full_shape_sampled_rows():
+    N, V, H = 16384, 151936, 4096
+    U.log(f"lmhead full N={N} V={V} H={H}: inputs")
+    inp = U.lmhead_inputs(1005, N, V, H, cur="torch", bad_rows=(5,))
+    kw = _kw()
+    U.log("  fused call")
+    gpu = U.run_lmhead(inp, to_host=False, **kw)
+    assert gpu["bad"] == 1
+    _sampled_rows_and_dw_check(inp, gpu, kw, 1005, "full")
