@@ -7,10 +7,11 @@ total loss within 1e-3 relative; dH and dW entrywise within (2^-8 + 1e-4)
 of the oracle's |dZ| |W| and |dZ|^T |H| (dZ is rounded to bf16 before the
 gradient products, which moves every term by at most 2^-8 of itself, and the
 fp32 softmax adds about 1e-5); excluded rows give exactly zero gradient
-rows.  At the full 16384 x 151936 x 4096 shape the
-oracle scores 64 sampled rows (log-prob, loss, dH); dW there is cross-checked
-against the logits-resident kernel on bf16 logits plus a torch GEMM (a looser
-bar, since those logits are rounded to bf16)."""
+rows.  At the full 16384 x 151936 x 4096 shape, and at N = 65281 (where the
+call takes 16384-column vocabulary chunks), the oracle scores 64 sampled rows
+(log-prob, loss, dH); dW there is cross-checked against the logits-resident
+kernel on bf16 logits plus a torch GEMM (a looser bar, since those logits are
+rounded to bf16)."""
 import numpy as np
 import pytest
 
