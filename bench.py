@@ -236,10 +236,38 @@ def cpu_baseline(s, seconds: float):
     n_valid = int(s["valid"].sum())
     # whole-step time at the measured per-row rate, plus the small steps
     step_time = t_small + t_rows / max(done, 1) * n_valid
+
+    # the same on one thread, over a shorter sample of the same rows
+    oracle.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.dcp_gate(lat.first_turn_pass, s["G"], *s["tau"])
+        rk1 = oracle.rank_tournament(ro.pass_turn, s["G"], s["M"], eps=float(np.float32(1e-6)))
+        oracle.token_advantages(rk1["A"], tok_r, tok_t, ro.n_turns, ro.n_tokens, s["gamma"],
+                                oracle.AGG_SEQ_MEAN_TOKEN_MEAN, float(ro.n_rollouts))
+        t_small1 = time.perf_counter() - t0
+        done1, t_rows1 = 0, 0.0
+        while done1 < done and t_rows1 < seconds / 3:
+            rows = valid_rows[done1:done1 + 8]
+            idx = torch.as_tensor(rows, device=s["logits"].device)
+            lg = s["logits"].index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)
+            tok = s["tok"][idx].cpu().numpy()
+            old = s["old"][idx].cpu().numpy()
+            ref = s["ref"][idx].cpu().numpy()
+            tc = time.perf_counter()
+            oracle.grpo_rows(lg, tok, old, ref, adv[rows], w[rows])
+            t_rows1 += time.perf_counter() - tc
+            done1 += rows.size
+    finally:
+        oracle.set_threads(cores)
+    step_time1 = t_small1 + t_rows1 / max(done1, 1) * n_valid
     return {"value": n_valid / step_time, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s) and "
                       f"the fused objective with dlogits on the first {done} generated-token rows "
-                      f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens"}
+                      f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens",
+            "value_1_thread": n_valid / step_time1,
+            "sample_1_thread": f"the same on one thread: small steps {t_small1:.2f} s, fused "
+                               f"objective on {done1} rows ({t_rows1:.1f} s)"}
 
 
 MFMA_BF16_PEAK = 2.5e15  # MI355X dense bf16 matrix-core peak, flop/s
