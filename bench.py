@@ -200,6 +200,17 @@ def hbm_probe(L, torch, dev, gib: int = 4, reps: int = 5):
     return out
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(s, seconds: float):
     """The fp64 oracle (as it is) on the host cores over a bounded sample of
     the same step: the tournament, gate and token advantages over the whole
@@ -265,6 +276,7 @@ def cpu_baseline(s, seconds: float):
             "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s) and "
                       f"the fused objective with dlogits on the first {done} generated-token rows "
                       f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens",
+            "cpu_model": _cpu_model(), "nproc": os.cpu_count(),
             "value_1_thread": n_valid / step_time1,
             "sample_1_thread": f"the same on one thread: small steps {t_small1:.2f} s, fused "
                                f"objective on {done1} rows ({t_rows1:.1f} s)"}
