@@ -157,7 +157,7 @@ def run_step(L, s, events=None):
             e0.record(stream)
         L.leap_grpo_logprob_loss_fwd_bwd(s["logits"][sl], V, R, V, s["tok"][sl], s["old"][sl],
                                          s["ref"][sl], s["adv_tok"][sl], s["w_tok"][sl],
-                                         s["params"], None, None, s["loss"][i:i + 1],
+                                         s["params"], None, None, None, s["loss"][i:i + 1],
                                          s["dlogits"][sl], s["ws"], s["ws_bytes"], s["err"])
         if events is not None:
             e1.record(stream)

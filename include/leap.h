@@ -205,6 +205,10 @@ size_t leap_grpo_workspace_size(int64_t N, int32_t V);
  *              logits_bf16 (in place), must not otherwise overlap it.
  * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
  * logp_out, tok_loss_out  float [N], nullable (tok_loss is unweighted loss_k).
+ * entropy_out  float [N], nullable: H_k = -sum_v p_v ln p_v of softmax(z)
+ *              in nats (0 for excluded rows) -- a per-token training
+ *              statistic beside Eq. 3, not a term of it; when NULL the
+ *              kernels skip its extra accumulator.
  * loss_out   float [1], required: sum_k w_k * loss_k, summed in a fixed order.
  * workspace  device buffer of >= leap_grpo_workspace_size(N, V) bytes,
  *            8-byte aligned; its contents on entry do not matter and it is
@@ -222,8 +226,8 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
                                            const float *old_logp, const float *ref_logp,
                                            const float *adv_tok, const float *w_tok,
                                            const leap_grpo_params *params, float *logp_out,
-                                           float *tok_loss_out, float *loss_out,
-                                           void *dlogits_bf16, void *workspace,
+                                           float *tok_loss_out, float *entropy_out,
+                                           float *loss_out, void *dlogits_bf16, void *workspace,
                                            size_t ws_bytes, int32_t *dev_err,
                                            hipStream_t stream);
 

@@ -80,6 +80,8 @@ def _load():
     lib.leap_oracle_grpo_rows_bf16.argtypes = row_args
     lib.leap_oracle_logprob_rows_bf16.restype = i64
     lib.leap_oracle_logprob_rows_bf16.argtypes = [P, i64, i64, i32, P, f64, P]
+    lib.leap_oracle_entropy_rows_bf16.restype = i64
+    lib.leap_oracle_entropy_rows_bf16.argtypes = [P, i64, i64, i32, f64, P]
     lib.leap_oracle_rollout_stats.restype = i64
     lib.leap_oracle_rollout_stats.argtypes = [P, P, P, P, i64, i32, i32, i32, P]
     _lib = lib
@@ -199,6 +201,20 @@ def logprob_rows(logits_bf16, token_ids, V=None, inv_temp=1.0):
     tok = _c(token_ids, np.int32)
     out = np.empty(N, np.float64)
     bad = lib.leap_oracle_logprob_rows_bf16(_p(lg), ld, N, V, _p(tok), float(inv_temp), _p(out))
+    return out, int(bad)
+
+
+def entropy_rows(logits_bf16, V=None, inv_temp=1.0):
+    """Shannon entropy (nats) of softmax(inv_temp * logits) per row, from bf16
+    logits [N, ld] (uint16): H = -sum_v p_v log p_v.  All -inf rows give NaN
+    and are counted in the second return value."""
+    lib = _load()
+    lg = np.ascontiguousarray(logits_bf16)
+    assert lg.dtype == np.uint16 and lg.ndim == 2
+    N, ld = lg.shape
+    V = ld if V is None else int(V)
+    out = np.empty(N, np.float64)
+    bad = lib.leap_oracle_entropy_rows_bf16(_p(lg), ld, N, V, float(inv_temp), _p(out))
     return out, int(bad)
 
 

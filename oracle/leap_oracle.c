@@ -462,6 +462,42 @@ int64_t leap_oracle_logprob_rows_bf16(const uint16_t *logits, int64_t ld,
 }
 
 /*
+ * Shannon entropy, in nats, of each row's token distribution
+ * p = softmax(inv_temp * logits): H = -sum_v p_v log p_v, a per-token
+ * quantity training logs beside the objective of Eq. 3 (the paper itself
+ * defines no entropy term).  Columns with p_v = 0 (-inf logits) contribute
+ * 0.  Rows whose logits are all -inf get NaN and are counted.
+ */
+int64_t leap_oracle_entropy_rows_bf16(const uint16_t *logits, int64_t ld,
+                                      int64_t N, int32_t V, double inv_temp,
+                                      double *ent)
+{
+    int64_t bad = 0;
+#pragma omp parallel reduction(+ : bad)
+    {
+        double *zs = (double *)malloc(sizeof(double) * (size_t)(V > 0 ? V : 1));
+        int64_t k;
+        int32_t v;
+#pragma omp for schedule(dynamic, 4)
+        for (k = 0; k < N; ++k) {
+            const uint16_t *row = logits + k * ld;
+            double lse, h = 0.0;
+            for (v = 0; v < V; ++v) zs[v] = inv_temp * bf16_to_double(row[v]);
+            (void)log_softmax_at(zs, V, 0, &lse);
+            if (lse == -INFINITY) { ent[k] = NAN; bad += 1; continue; }
+            for (v = 0; v < V; ++v) {
+                const double logp = zs[v] - lse;
+                const double p = exp(logp);
+                if (p > 0.0) h -= p * logp;
+            }
+            ent[k] = h;
+        }
+        free(zs);
+    }
+    return bad;
+}
+
+/*
  * Training statistics of the method (test infrastructure like the rest).
  *
  * Definitions followed:

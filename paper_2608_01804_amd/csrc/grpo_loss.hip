@@ -28,6 +28,9 @@
 //  * Larger vocabularies use a streaming variant that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
 // kernel sums them in a fixed order (bitwise reproducible).
+// Optional output: each row's entropy H = -sum_v p_v ln p_v (nats), from a
+// third accumulator t = sum 2^d * d beside the sum-exp (the ENT variants;
+// without it the kernels are unchanged).
 #include "objective.h"
 #include "row_common.h"
 
@@ -46,16 +49,17 @@ __device__ __forceinline__ void zero_row(uint16_t* drow, int V, int tid) {
     for (int e = (nfull << 3) + tid; e < V; e += BLOCK) drow[e] = 0;
 }
 
-template <int BLOCK, int CH, int SAFE>
+template <int BLOCK, int CH, int SAFE, bool ENT>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
 grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
                    const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
                    const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
                    const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
-                   float* __restrict__ tok_loss_out, float* __restrict__ row_loss,
-                   uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+                   float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
+                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int lane16 = tid * 16;
     const int64_t row = blockIdx.x;
@@ -70,6 +74,7 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
         if (tid == 0) {
             if (w != 0.0f) count_error(dev_err);  // token id out of range
             write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+            if (ENT) entropy_out[row] = 0.0f;
         }
         zero_row<BLOCK>(drow, V, tid);
         return;
@@ -94,28 +99,46 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
     const float c2 = kLog2e * p.inv_temp;
     const float mc = (m == -INFINITY) ? 0.0f : m * c2;
     float s = 0.0f;
+    float t = 0.0f;  // ENT: sum of 2^d * d
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
         if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
         uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
-            const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
-            s += a;
-            s += b;
-            wv[q] = pack_f16(a, b);
+            if constexpr (ENT) {
+                const float da = vmax(fmaf(bf_lo(wv[q]), c2, -mc), kMinExp2Arg);
+                const float db = vmax(fmaf(bf_hi(wv[q]), c2, -mc), kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(da);
+                const float b = __builtin_amdgcn_exp2f(db);
+                s += a;
+                s += b;
+                t = fmaf(a, da, t);
+                t = fmaf(b, db, t);
+                wv[q] = pack_f16(a, b);
+            } else {
+                const float a = __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
+                const float b = __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+                s += a;
+                s += b;
+                wv[q] = pack_f16(a, b);
+            }
         }
         x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
     }
 
     float M = (m == -INFINITY) ? -INFINITY : mc;
     float S = s;
-    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+    float T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
     if (M == -INFINITY) {  // every logit of the row is -inf
         if (tid == 0) {
             count_error(dev_err);
             write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+            if (ENT) entropy_out[row] = 0.0f;
         }
         zero_row<BLOCK>(drow, V, tid);
         return;
@@ -159,7 +182,10 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
         }
         prev = out;
     }
-    if (tid == 0) write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+    if (tid == 0) {
+        write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+        if (ENT) entropy_out[row] = entropy_of(S, T);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -167,15 +193,17 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
 // read to form dlogits.  Each chunk is read and written by one thread only,
 // so in-place use is safe.
 // ---------------------------------------------------------------------------
-template <int BLOCK>
+template <int BLOCK, bool ENT>
 __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
     const uint16_t* logits, int64_t ld, int V, const int32_t* __restrict__ token_ids,
     const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
     const float* __restrict__ adv_tok, const float* __restrict__ w_tok, Params p,
-    float* __restrict__ logp_out, float* __restrict__ tok_loss_out, float* __restrict__ row_loss,
-    uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    float* __restrict__ logp_out, float* __restrict__ tok_loss_out,
+    float* __restrict__ entropy_out, float* __restrict__ row_loss, uint16_t* dlogits,
+    int32_t* __restrict__ dev_err) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
     const int nchunks = (V + 7) >> 3;
@@ -192,7 +220,10 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
     }
     if (!live) {
         zero_row<BLOCK>(drow, V, tid);
-        if (tid == 0) write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+        if (tid == 0) {
+            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+            if (ENT) entropy_out[row] = 0.0f;
+        }
         return;
     }
     const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
@@ -200,6 +231,7 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
     const u32x4* src = reinterpret_cast<const u32x4*>(xrow);
 
     float m = -INFINITY, s = 0.0f;  // base-2 units
+    float t = 0.0f;                 // ENT: sum of 2^d * d, d = f - m
     for (int c = tid; c < nchunks; c += BLOCK) {
         u32x4 v = src[c];
         if (c == nfull) v = mask_tail(v, V & 7);
@@ -215,18 +247,41 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
         for (int e = 1; e < 8; ++e) cm = vmax(cm, f[e]);
         if (cm == -INFINITY) continue;
         if (cm > m) {
+            if constexpr (ENT) {
+                if (m == -INFINITY) {
+                    t = 0.0f;
+                } else {
+                    const float dm = m - cm;
+                    t = (t + dm * s) * exp2f(dm);
+                }
+            }
             s = (m == -INFINITY) ? 0.0f : s * exp2f(m - cm);
             m = cm;
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += exp2f(f[e] - m);
+        for (int e = 0; e < 8; ++e) {
+            if constexpr (ENT) {
+                const float d = vmax(f[e] - m, kMinExp2Arg);
+                const float a = exp2f(d);
+                s += a;
+                t = fmaf(a, d, t);
+            } else {
+                s += exp2f(f[e] - m);
+            }
+        }
     }
-    float M = m, S = s;
-    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+    float M = m, S = s, T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
     if (M == -INFINITY) {
         if (tid == 0) count_error(dev_err);
         zero_row<BLOCK>(drow, V, tid);
-        if (tid == 0) write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+        if (tid == 0) {
+            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+            if (ENT) entropy_out[row] = 0.0f;
+        }
         return;
     }
     const float lse2 = M + log2f(S);
@@ -254,7 +309,10 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
                 drow[(c << 3) + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
         }
     }
-    if (tid == 0) write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+    if (tid == 0) {
+        write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+        if (ENT) entropy_out[row] = entropy_of(S, T);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -262,15 +320,17 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
 // ---------------------------------------------------------------------------
 using RowKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*,
                            const float*, const float*, const float*, Params, float*, float*,
-                           float*, uint16_t*, int32_t*);
+                           float*, float*, uint16_t*, int32_t*);
 
 struct RowConfig {
-    RowKernel fn;
+    RowKernel fn;      // without the entropy output
+    RowKernel fn_ent;  // with it
     int block;
     int ch;  // 0: streaming variant
 };
 
-#define LEAP_RES(B, C, S) RowConfig{grpo_rows_resident<B, C, S>, B, C}
+#define LEAP_RES(B, C, S) \
+    RowConfig{grpo_rows_resident<B, C, S, false>, grpo_rows_resident<B, C, S, true>, B, C}
 
 // The kernel for V: the resident shape row::pick_resident_shape chooses, or
 // the streaming variant.
@@ -284,7 +344,7 @@ RowConfig pick_row_config(int V) {
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i < 0) return RowConfig{grpo_rows_stream<1024>, 1024, 0};
+    if (i < 0) return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0};
     return table[i];
 }
 
@@ -303,8 +363,9 @@ LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
 LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     const void* logits_bf16, int64_t ld, int64_t N, int32_t V, const int32_t* token_ids,
     const float* old_logp, const float* ref_logp, const float* adv_tok, const float* w_tok,
-    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* loss_out,
-    void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
+    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
+    float* loss_out, void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err,
+    hipStream_t stream) {
     using namespace leap;
     if (N < 0 || V < 1 || ld < V || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     const leap_grpo_params& pp = *params;
@@ -335,9 +396,10 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     float* row_loss = static_cast<float*>(workspace);
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
-        hipLaunchKernelGGL(rc.fn, dim3(static_cast<unsigned>(N)), dim3(rc.block), 0, stream,
-                           static_cast<const uint16_t*>(logits_bf16), ld, V, token_ids, old_logp,
-                           ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss,
+        hipLaunchKernelGGL(entropy_out ? rc.fn_ent : rc.fn, dim3(static_cast<unsigned>(N)),
+                           dim3(rc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
+                           V, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
+                           tok_loss_out, entropy_out, row_loss,
                            static_cast<uint16_t*>(dlogits_bf16), dev_err);
         const leap_status st = launch_status();
         if (st != LEAP_OK) return st;

@@ -100,6 +100,64 @@ __device__ __forceinline__ void block_ms_reduce(float& m, float& s, float* s_m, 
     wave_ms_reduce(m, s);
 }
 
+// Exponents below this give 2^d == 0 in fp32; clamping -inf to it keeps the
+// entropy sum's products 2^d * d finite (0) without changing any 2^d.
+constexpr float kMinExp2Arg = -256.0f;
+
+// (m, s, t) triples in base-2 units for the entropy: s = sum 2^d and
+// t = sum 2^d * d over the elements' exponents d relative to m.  Moving the
+// reference from m to M >= m scales both by 2^(m - M) and adds (m - M) * s
+// to t.  A side with m == -inf holds no element and adds nothing.  Symmetric
+// like ms_merge.
+__device__ __forceinline__ void mst_merge(float& m, float& s, float& t, float m2, float s2,
+                                          float t2) {
+    const float M = fmaxf(m, m2);
+    if (M == -INFINITY) return;
+    const float e1 = __builtin_amdgcn_exp2f(m - M);
+    const float e2 = __builtin_amdgcn_exp2f(m2 - M);
+    const float t1 = (m == -INFINITY) ? 0.0f : (t + (m - M) * s) * e1;
+    const float u2 = (m2 == -INFINITY) ? 0.0f : (t2 + (m2 - M) * s2) * e2;
+    t = t1 + u2;
+    s = s * e1 + s2 * e2;
+    m = M;
+}
+
+__device__ __forceinline__ void wave_mst_reduce(float& m, float& s, float& t) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float m2 = __shfl_xor(m, o, kWave);
+        const float s2 = __shfl_xor(s, o, kWave);
+        const float t2 = __shfl_xor(t, o, kWave);
+        mst_merge(m, s, t, m2, s2, t2);
+    }
+}
+
+// Block-wide (m, s, t) merge, in the fixed order of block_ms_reduce.
+template <int BLOCK>
+__device__ __forceinline__ void block_mst_reduce(float& m, float& s, float& t, float* s_m,
+                                                 float* s_s, float* s_t, int tid) {
+    constexpr int NW = BLOCK / kWave;
+    wave_mst_reduce(m, s, t);
+    if (NW == 1) return;
+    const int lane = tid & (kWave - 1);
+    if (lane == 0) {
+        s_m[tid / kWave] = m;
+        s_s[tid / kWave] = s;
+        s_t[tid / kWave] = t;
+    }
+    __syncthreads();
+    m = (lane < NW) ? s_m[lane] : -INFINITY;
+    s = (lane < NW) ? s_s[lane] : 0.0f;
+    t = (lane < NW) ? s_t[lane] : 0.0f;
+    wave_mst_reduce(m, s, t);
+}
+
+// Entropy in nats of a row from its merged (M, S, T): with p = 2^d / S,
+// H = -sum p ln p = ln 2 * (log2 S - T / S).
+__device__ __forceinline__ float entropy_of(float S, float T) {
+    return kLn2 * (__builtin_amdgcn_logf(S) - T / S);
+}
+
 // Elementwise max of two packed fp16 pairs (maxNum: a quiet NaN operand is
 // ignored).  Applied to raw bf16 words it orders them like their bf16 values
 // for finite magnitudes below 2^121; the bf16 -inf pattern reads as a NaN.

@@ -99,7 +99,7 @@ def bf16_device(lg_u16):
 
 
 def run_grpo(lg_dev, V, tok, old, ref, adv, w, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0,
-             inv_temp=1.0, inplace=False, want_tok_loss=True):
+             inv_temp=1.0, inplace=False, want_tok_loss=True, want_entropy=False):
     """lg_dev: bf16 device tensor [N, ld].  Returns numpy logp, tok_loss, loss,
     dlogits (bf16 bits as uint16 [N, ld], device copy kept as 'dl_dev'), bad."""
     import torch
@@ -108,6 +108,8 @@ def run_grpo(lg_dev, V, tok, old, ref, adv, w, eps_lo=0.2, eps_hi=0.2, kl_coef=0
     dl = lg_dev if inplace else torch.full_like(lg_dev, float("nan"))
     lp = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
     tl = torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+    ent = (torch.full((max(1, N),), float("nan"), dtype=torch.float32, device=dev())
+           if want_entropy else None)
     loss = torch.full((1,), float("nan"), dtype=torch.float32, device=dev())
     ws_bytes = L.leap_grpo_workspace_size(N, V)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev())
@@ -116,10 +118,11 @@ def run_grpo(lg_dev, V, tok, old, ref, adv, w, eps_lo=0.2, eps_hi=0.2, kl_coef=0
     L.leap_grpo_logprob_loss_fwd_bwd(lg_dev, ld, N, V, T(np.asarray(tok, np.int32)),
                                      T(np.asarray(old, np.float32)), T(np.asarray(ref, np.float32)),
                                      T(np.asarray(adv, np.float32)), T(np.asarray(w, np.float32)),
-                                     p, lp, tl if want_tok_loss else None, loss, dl, ws, ws_bytes,
-                                     err)
+                                     p, lp, tl if want_tok_loss else None, ent, loss, dl, ws,
+                                     ws_bytes, err)
     torch.cuda.synchronize()
     return {"logp": lp.cpu().numpy()[:N], "tok_loss": tl.cpu().numpy()[:N],
+            "entropy": ent.cpu().numpy()[:N] if ent is not None else None,
             "loss": float(loss.item()), "dl_dev": dl, "bad": int(err.item())}
 
 

@@ -128,7 +128,8 @@ def test_token_advantages_rejects(kw):
 def _grpo(**kw):
     p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
     a = dict(logits=FAKE, ld=1024, N=8, V=1000, token_ids=FAKE, old_logp=FAKE, ref_logp=FAKE,
-             adv_tok=FAKE, w_tok=FAKE, params=p, logp_out=None, tok_loss_out=None, loss_out=FAKE,
+             adv_tok=FAKE, w_tok=FAKE, params=p, logp_out=None, tok_loss_out=None, entropy_out=None,
+             loss_out=FAKE,
              dlogits=FAKE + (1 << 30), workspace=FAKE, ws_bytes=1 << 20, dev_err=None, stream=0)
     a.update(kw)
     return L.leap_grpo_logprob_loss_fwd_bwd(**a)

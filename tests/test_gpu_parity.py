@@ -351,3 +351,38 @@ def test_grpo_full_size_microbatch(name, mb_index):
     U.check_dlogits(U.dl_rows(gpu1["dl_dev"], sample, V), lg, sample, tok, old, ref, adv, w1, V,
                     atol=2e-2, kw=KW)
     assert gpu1["bad"] == 0
+
+
+# ----------------------------------------------------------------------------
+# Optional per-token entropy output of the fused call
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("V,N,inv_temp", [(1000, 64, 1.0), (5000, 32, 0.7), (32768, 64, 1.0),
+                                          (151936, 24, 1.0), (151936, 8, 1.3), (200003, 8, 1.0)])
+def test_grpo_entropy_output(V, N, inv_temp):
+    import torch
+    rng = np.random.default_rng(V + N)
+
+    def edit(lg, tok):
+        lg[1, ::7] = 0xFF80  # -inf columns
+        tok[1] = 3
+        tok[2] = V  # out of range: counted, excluded
+
+    ld = (V + 7) // 8 * 8
+    lg, tok, old, ref = U.make_inputs_host(V + 3, N, V, ld=ld, edit=edit)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = rng.choice([0.0, 1.0], N, p=[0.25, 0.75]).astype(np.float32)
+    w[:3] = 1.0
+    kw = dict(KW, inv_temp=inv_temp)
+    U.log(f"grpo entropy V={V} N={N} T^-1={inv_temp}")
+    lg_dev = U.bf16_device(lg)
+    a = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, want_entropy=True, **kw)
+    b = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, **kw)
+    # requesting the entropy changes no other output
+    assert torch.equal(a["dl_dev"].view(torch.int16), b["dl_dev"].view(torch.int16))
+    assert np.array_equal(a["logp"], b["logp"]) and a["loss"] == b["loss"]
+    assert a["bad"] == b["bad"] == 1
+    h, bad = oracle.entropy_rows(lg, V=V, inv_temp=inv_temp)
+    assert bad == 0
+    valid = (w != 0) & (tok >= 0) & (tok < V)
+    assert np.all(a["entropy"][~valid] == 0)
+    np.testing.assert_allclose(a["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)

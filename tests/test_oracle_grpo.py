@@ -198,3 +198,63 @@ def test_minus_inf_columns_get_zero_probability():
     np.testing.assert_allclose(out["logp"][0], _logp_torch(np.where(finite, x, -1e300), y)[0],
                                atol=1e-12)
     assert np.all(out["dlogits"][0][~finite] == 0)
+
+
+# ----------------------------------------------------------------------------
+# Per-token entropy of softmax(inv_temp * logits), the optional output of the
+# fused call: H = -sum_v p_v log p_v in nats.
+# ----------------------------------------------------------------------------
+NEG_INF = 0xFF80
+
+
+def test_entropy_closed_forms():
+    # uniform logits: ln V; a point mass: 0; two finite columns: the binary
+    # entropy of p = 1 / (1 + e^b)
+    V = 4096
+    lg = np.full((4, V), NEG_INF, np.uint16)
+    lg[0, :] = wl.f32_to_bf16_bits(np.float32(1.5))
+    lg[1, 17] = wl.f32_to_bf16_bits(np.float32(-3.0))
+    b = 1.25  # exact in bf16
+    lg[2, 3] = wl.f32_to_bf16_bits(np.float32(0.0))
+    lg[2, 4000] = wl.f32_to_bf16_bits(np.float32(b))
+    lg[3, :] = wl.f32_to_bf16_bits(np.float32(0.0))
+    lg[3, 0] = NEG_INF  # V - 1 equal columns
+    h, bad = oracle.entropy_rows(lg)
+    assert bad == 0
+    p = 1.0 / (1.0 + np.exp(b))
+    want = [np.log(V), 0.0, -p * np.log(p) - (1 - p) * np.log1p(-p), np.log(V - 1)]
+    np.testing.assert_allclose(h, want, rtol=1e-12, atol=1e-15)
+
+
+def test_entropy_matches_scipy_and_temperature():
+    rng = np.random.default_rng(11)
+    N, V = 6, 1000
+    lg = wl.f32_to_bf16_bits(rng.normal(0, 2.0, (N, V)).astype(np.float32))
+    x = wl.bf16_bits_to_f32(lg).astype(np.float64)
+    for inv_temp in (1.0, 0.5, 1.7):
+        h, bad = oracle.entropy_rows(lg, inv_temp=inv_temp)
+        assert bad == 0
+        z = inv_temp * x
+        p = np.exp(z - z.max(axis=1, keepdims=True))
+        p /= p.sum(axis=1, keepdims=True)
+        np.testing.assert_allclose(h, stats.entropy(p, axis=1), rtol=1e-12)
+        assert np.all(h >= 0) and np.all(h <= np.log(V))
+
+
+def test_entropy_shift_invariant_and_uses_first_v_columns():
+    rng = np.random.default_rng(12)
+    N, V, ld = 4, 300, 304
+    ints = rng.integers(-20, 20, (N, ld)).astype(np.float32)  # exact in bf16, also + 7
+    a = wl.f32_to_bf16_bits(ints)
+    b = wl.f32_to_bf16_bits(ints + 7.0)
+    b[:, V:] = wl.f32_to_bf16_bits(np.float32(100.0))  # padding past V is ignored
+    ha, _ = oracle.entropy_rows(a, V=V)
+    hb, _ = oracle.entropy_rows(b, V=V)
+    np.testing.assert_allclose(ha, hb, rtol=1e-13)
+
+
+def test_entropy_all_minus_inf_row_is_counted():
+    lg = np.full((2, 64), NEG_INF, np.uint16)
+    lg[1, :] = 0
+    h, bad = oracle.entropy_rows(lg)
+    assert bad == 1 and np.isnan(h[0]) and abs(h[1] - np.log(64)) < 1e-13
