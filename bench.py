@@ -341,32 +341,70 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
             "stats_frac": stats_bytes / t_stats / HBM_PEAK, "bwd_frac": bwd_bytes / t_bwd / HBM_PEAK}
 
 
+def entropy_leg(L, torch, s, reps: int = 20):
+    """The fused call on the first microbatch without and with the optional
+    per-token entropy output (HIP events on the launch stream, per-call
+    average of `reps` back-to-back calls each): the entropy's cost."""
+    V, R = s["V"], s["R"]
+    ent = torch.empty(R, dtype=torch.float32, device=s["logits"].device)
+    stream = torch.cuda.current_stream()
+
+    def timed(entropy_out):
+        def call():
+            L.leap_grpo_logprob_loss_fwd_bwd(s["logits"][:R], V, R, V, s["tok"][:R], s["old"][:R],
+                                             s["ref"][:R], s["adv_tok"][:R], s["w_tok"][:R],
+                                             s["params"], None, None, entropy_out, s["loss"][:1],
+                                             s["dlogits"][:R], s["ws"], s["ws_bytes"], s["err"])
+
+        settle(torch, call)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps / 1e3
+
+    t, t_ent = timed(None), timed(ent)
+    log(f"[bench] fused call, first microbatch: {t * 1e6:.1f} us; with entropy {t_ent * 1e6:.1f} us")
+    return {"workload": f"fused call on the first microbatch ({R} x {V})", "call_us": t * 1e6,
+            "call_us_with_entropy": t_ent * 1e6}
+
+
 def logprob_leg(L, torch, s, reps: int = 20):
     """The forward-only log-probability (old-policy / reference passes) on the
     first microbatch of the resident logits, every row read: HIP events on the
-    launch stream around `reps` back-to-back calls, per-call average."""
+    launch stream around `reps` back-to-back calls, per-call average; then the
+    same with the optional per-row entropy output."""
     V, R = s["V"], s["R"]
     lg, tok = s["logits"][:R], s["tok"][:R]
     out = torch.empty(R, dtype=torch.float32, device=lg.device)
+    ent = torch.empty(R, dtype=torch.float32, device=lg.device)
     stream = torch.cuda.current_stream()
 
-    def call():
-        L.leap_logprob_fwd(lg, V, R, V, tok, None, 1.0, out, s["err"])
+    def timed(entropy_out):
+        def call():
+            L.leap_logprob_fwd(lg, V, R, V, tok, None, 1.0, out, entropy_out, s["err"])
 
-    settle(torch, call)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(reps):
-        call()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t = e0.elapsed_time(e1) / reps / 1e3
+        settle(torch, call)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps / 1e3
+
+    t = timed(None)
+    t_ent = timed(ent)
     nbytes = R * (2 * V + 8)
-    log(f"[bench] forward-only log-prob {R} x {V}: {t * 1e6:.1f} us ({nbytes / t / 1e9:.0f} GB/s)")
+    log(f"[bench] forward-only log-prob {R} x {V}: {t * 1e6:.1f} us ({nbytes / t / 1e9:.0f} GB/s); "
+        f"with entropy {t_ent * 1e6:.1f} us")
     return {"workload": f"forward-only log-prob: first microbatch ({R} rows, all read) x {V}",
             "call_us": t * 1e6, "GBps": nbytes / t / 1e9, "frac": nbytes / t / HBM_PEAK,
-            "bytes_per_call": nbytes}
+            "bytes_per_call": nbytes, "call_us_with_entropy": t_ent * 1e6}
 
 
 def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
@@ -611,6 +649,7 @@ def main():
 
     shard = shard_leg(L, torch, s) if not args.no_shard else None
     fwd = logprob_leg(L, torch, s)
+    ent = entropy_leg(L, torch, s)
     rstats = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
@@ -646,6 +685,7 @@ def main():
         "lmhead": lm,
         "vocab_shard": shard,
         "logprob_fwd": fwd,
+        "entropy": ent,
         "rollout_stats": rstats,
     }
     print(json.dumps(out), flush=True)

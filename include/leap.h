@@ -239,17 +239,19 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
  *   logp_out[k] = z[y_k] - log sum_v exp(z[v]),  z = inv_temperature * logits[k]
  *
  * logits_bf16 [N][ld] bf16, token_ids int32 [N], logp_out float [N].
- * w_tok float [N], nullable: a row with w_tok[k] == 0 is not read and gets 0.
- * A token id outside [0, V) or a row of all -inf logits counts in *dev_err
- * and gets NaN.  Alignment and range rules as leap_grpo_logprob_loss_fwd_bwd;
+ * entropy_out float [N], nullable: H_k = -sum_v p_v ln p_v of softmax(z) in
+ *             nats, as in leap_grpo_logprob_loss_fwd_bwd.
+ * w_tok float [N], nullable: a row with w_tok[k] == 0 is not read and gets 0
+ * (log-prob and entropy).  A token id outside [0, V) or a row of all -inf
+ * logits counts in *dev_err and gets NaN (log-prob and entropy).  Alignment and range rules as leap_grpo_logprob_loss_fwd_bwd;
  * no workspace.
  * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a non-positive or
  * non-finite inv_temperature, a required pointer NULL; LEAP_ERR_MISALIGNED.
  */
 leap_status leap_logprob_fwd(const void *logits_bf16, int64_t ld, int64_t N, int32_t V,
                              const int32_t *token_ids, const float *w_tok,
-                             float inv_temperature, float *logp_out, int32_t *dev_err,
-                             hipStream_t stream);
+                             float inv_temperature, float *logp_out, float *entropy_out,
+                             int32_t *dev_err, hipStream_t stream);
 
 /* Workspace bytes leap_grpo_lmhead_fwd_bwd needs (0 for invalid sizes). */
 size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);

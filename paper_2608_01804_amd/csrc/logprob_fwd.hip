@@ -6,7 +6,8 @@
 // VGPRs for V up to 196608 (one HBM read, lane maximum with v_pk_max_f16 on the
 // raw bf16 words, one v_exp_f32 per element, one (max, sum) merge), a
 // streaming online-softmax variant beyond that.  Only 2V bytes are read and 4
-// written per row.
+// written per row (8 with the optional per-row entropy, which adds a third
+// accumulator t = sum 2^d * d beside the sum-exp: the ENT variants).
 #include "row_common.h"
 
 namespace leap {
@@ -18,17 +19,22 @@ __device__ __forceinline__ bool fwd_skip(const float* w_tok, int64_t row) {
     return w_tok != nullptr && w_tok[row] == 0.0f;
 }
 
-template <int BLOCK, int CH, int SAFE>
+template <int BLOCK, int CH, int SAFE, bool ENT>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
 logprob_rows_resident(const uint16_t* __restrict__ logits, int64_t ld, int V,
                       const int32_t* __restrict__ token_ids, const float* __restrict__ w_tok,
-                      float inv_temp, float* __restrict__ logp_out, int32_t* __restrict__ dev_err) {
+                      float inv_temp, float* __restrict__ logp_out,
+                      float* __restrict__ entropy_out, int32_t* __restrict__ dev_err) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
     if (fwd_skip(w_tok, row)) {
-        if (tid == 0) logp_out[row] = 0.0f;
+        if (tid == 0) {
+            logp_out[row] = 0.0f;
+            if (ENT) entropy_out[row] = 0.0f;
+        }
         return;
     }
     const int y = token_ids[row];
@@ -36,6 +42,7 @@ logprob_rows_resident(const uint16_t* __restrict__ logits, int64_t ld, int V,
         if (tid == 0) {
             count_error(dev_err);
             logp_out[row] = __builtin_nanf("");
+            if (ENT) entropy_out[row] = __builtin_nanf("");
         }
         return;
     }
@@ -49,39 +56,61 @@ logprob_rows_resident(const uint16_t* __restrict__ logits, int64_t ld, int V,
     const float c2 = kLog2e * inv_temp;
     const float mc = (m == -INFINITY) ? 0.0f : m * c2;
     float s = 0.0f;
+    float t = 0.0f;  // ENT: sum of 2^d * d
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
         const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            s += __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
-            s += __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+            if constexpr (ENT) {
+                const float da = vmax(fmaf(bf_lo(wv[q]), c2, -mc), kMinExp2Arg);
+                const float db = vmax(fmaf(bf_hi(wv[q]), c2, -mc), kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(da);
+                const float b = __builtin_amdgcn_exp2f(db);
+                s += a;
+                s += b;
+                t = fmaf(a, da, t);
+                t = fmaf(b, db, t);
+            } else {
+                s += __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
+                s += __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+            }
         }
     }
     float M = (m == -INFINITY) ? -INFINITY : mc;
     float S = s;
-    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+    float T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
     if (tid == 0) {
         if (M == -INFINITY) {
             count_error(dev_err);
             logp_out[row] = __builtin_nanf("");
+            if (ENT) entropy_out[row] = __builtin_nanf("");
         } else {
             logp_out[row] = inv_temp * xy - (M + __builtin_amdgcn_logf(S)) * kLn2;
+            if (ENT) entropy_out[row] = entropy_of(S, T);
         }
     }
 }
 
-template <int BLOCK>
+template <int BLOCK, bool ENT>
 __global__ __launch_bounds__(BLOCK) void logprob_rows_stream(
     const uint16_t* __restrict__ logits, int64_t ld, int V, const int32_t* __restrict__ token_ids,
     const float* __restrict__ w_tok, float inv_temp, float* __restrict__ logp_out,
-    int32_t* __restrict__ dev_err) {
+    float* __restrict__ entropy_out, int32_t* __restrict__ dev_err) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
     if (fwd_skip(w_tok, row)) {
-        if (tid == 0) logp_out[row] = 0.0f;
+        if (tid == 0) {
+            logp_out[row] = 0.0f;
+            if (ENT) entropy_out[row] = 0.0f;
+        }
         return;
     }
     const int y = token_ids[row];
@@ -89,6 +118,7 @@ __global__ __launch_bounds__(BLOCK) void logprob_rows_stream(
         if (tid == 0) {
             count_error(dev_err);
             logp_out[row] = __builtin_nanf("");
+            if (ENT) entropy_out[row] = __builtin_nanf("");
         }
         return;
     }
@@ -98,6 +128,7 @@ __global__ __launch_bounds__(BLOCK) void logprob_rows_stream(
     const float c2 = kLog2e * inv_temp;
     const u32x4* src = reinterpret_cast<const u32x4*>(xrow);
     float m = -INFINITY, s = 0.0f;  // base-2 units
+    float t = 0.0f;                 // ENT: sum of 2^d * d, d = f - m
     for (int c = tid; c < nchunks; c += BLOCK) {
         u32x4 v = src[c];
         if (c == nfull) v = mask_tail(v, V & 7);
@@ -113,33 +144,57 @@ __global__ __launch_bounds__(BLOCK) void logprob_rows_stream(
         for (int e = 1; e < 8; ++e) cm = vmax(cm, f[e]);
         if (cm == -INFINITY) continue;
         if (cm > m) {
+            if constexpr (ENT) {
+                if (m == -INFINITY) {
+                    t = 0.0f;
+                } else {
+                    const float dm = m - cm;
+                    t = (t + dm * s) * __builtin_amdgcn_exp2f(dm);
+                }
+            }
             s = (m == -INFINITY) ? 0.0f : s * __builtin_amdgcn_exp2f(m - cm);
             m = cm;
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += __builtin_amdgcn_exp2f(f[e] - m);
+        for (int e = 0; e < 8; ++e) {
+            if constexpr (ENT) {
+                const float d = vmax(f[e] - m, kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(d);
+                s += a;
+                t = fmaf(a, d, t);
+            } else {
+                s += __builtin_amdgcn_exp2f(f[e] - m);
+            }
+        }
     }
-    block_ms_reduce<BLOCK>(m, s, s_m, s_s, tid);
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(m, s, t, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(m, s, s_m, s_s, tid);
     if (tid == 0) {
         if (m == -INFINITY) {
             count_error(dev_err);
             logp_out[row] = __builtin_nanf("");
+            if (ENT) entropy_out[row] = __builtin_nanf("");
         } else {
             const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
             logp_out[row] = inv_temp * xy - (m + __builtin_amdgcn_logf(s)) * kLn2;
+            if (ENT) entropy_out[row] = entropy_of(s, t);
         }
     }
 }
 
 using FwdKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*, float,
-                           float*, int32_t*);
+                           float*, float*, int32_t*);
 
 struct FwdConfig {
-    FwdKernel fn;
+    FwdKernel fn;      // without the entropy output
+    FwdKernel fn_ent;  // with it
     int block;
 };
 
-#define LEAP_FWD(B, C, S) FwdConfig{logprob_rows_resident<B, C, S>, B}
+#define LEAP_FWD(B, C, S) \
+    FwdConfig{logprob_rows_resident<B, C, S, false>, logprob_rows_resident<B, C, S, true>, B}
 
 FwdConfig pick_fwd_config(int V) {
     static const FwdConfig table[] = {
@@ -151,7 +206,7 @@ FwdConfig pick_fwd_config(int V) {
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i < 0) return FwdConfig{logprob_rows_stream<1024>, 1024};
+    if (i < 0) return FwdConfig{logprob_rows_stream<1024, false>, logprob_rows_stream<1024, true>, 1024};
     return table[i];
 }
 
@@ -162,8 +217,8 @@ FwdConfig pick_fwd_config(int V) {
 
 LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64_t N, int32_t V,
                                       const int32_t* token_ids, const float* w_tok,
-                                      float inv_temperature, float* logp_out, int32_t* dev_err,
-                                      hipStream_t stream) {
+                                      float inv_temperature, float* logp_out,
+                                      float* entropy_out, int32_t* dev_err, hipStream_t stream) {
     using namespace leap;
     if (N < 0 || V < 1 || ld < V) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -173,8 +228,8 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
     if (!aligned16(logits_bf16) || (ld & 7) != 0) return LEAP_ERR_MISALIGNED;
     if (N > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
     const FwdConfig fc = pick_fwd_config(V);
-    hipLaunchKernelGGL(fc.fn, dim3(static_cast<unsigned>(N)), dim3(fc.block), 0, stream,
-                       static_cast<const uint16_t*>(logits_bf16), ld, V, token_ids, w_tok,
-                       inv_temperature, logp_out, dev_err);
+    hipLaunchKernelGGL(entropy_out ? fc.fn_ent : fc.fn, dim3(static_cast<unsigned>(N)),
+                       dim3(fc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld, V,
+                       token_ids, w_tok, inv_temperature, logp_out, entropy_out, dev_err);
     return launch_status();
 }

@@ -97,7 +97,7 @@ def lib() -> ctypes.CDLL:
                                                  ctypes.POINTER(leap_grpo_params), P, P, P, P,
                                                  P, P, ctypes.c_size_t, P, P]
     L.leap_logprob_fwd.restype = ctypes.c_int
-    L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P]
+    L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P, P]
     L.leap_lmhead_workspace_size.restype = ctypes.c_size_t
     L.leap_lmhead_workspace_size.argtypes = [i64, i32, i32]
     L.leap_grpo_lmhead_fwd_bwd.restype = ctypes.c_int
@@ -239,13 +239,14 @@ def leap_grpo_logprob_loss_fwd_bwd(logits, ld, N, V, token_ids, old_logp, ref_lo
     _check(st, "leap_grpo_logprob_loss_fwd_bwd")
 
 
-def leap_logprob_fwd(logits, ld, N, V, token_ids, w_tok, inv_temperature, logp_out, dev_err=None,
-                     stream=None) -> None:
+def leap_logprob_fwd(logits, ld, N, V, token_ids, w_tok, inv_temperature, logp_out,
+                     entropy_out=None, dev_err=None, stream=None) -> None:
     st = lib().leap_logprob_fwd(
         _ptr(logits, "bfloat16", "logits"), int(ld), int(N), int(V),
         _ptr(token_ids, "int32", "token_ids"), _ptr(w_tok, "float32", "w_tok"),
         float(inv_temperature), _ptr(logp_out, "float32", "logp_out"),
-        _ptr(dev_err, "int32", "dev_err"), _stream(stream))
+        _ptr(entropy_out, "float32", "entropy_out"), _ptr(dev_err, "int32", "dev_err"),
+        _stream(stream))
     _check(st, "leap_logprob_fwd")
 
 

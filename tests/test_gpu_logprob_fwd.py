@@ -1,5 +1,6 @@
 """GPU parity of the forward-only log-probability entry point against the
-oracle's log-softmax (log-probs within 2e-3 absolute)."""
+oracle's log-softmax (log-probs within 2e-3 absolute) and, when requested,
+the oracle's per-row entropy (1e-4 relative + 2e-4 absolute)."""
 import numpy as np
 import pytest
 
@@ -13,15 +14,20 @@ SHAPES = [(16, 16, 64), (1000, 1008, 64), (4093, 4096, 32), (32768, 32768, 64),
           (65536, 65536, 16), (151936, 151936, 64), (196608, 196608, 8), (200003, 200008, 8)]
 
 
-def _run(lg_dev, V, tok, w=None, inv_temp=1.0):
+def _run(lg_dev, V, tok, w=None, inv_temp=1.0, want_entropy=False):
     import torch
     from paper_2608_01804_amd import leap as L
     N, ld = lg_dev.shape
     out = torch.full((max(N, 1),), float("inf"), dtype=torch.float32, device=U.dev())
+    ent = (torch.full((max(N, 1),), float("inf"), dtype=torch.float32, device=U.dev())
+           if want_entropy else None)
     err = U.zeros_i32(1)
     L.leap_logprob_fwd(lg_dev, ld, N, V, U.T(np.asarray(tok, np.int32)),
-                       None if w is None else U.T(np.asarray(w, np.float32)), inv_temp, out, err)
+                       None if w is None else U.T(np.asarray(w, np.float32)), inv_temp, out, ent,
+                       err)
     torch.cuda.synchronize()
+    if want_entropy:
+        return out.cpu().numpy()[:N], int(err.item()), ent.cpu().numpy()[:N]
     return out.cpu().numpy()[:N], int(err.item())
 
 
@@ -67,3 +73,26 @@ def test_logprob_fwd_matches_fused_kernel_logp():
     fused = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, np.zeros(N, np.float32), w)
     fwd, _ = _run(U.bf16_device(lg), V, tok)
     assert np.max(np.abs(fwd - fused["logp"])) < 1e-5
+
+
+@pytest.mark.parametrize("V,ld,N", [(1000, 1008, 64), (32768, 32768, 32), (151936, 151936, 32),
+                                    (200003, 200008, 8)])
+def test_logprob_fwd_entropy(V, ld, N):
+    lg = wl.logits_host(V + 5, N, V, ld=ld)
+    tok = wl.sample_tokens_host(lg, V, V + 5)
+    lg[1, ::5] = 0xFF80  # -inf columns
+    tok[1] = 2
+    tok[2] = V  # out of range: NaN, counted
+    w = np.ones(N, np.float32)
+    w[3] = 0.0  # not read: 0
+    lg_dev = U.bf16_device(lg)
+    got, err, ent = _run(lg_dev, V, tok, w=w, inv_temp=0.8, want_entropy=True)
+    plain, err2 = _run(lg_dev, V, tok, w=w, inv_temp=0.8)
+    assert err == err2 == 1
+    assert np.array_equal(got, plain, equal_nan=True)  # the entropy changes no log-prob
+    h, bad = oracle.entropy_rows(lg, V=V, inv_temp=0.8)
+    assert bad == 0
+    assert np.isnan(ent[2]) and ent[3] == 0.0
+    ok = np.ones(N, bool)
+    ok[[2, 3]] = False
+    np.testing.assert_allclose(ent[ok], h[ok], rtol=1e-4, atol=2e-4)
