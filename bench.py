@@ -677,7 +677,7 @@ def main():
                    "vocab": V, "microbatch_rows": R, "G": meta["G"], "max_turns": meta["M"]},
         "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": traffic,
-                     "kernel": "grpo_rows_resident<1024,19> + loss_reduce (one fused call)",
+                     "kernel": "grpo_rows_resident<1024,19,16,false> + loss_reduce (one fused call)",
                      "avg_launch_us": k4_avg_s * 1e6, "bytes_per_launch": bytes_per_launch,
                      "probe_GBps": probe,
                      "frac_of_probe_copy": achieved / 1e9 / probe["copy_GBps"]},
