@@ -276,14 +276,16 @@ def test_grpo_inplace_and_deterministic():
     adv = rng.normal(0, 1, N).astype(np.float32)
     w = rng.choice([0.0, 1.0], N, p=[0.2, 0.8]).astype(np.float32)
     U.log("grpo in-place / determinism")
-    a = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
+    a = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, want_entropy=True, **KW)
     b = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
-    c = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, inplace=True, **KW)
+    c = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, inplace=True, want_entropy=True,
+                   **KW)
     import torch
     assert torch.equal(a["dl_dev"].view(torch.int16), b["dl_dev"].view(torch.int16))
     assert torch.equal(a["dl_dev"].view(torch.int16), c["dl_dev"].view(torch.int16))
     assert a["loss"] == b["loss"] == c["loss"]
     assert np.array_equal(a["logp"], c["logp"])
+    assert np.array_equal(a["entropy"], c["entropy"])  # in place: the row is read before written
 
 
 def test_grpo_all_masked_and_empty():
