@@ -341,6 +341,73 @@ def shard_leg(L, torch, s, n_shards: int = 8, reps: int = 20):
             "stats_frac": stats_bytes / t_stats / HBM_PEAK, "bwd_frac": bwd_bytes / t_bwd / HBM_PEAK}
 
 
+def _us_per_call(torch, fn, reps: int) -> float:
+    """Average µs per call of `reps` back-to-back calls of fn (HIP events on
+    the launch stream), after a short settling run."""
+    stream = torch.cuda.current_stream()
+    settle(torch, fn, ms=100)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps * 1e3
+
+
+def small_leg(L, torch, s, reps: int = 200):
+    """Latency of the gate, the tournament and the token advantages (µs per
+    call): on the measured step, and the gate and tournament on the
+    tournament-stress workload (4096 groups x G=64, M=3), both outcome
+    orders."""
+    import workloads as wl
+    G, M = s["G"], s["M"]
+    n = s["ro"].n_rollouts
+    mid = {
+        "groups": n // G, "G": G, "rows": s["rows"],
+        "gate_us": _us_per_call(torch, lambda: L.leap_dcp_gate(
+            s["ftp"], n // G, G, s["tau"][0], s["tau"][1], s["n_fail"], s["gate"]), reps),
+        "rank_us": _us_per_call(torch, lambda: L.leap_rank_advantages(
+            s["pass_turn"], None, None, n // G, G, M, L.LEAP_KEY_TURN, L.LEAP_ADV_STD, 1e-6, None,
+            None, None, s["reward"], s["adv_roll"], s["err"]), reps),
+        "token_adv_us": _us_per_call(torch, lambda: L.leap_token_advantages(
+            s["adv_roll"], s["tok_r"], s["tok_t"], s["n_turns"], s["n_gen"], n, s["rows"],
+            s["gamma"], L.LEAP_AGG_SEQ_MEAN_TOKEN_MEAN, float(n), s["adv_tok"], s["w_tok"],
+            s["err"]), reps),
+    }
+    dev = s["pass_turn"].device
+    lat = wl.draw_latent("stress")
+    Gs, Ms, ng = lat.G, lat.M, lat.n_groups
+    tmin, tmax = L.leap_dcp_tau_from_pass_rate(Gs, 0, 1, 1, 3, 4, 1)
+    ftp = torch.from_numpy(lat.first_turn_pass).to(dev)
+    gate = torch.empty(ng, dtype=torch.uint8, device=dev)
+    nf = torch.empty(ng, dtype=torch.int32, device=dev)
+    L.leap_dcp_gate(ftp, ng, Gs, tmin, tmax, nf, gate)
+    ro = wl.realize(lat, gate.cpu().numpy())
+    pt = torch.from_numpy(ro.pass_turn).to(dev)
+    sq = torch.from_numpy(ro.speedup_q).to(dev)
+    nt = torch.from_numpy(wl.stress_token_counts(lat)).to(dev)
+    nr = ng * Gs
+    rew = torch.empty(nr, dtype=torch.float32, device=dev)
+    adv = torch.empty(nr, dtype=torch.float32, device=dev)
+    stress = {
+        "groups": ng, "G": Gs, "rollouts": nr,
+        "gate_us": _us_per_call(torch, lambda: L.leap_dcp_gate(ftp, ng, Gs, tmin, tmax, nf, gate),
+                                reps),
+        "rank_turn_us": _us_per_call(torch, lambda: L.leap_rank_advantages(
+            pt, None, None, ng, Gs, Ms, L.LEAP_KEY_TURN, L.LEAP_ADV_STD, 1e-6, None, None, None,
+            rew, adv, s["err"]), reps),
+        "rank_lex_us": _us_per_call(torch, lambda: L.leap_rank_advantages(
+            pt, sq, nt, ng, Gs, Ms, L.LEAP_KEY_LEX, L.LEAP_ADV_STD, 1e-6, None, None, None, rew,
+            adv, s["err"]), reps),
+    }
+    log(f"[bench] step: gate {mid['gate_us']:.1f} us, tournament {mid['rank_us']:.1f} us, token "
+        f"advantages {mid['token_adv_us']:.1f} us; stress {ng}x{Gs}: gate {stress['gate_us']:.1f} "
+        f"us, tournament {stress['rank_turn_us']:.1f} us (turn), {stress['rank_lex_us']:.1f} us (lex)")
+    return {"step": mid, "stress": stress}
+
+
 def entropy_leg(L, torch, s, reps: int = 20):
     """The fused call on the first microbatch without and with the optional
     per-token entropy output (HIP events on the launch stream, per-call
@@ -650,6 +717,7 @@ def main():
     shard = shard_leg(L, torch, s) if not args.no_shard else None
     fwd = logprob_leg(L, torch, s)
     ent = entropy_leg(L, torch, s)
+    small = small_leg(L, torch, s)
     rstats = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
@@ -686,6 +754,7 @@ def main():
         "vocab_shard": shard,
         "logprob_fwd": fwd,
         "entropy": ent,
+        "small_kernels": small,
         "rollout_stats": rstats,
     }
     print(json.dumps(out), flush=True)
