@@ -356,6 +356,30 @@ def _us_per_call(torch, fn, reps: int) -> float:
     return e0.elapsed_time(e1) / reps * 1e3
 
 
+def graph_leg(L, torch, s, steps: int):
+    """The whole step captured once in a HIP graph and replayed `steps`
+    times (host clock around the replays, synchronised on both sides):
+    what launching the step's calls one by one costs against a replay."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_step(L, s)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run_step(L, s)
+    settle(torch, g.replay)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    t = (time.perf_counter() - t0) / steps
+    log(f"[bench] step replayed from a HIP graph: {t * 1e3:.3f} ms")
+    return {"ms_per_step": t * 1e3, "steps": steps}
+
+
 def small_leg(L, torch, s, reps: int = 200):
     """Latency of the gate, the tournament and the token advantages (µs per
     call): on the measured step, and the gate and tournament on the
@@ -718,6 +742,7 @@ def main():
     fwd = logprob_leg(L, torch, s)
     ent = entropy_leg(L, torch, s)
     small = small_leg(L, torch, s)
+    graph = graph_leg(L, torch, s, args.steps)
     rstats = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
     lm = None
@@ -755,6 +780,7 @@ def main():
         "logprob_fwd": fwd,
         "entropy": ent,
         "small_kernels": small,
+        "graph_replay": graph,
         "rollout_stats": rstats,
     }
     print(json.dumps(out), flush=True)
