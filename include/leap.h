@@ -41,7 +41,7 @@ typedef enum leap_status {
     LEAP_ERR_INVALID_ARG = 1, /* null required pointer, size or enum out of range */
     LEAP_ERR_MISALIGNED = 2,  /* a pointer or leading dimension breaks the alignment rule */
     LEAP_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size() value */
-    LEAP_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
+    LEAP_ERR_UNSUPPORTED = 4, /* valid request the library does not implement */
     LEAP_ERR_HIP = 5          /* the HIP runtime reported an error at launch */
 } leap_status;
 
