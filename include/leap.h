@@ -321,13 +321,16 @@ leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight
  *   falls in the shard, else owned = 0, zy = 0.  A row with w_tok[k] == 0
  *   (w_tok nullable) or whose shard columns are all -inf gives m2 = -inf,
  *   s = 0 and is not read in the first case.
+ *   partial_t [N] float, nullable: the entropy partial
+ *   t = sum_v 2^(c x_v - m2) * (c x_v - m2) over the shard's columns (0 when
+ *   m2 = -inf); needed by leap_vocab_merge_objective's entropy output.
  *   logits_bf16 [N][ld] bf16 holding the shard's V_shard columns; alignment
  *   and range rules as leap_grpo_logprob_loss_fwd_bwd; vocab_start >= 0.
  */
 leap_status leap_vocab_shard_stats(const void *logits_bf16, int64_t ld, int64_t N, int32_t V_shard,
                                    int32_t vocab_start, const int32_t *token_ids,
                                    const float *w_tok, float inv_temperature, float *partial,
-                                   hipStream_t stream);
+                                   float *partial_t, hipStream_t stream);
 
 /* Workspace bytes leap_vocab_merge_objective needs for N rows. */
 size_t leap_vocab_merge_workspace_size(int64_t N);
@@ -343,18 +346,23 @@ size_t leap_vocab_merge_workspace_size(int64_t N);
  *   row_state (0, +inf); a token id outside [0, V_total) with w != 0, a row
  *   whose token no shard (or more than one shard) reports, or a row of all
  *   -inf logits also counts in *dev_err.
+ *   entropy_out [N] float, nullable: the row's entropy as in
+ *   leap_grpo_logprob_loss_fwd_bwd (0 for an excluded row), merged from
+ *   partials_t [n_shards][N] float (every shard's partial_t, shard-major),
+ *   which it then requires.
  * Errors: LEAP_ERR_INVALID_ARG (N < 0, n_shards < 1, V_total < 1, a
- * parameter out of range, a required pointer NULL), LEAP_ERR_MISALIGNED,
+ * parameter out of range, a required pointer NULL, entropy_out without
+ * partials_t), LEAP_ERR_MISALIGNED,
  * LEAP_ERR_WORKSPACE, LEAP_ERR_UNSUPPORTED (unknown kl_type).
  */
-leap_status leap_vocab_merge_objective(const float *partials, int32_t n_shards, int64_t N,
-                                       int32_t V_total, const int32_t *token_ids,
-                                       const float *old_logp, const float *ref_logp,
-                                       const float *adv_tok, const float *w_tok,
-                                       const leap_grpo_params *params, float *logp_out,
-                                       float *tok_loss_out, float *loss_out, float *row_state,
-                                       void *workspace, size_t ws_bytes, int32_t *dev_err,
-                                       hipStream_t stream);
+leap_status leap_vocab_merge_objective(const float *partials, const float *partials_t,
+                                       int32_t n_shards, int64_t N, int32_t V_total,
+                                       const int32_t *token_ids, const float *old_logp,
+                                       const float *ref_logp, const float *adv_tok,
+                                       const float *w_tok, const leap_grpo_params *params,
+                                       float *logp_out, float *tok_loss_out, float *entropy_out,
+                                       float *loss_out, float *row_state, void *workspace,
+                                       size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
 
 /*
  * leap_vocab_shard_bwd: dlogits[k][v] = g_k * ([vocab_start + v == y_k] -

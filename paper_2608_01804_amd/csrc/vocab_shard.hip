@@ -34,19 +34,25 @@ __device__ __forceinline__ void write_partial(float4* out, int64_t row, float m2
     out[row] = make_float4(m2, s, zy, owned);
 }
 
-template <int BLOCK, int CH, int SAFE>
+// ENT variants also write t = sum 2^(x c - m2) * (x c - m2) to partial_t
+// (0 for an excluded row or an all -inf shard): the entropy's partial.
+template <int BLOCK, int CH, int SAFE, bool ENT>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
 shard_stats_resident(const uint16_t* __restrict__ logits, int64_t ld, int V, int vocab_start,
                      const int32_t* __restrict__ token_ids, const float* __restrict__ w_tok,
-                     float inv_temp, float4* __restrict__ partial) {
+                     float inv_temp, float4* __restrict__ partial, float* __restrict__ partial_t) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
     const int yl = token_ids[row] - vocab_start;
     const bool owned = yl >= 0 && yl < V;
     if (w_tok != nullptr && w_tok[row] == 0.0f) {
-        if (tid == 0) write_partial(partial, row, -INFINITY, 0.0f, 0.0f, owned ? 1.0f : 0.0f);
+        if (tid == 0) {
+            write_partial(partial, row, -INFINITY, 0.0f, 0.0f, owned ? 1.0f : 0.0f);
+            if (ENT) partial_t[row] = 0.0f;
+        }
         return;
     }
     const uint16_t* xrow = logits + row * ld;
@@ -57,38 +63,59 @@ shard_stats_resident(const uint16_t* __restrict__ logits, int64_t ld, int V, int
     const float c2 = kLog2e * inv_temp;
     const float mc = (m == -INFINITY) ? 0.0f : m * c2;
     float s = 0.0f;
+    float t = 0.0f;  // ENT: sum of 2^d * d
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
         const uint32_t wv[4] = {x[j].x, x[j].y, x[j].z, x[j].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            s += __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
-            s += __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+            if constexpr (ENT) {
+                const float da = vmax(fmaf(bf_lo(wv[q]), c2, -mc), kMinExp2Arg);
+                const float db = vmax(fmaf(bf_hi(wv[q]), c2, -mc), kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(da);
+                const float b = __builtin_amdgcn_exp2f(db);
+                s += a;
+                s += b;
+                t = fmaf(a, da, t);
+                t = fmaf(b, db, t);
+            } else {
+                s += __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -mc));
+                s += __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -mc));
+            }
         }
     }
     float M = (m == -INFINITY) ? -INFINITY : mc;
     float S = s;
-    block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+    float T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
     if (tid == 0) {
         const float zy = owned ? __uint_as_float(static_cast<uint32_t>(xrow[yl]) << 16) : 0.0f;
         write_partial(partial, row, M, M == -INFINITY ? 0.0f : S, zy, owned ? 1.0f : 0.0f);
+        if (ENT) partial_t[row] = M == -INFINITY ? 0.0f : T;
     }
 }
 
 // Any shard width: online (max, sum) over the row's chunks.
-template <int BLOCK>
+template <int BLOCK, bool ENT>
 __global__ __launch_bounds__(BLOCK) void shard_stats_stream(
     const uint16_t* __restrict__ logits, int64_t ld, int V, int vocab_start,
     const int32_t* __restrict__ token_ids, const float* __restrict__ w_tok, float inv_temp,
-    float4* __restrict__ partial) {
+    float4* __restrict__ partial, float* __restrict__ partial_t) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
+    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
     const int yl = token_ids[row] - vocab_start;
     const bool owned = yl >= 0 && yl < V;
     if (w_tok != nullptr && w_tok[row] == 0.0f) {
-        if (tid == 0) write_partial(partial, row, -INFINITY, 0.0f, 0.0f, owned ? 1.0f : 0.0f);
+        if (tid == 0) {
+            write_partial(partial, row, -INFINITY, 0.0f, 0.0f, owned ? 1.0f : 0.0f);
+            if (ENT) partial_t[row] = 0.0f;
+        }
         return;
     }
     const uint16_t* xrow = logits + row * ld;
@@ -97,6 +124,7 @@ __global__ __launch_bounds__(BLOCK) void shard_stats_stream(
     const float c2 = kLog2e * inv_temp;
     const u32x4* src = reinterpret_cast<const u32x4*>(xrow);
     float m = -INFINITY, s = 0.0f;
+    float t = 0.0f;  // ENT: sum of 2^d * d, d = f - m
     for (int c = tid; c < nchunks; c += BLOCK) {
         u32x4 v = src[c];
         if (c == nfull) v = mask_tail(v, V & 7);
@@ -112,28 +140,51 @@ __global__ __launch_bounds__(BLOCK) void shard_stats_stream(
         for (int e = 1; e < 8; ++e) cm = vmax(cm, f[e]);
         if (cm == -INFINITY) continue;
         if (cm > m) {
+            if constexpr (ENT) {
+                if (m == -INFINITY) {
+                    t = 0.0f;
+                } else {
+                    const float dm = m - cm;
+                    t = (t + dm * s) * __builtin_amdgcn_exp2f(dm);
+                }
+            }
             s = (m == -INFINITY) ? 0.0f : s * __builtin_amdgcn_exp2f(m - cm);
             m = cm;
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += __builtin_amdgcn_exp2f(f[e] - m);
+        for (int e = 0; e < 8; ++e) {
+            if constexpr (ENT) {
+                const float d = vmax(f[e] - m, kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(d);
+                s += a;
+                t = fmaf(a, d, t);
+            } else {
+                s += __builtin_amdgcn_exp2f(f[e] - m);
+            }
+        }
     }
-    block_ms_reduce<BLOCK>(m, s, s_m, s_s, tid);
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(m, s, t, s_m, s_s, s_t, tid);
+    else
+        block_ms_reduce<BLOCK>(m, s, s_m, s_s, tid);
     if (tid == 0) {
         const float zy = owned ? __uint_as_float(static_cast<uint32_t>(xrow[yl]) << 16) : 0.0f;
         write_partial(partial, row, m, m == -INFINITY ? 0.0f : s, zy, owned ? 1.0f : 0.0f);
+        if (ENT) partial_t[row] = m == -INFINITY ? 0.0f : t;
     }
 }
 
 using StatsKernel = void (*)(const uint16_t*, int64_t, int, int, const int32_t*, const float*,
-                             float, float4*);
+                             float, float4*, float*);
 
 struct StatsConfig {
-    StatsKernel fn;
+    StatsKernel fn;      // without the entropy partial
+    StatsKernel fn_ent;  // with it
     int block;
 };
 
-#define LEAP_SHARD(B, C, S) StatsConfig{shard_stats_resident<B, C, S>, B}
+#define LEAP_SHARD(B, C, S) \
+    StatsConfig{shard_stats_resident<B, C, S, false>, shard_stats_resident<B, C, S, true>, B}
 
 StatsConfig pick_stats_config(int V) {
     static const StatsConfig table[] = {
@@ -145,7 +196,7 @@ StatsConfig pick_stats_config(int V) {
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i < 0) return StatsConfig{shard_stats_stream<1024>, 1024};
+    if (i < 0) return StatsConfig{shard_stats_stream<1024, false>, shard_stats_stream<1024, true>, 1024};
     return table[i];
 }
 
@@ -154,12 +205,16 @@ StatsConfig pick_stats_config(int V) {
 // ---------------------------------------------------------------------------
 // Merge: one wave per row, lanes over shards in index order.
 // ---------------------------------------------------------------------------
+// ENT: the shards' entropy partials merge with their (max, sum) pairs as
+// (max, sum, t) triples, and the row's entropy goes to entropy_out.
+template <bool ENT>
 __global__ __launch_bounds__(256) void merge_objective_kernel(
-    const float4* __restrict__ partials, int n_shards, int64_t N, int V_total,
-    const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
-    const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
-    const float* __restrict__ w_tok, obj::Params p, float* __restrict__ logp_out,
-    float* __restrict__ tok_loss_out, float* __restrict__ row_loss, float2* __restrict__ row_state,
+    const float4* __restrict__ partials, const float* __restrict__ partials_t, int n_shards,
+    int64_t N, int V_total, const int32_t* __restrict__ token_ids,
+    const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
+    const float* __restrict__ adv_tok, const float* __restrict__ w_tok, obj::Params p,
+    float* __restrict__ logp_out, float* __restrict__ tok_loss_out,
+    float* __restrict__ entropy_out, float* __restrict__ row_loss, float2* __restrict__ row_state,
     int32_t* __restrict__ dev_err) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t row = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave;
@@ -171,23 +226,30 @@ __global__ __launch_bounds__(256) void merge_objective_kernel(
             if (count) count_error(dev_err);
             obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
             row_state[row] = make_float2(0.0f, INFINITY);
+            if (ENT) entropy_out[row] = 0.0f;
         }
     };
     if (!row_live(w, y, V_total)) {
         exclude(w != 0.0f);  // token id out of range
         return;
     }
-    float m = -INFINITY, s = 0.0f, zy = 0.0f;
+    float m = -INFINITY, s = 0.0f, t = 0.0f, zy = 0.0f;
     int owners = 0;
     for (int k = lane; k < n_shards; k += kWave) {
         const float4 q = partials[static_cast<int64_t>(k) * N + row];
-        ms_merge(m, s, q.x, q.y);
+        if constexpr (ENT)
+            mst_merge(m, s, t, q.x, q.y, partials_t[static_cast<int64_t>(k) * N + row]);
+        else
+            ms_merge(m, s, q.x, q.y);
         if (q.w != 0.0f) {
             ++owners;
             zy += q.z;
         }
     }
-    wave_ms_reduce(m, s);
+    if constexpr (ENT)
+        wave_mst_reduce(m, s, t);
+    else
+        wave_ms_reduce(m, s);
     owners = wave_sum_i32(owners);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) zy += __shfl_xor(zy, o, kWave);
@@ -200,6 +262,7 @@ __global__ __launch_bounds__(256) void merge_objective_kernel(
     const RowOut o = obj::row_epilogue(lse2, zy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
     obj::write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
     row_state[row] = make_float2(o.g, lse2);
+    if (ENT) entropy_out[row] = entropy_of(s, t);
 }
 
 // ---------------------------------------------------------------------------
@@ -286,7 +349,7 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
                                             int32_t V_shard, int32_t vocab_start,
                                             const int32_t* token_ids, const float* w_tok,
                                             float inv_temperature, float* partial,
-                                            hipStream_t stream) {
+                                            float* partial_t, hipStream_t stream) {
     using namespace leap;
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -296,9 +359,10 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
     if (!aligned16(logits_bf16) || (ld & 7) != 0 || !aligned16(partial)) return LEAP_ERR_MISALIGNED;
     if (N > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
     const StatsConfig sc = pick_stats_config(V_shard);
-    hipLaunchKernelGGL(sc.fn, dim3(static_cast<unsigned>(N)), dim3(sc.block), 0, stream,
-                       static_cast<const uint16_t*>(logits_bf16), ld, V_shard, vocab_start,
-                       token_ids, w_tok, inv_temperature, reinterpret_cast<float4*>(partial));
+    hipLaunchKernelGGL(partial_t ? sc.fn_ent : sc.fn, dim3(static_cast<unsigned>(N)),
+                       dim3(sc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
+                       V_shard, vocab_start, token_ids, w_tok, inv_temperature,
+                       reinterpret_cast<float4*>(partial), partial_t);
     return launch_status();
 }
 
@@ -308,10 +372,11 @@ LEAP_API size_t leap_vocab_merge_workspace_size(int64_t N) {
 }
 
 LEAP_API leap_status leap_vocab_merge_objective(
-    const float* partials, int32_t n_shards, int64_t N, int32_t V_total, const int32_t* token_ids,
-    const float* old_logp, const float* ref_logp, const float* adv_tok, const float* w_tok,
-    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* loss_out,
-    float* row_state, void* workspace, size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
+    const float* partials, const float* partials_t, int32_t n_shards, int64_t N, int32_t V_total,
+    const int32_t* token_ids, const float* old_logp, const float* ref_logp, const float* adv_tok,
+    const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
+    float* entropy_out, float* loss_out, float* row_state, void* workspace, size_t ws_bytes,
+    int32_t* dev_err, hipStream_t stream) {
     using namespace leap;
     if (N < 0 || n_shards < 1 || V_total < 1 || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     if (!params_ok(*params)) return LEAP_ERR_INVALID_ARG;
@@ -321,6 +386,7 @@ LEAP_API leap_status leap_vocab_merge_objective(
     if (N > 0) {
         if (!partials || !token_ids || !old_logp || !ref_logp || !adv_tok || !w_tok || !row_state)
             return LEAP_ERR_INVALID_ARG;
+        if (entropy_out && !partials_t) return LEAP_ERR_INVALID_ARG;
         if (!aligned16(partials) || (reinterpret_cast<uintptr_t>(row_state) & 7u) != 0)
             return LEAP_ERR_MISALIGNED;
         if (N > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
@@ -330,11 +396,12 @@ LEAP_API leap_status leap_vocab_merge_objective(
     const obj::Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     float* row_loss = static_cast<float*>(workspace);
     if (N > 0) {
-        hipLaunchKernelGGL(merge_objective_kernel, dim3(static_cast<unsigned>((N + 3) / 4)),
-                           dim3(256), 0, stream, reinterpret_cast<const float4*>(partials),
-                           n_shards, N, V_total, token_ids, old_logp, ref_logp, adv_tok, w_tok, p,
-                           logp_out, tok_loss_out, row_loss, reinterpret_cast<float2*>(row_state),
-                           dev_err);
+        hipLaunchKernelGGL(entropy_out ? merge_objective_kernel<true> : merge_objective_kernel<false>,
+                           dim3(static_cast<unsigned>((N + 3) / 4)), dim3(256), 0, stream,
+                           reinterpret_cast<const float4*>(partials), partials_t, n_shards, N,
+                           V_total, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
+                           tok_loss_out, entropy_out, row_loss,
+                           reinterpret_cast<float2*>(row_state), dev_err);
         const leap_status st = launch_status();
         if (st != LEAP_OK) return st;
     }

@@ -105,12 +105,12 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(leap_grpo_params), P, P, P, P, P, i32,
                                            P, ctypes.c_size_t, P, P]
     L.leap_vocab_shard_stats.restype = ctypes.c_int
-    L.leap_vocab_shard_stats.argtypes = [P, i64, i64, i32, i32, P, P, f32, P, P]
+    L.leap_vocab_shard_stats.argtypes = [P, i64, i64, i32, i32, P, P, f32, P, P, P]
     L.leap_vocab_merge_workspace_size.restype = ctypes.c_size_t
     L.leap_vocab_merge_workspace_size.argtypes = [i64]
     L.leap_vocab_merge_objective.restype = ctypes.c_int
-    L.leap_vocab_merge_objective.argtypes = [P, i32, i64, i32, P, P, P, P, P,
-                                             ctypes.POINTER(leap_grpo_params), P, P, P, P, P,
+    L.leap_vocab_merge_objective.argtypes = [P, P, i32, i64, i32, P, P, P, P, P,
+                                             ctypes.POINTER(leap_grpo_params), P, P, P, P, P, P,
                                              ctypes.c_size_t, P, P]
     L.leap_vocab_shard_bwd.restype = ctypes.c_int
     L.leap_vocab_shard_bwd.argtypes = [P, i64, i64, i32, i32, P, P, f32, P, P]
@@ -272,11 +272,12 @@ def leap_grpo_lmhead_fwd_bwd(hidden, weight, N, V, H, token_ids, old_logp, ref_l
 
 
 def leap_vocab_shard_stats(logits, ld, N, V_shard, vocab_start, token_ids, w_tok, inv_temperature,
-                           partial, stream=None) -> None:
+                           partial, stream=None, partial_t=None) -> None:
     st = lib().leap_vocab_shard_stats(
         _ptr(logits, "bfloat16", "logits"), int(ld), int(N), int(V_shard), int(vocab_start),
         _ptr(token_ids, "int32", "token_ids"), _ptr(w_tok, "float32", "w_tok"),
-        float(inv_temperature), _ptr(partial, "float32", "partial"), _stream(stream))
+        float(inv_temperature), _ptr(partial, "float32", "partial"),
+        _ptr(partial_t, "float32", "partial_t"), _stream(stream))
     _check(st, "leap_vocab_shard_stats")
 
 
@@ -287,14 +288,16 @@ def leap_vocab_merge_workspace_size(N) -> int:
 def leap_vocab_merge_objective(partials, n_shards, N, V_total, token_ids, old_logp, ref_logp,
                                adv_tok, w_tok, params: leap_grpo_params, logp_out, tok_loss_out,
                                loss_out, row_state, workspace, ws_bytes, dev_err=None,
-                               stream=None) -> None:
+                               stream=None, partials_t=None, entropy_out=None) -> None:
     st = lib().leap_vocab_merge_objective(
-        _ptr(partials, "float32", "partials"), int(n_shards), int(N), int(V_total),
+        _ptr(partials, "float32", "partials"), _ptr(partials_t, "float32", "partials_t"),
+        int(n_shards), int(N), int(V_total),
         _ptr(token_ids, "int32", "token_ids"), _ptr(old_logp, "float32", "old_logp"),
         _ptr(ref_logp, "float32", "ref_logp"), _ptr(adv_tok, "float32", "adv_tok"),
         _ptr(w_tok, "float32", "w_tok"), ctypes.byref(params) if params is not None else None,
         _ptr(logp_out, "float32", "logp_out"), _ptr(tok_loss_out, "float32", "tok_loss_out"),
-        _ptr(loss_out, "float32", "loss_out"), _ptr(row_state, "float32", "row_state"),
+        _ptr(entropy_out, "float32", "entropy_out"), _ptr(loss_out, "float32", "loss_out"),
+        _ptr(row_state, "float32", "row_state"),
         _ptr(workspace, None, "workspace"), int(ws_bytes), _ptr(dev_err, "int32", "dev_err"),
         _stream(stream))
     _check(st, "leap_vocab_merge_objective")

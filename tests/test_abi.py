@@ -304,6 +304,10 @@ def test_vocab_shard_entry_points_reject():
         L.leap_vocab_merge_objective(FAKE, 2, 8, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, p, None, None,
                                      FAKE, FAKE, FAKE, 16, stream=0)
     assert e.value.status == L.LEAP_ERR_WORKSPACE
+    with pytest.raises(L.LeapError) as e:  # the entropy needs the shards' entropy partials
+        L.leap_vocab_merge_objective(FAKE, 2, 8, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, p, None, None,
+                                     FAKE, FAKE, FAKE, 1 << 20, stream=0, entropy_out=FAKE)
+    assert e.value.status == L.LEAP_ERR_INVALID_ARG
     with pytest.raises(L.LeapError) as e:
         L.leap_vocab_shard_bwd(FAKE, 1000, 8, 1000, 0, FAKE, FAKE, 1.0, FAKE + 2048, stream=0)
     assert e.value.status == L.LEAP_ERR_INVALID_ARG  # partial overlap with the logits

@@ -23,7 +23,7 @@ def _shards(V, widths):
     return list(zip(starts.tolist(), list(widths)))
 
 
-def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False):
+def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False, want_entropy=False):
     """lg: host bf16 bit patterns [N, ld]; returns partials (n_shards, N, 4),
     merged outputs and the concatenated dlogits [N, V] (uint16)."""
     import torch
@@ -31,6 +31,8 @@ def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False):
     N = lg.shape[0]
     dev = U.dev()
     parts = torch.full((len(shards), max(N, 1), 4), float("nan"), dtype=torch.float32, device=dev)
+    parts_t = (torch.full((len(shards), max(N, 1)), float("nan"), dtype=torch.float32, device=dev)
+               if want_entropy else None)
     shard_dev = []
     tok_d, w_d = U.T(np.asarray(tok, np.int32)), U.T(np.asarray(w, np.float32))
     for k, (a, width) in enumerate(shards):
@@ -39,7 +41,8 @@ def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False):
         buf[:, :width] = lg[:, a:a + width]
         t = torch.from_numpy(buf.view(np.int16)).to(dev).view(torch.bfloat16)
         shard_dev.append((t, ld))
-        L.leap_vocab_shard_stats(t, ld, N, width, a, tok_d, w_d, kw["inv_temp"], parts[k])
+        L.leap_vocab_shard_stats(t, ld, N, width, a, tok_d, w_d, kw["inv_temp"], parts[k],
+                                 partial_t=parts_t[k] if want_entropy else None)
     p = L.leap_grpo_params(kw["eps_lo"], kw["eps_hi"], kw["kl_coef"], kw["kl_type"], kw["inv_temp"])
     lp = torch.full((max(N, 1),), float("nan"), dtype=torch.float32, device=dev)
     tl = torch.full_like(lp, float("nan"))
@@ -48,9 +51,11 @@ def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False):
     ws_bytes = L.leap_vocab_merge_workspace_size(N)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     err = U.zeros_i32(1)
+    ent = torch.full_like(lp, float("nan")) if want_entropy else None
     L.leap_vocab_merge_objective(parts, len(shards), N, V, tok_d, U.T(np.asarray(old, np.float32)),
                                  U.T(np.asarray(ref, np.float32)), U.T(np.asarray(adv, np.float32)),
-                                 w_d, p, lp, tl, loss, state, ws, ws_bytes, err)
+                                 w_d, p, lp, tl, loss, state, ws, ws_bytes, err,
+                                 partials_t=parts_t, entropy_out=ent)
     out = np.zeros((N, V), np.uint16)
     for (a, width), (t, ld) in zip(shards, shard_dev):
         d = t if inplace else torch.full_like(t, float("nan"))
@@ -59,7 +64,8 @@ def _run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=False):
     torch.cuda.synchronize()
     return {"parts": parts.cpu().numpy()[:, :N], "logp": lp.cpu().numpy()[:N],
             "tok_loss": tl.cpu().numpy()[:N], "loss": float(loss.item()),
-            "state": state.cpu().numpy()[:N], "bad": int(err.item()), "dl": out}
+            "state": state.cpu().numpy()[:N], "bad": int(err.item()), "dl": out,
+            "entropy": ent.cpu().numpy()[:N] if want_entropy else None}
 
 
 def _check(lg, V, tok, old, ref, adv, w, shards, gpu, kw, atol_dl=2e-2, bad=0):
@@ -173,3 +179,37 @@ def test_merge_on_oracle_partials():
     o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V)
     assert np.max(np.abs(lp.cpu().numpy() - o["logp"])) < 2e-4
     assert abs(loss.item() - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7
+
+
+@pytest.mark.parametrize("widths,inv_temp", [([18992] * 8, 1.0), ([1000, 7, 40000, 12289], 0.9)])
+def test_shards_entropy(widths, inv_temp):
+    """The merged entropy against the oracle's on the whole rows; asking for
+    it changes no other output."""
+    V = sum(widths)
+    N = 48
+    kw = dict(KW, inv_temp=inv_temp)
+    U.log(f"vocab shards entropy {widths[:2]}.. x{len(widths)} V={V} T^-1={inv_temp}")
+    lg = wl.logits_host(3103, N, V)
+    tok = wl.sample_tokens_host(lg, V, 3103)
+    lg[1, ::3] = 0xFF80  # -inf columns
+    lg[2, :1007] = 0xFF80  # the first two shards all -inf in the second case
+    tok[1], tok[2] = 1, V - 1
+    cur, _ = oracle.logprob_rows(lg, tok, V=V, inv_temp=inv_temp)
+    n_old, n_ref = wl.logp_noise(3103, N)
+    old, ref = (cur + n_old).astype(np.float32), (cur + n_ref).astype(np.float32)
+    rng = np.random.default_rng(3103)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = np.ones(N, np.float32)
+    w[[5, 17]] = 0.0
+    shards = _shards(V, widths)
+    a = _run(lg, V, tok, old, ref, adv, w, shards, kw, want_entropy=True)
+    b = _run(lg, V, tok, old, ref, adv, w, shards, kw)
+    assert a["bad"] == b["bad"] == 0
+    assert np.array_equal(a["parts"], b["parts"], equal_nan=True)
+    assert np.array_equal(a["logp"], b["logp"]) and a["loss"] == b["loss"]
+    assert np.array_equal(a["dl"], b["dl"])
+    h, bad = oracle.entropy_rows(lg, V=V, inv_temp=inv_temp)
+    assert bad == 0
+    valid = w != 0
+    assert np.all(a["entropy"][~valid] == 0)
+    np.testing.assert_allclose(a["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)
