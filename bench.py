@@ -512,6 +512,27 @@ def _token_logp_torch(torch, hidden, weight, y, row_chunk=256):
     return out
 
 
+STAT_FIELDS = ("groups", "rollouts", "activated_groups", "multi_turn_rollouts",
+               "recovered_rollouts", "debugging_groups", "recovered_groups", "total_turns",
+               "passed_rollouts")
+
+
+def stats_report(counters, n_buckets: int) -> dict:
+    """The counters leap_rollout_stats wrote, named, with the rates the paper
+    reports formed from them for the benchmark's record (activated fraction,
+    per-rollout and per-group recovery, turns per pass)."""
+    c = [int(v) for v in counters]
+    out = dict(zip(STAT_FIELDS, c[:9]))
+    out["composition"] = [[c[9 + (b * 3 + o) * 2: 9 + (b * 3 + o) * 2 + 2] for o in range(3)]
+                          for b in range(n_buckets)]
+    ratio = lambda a, b: (a / b) if b else None  # noqa: E731
+    out["activated_fraction"] = ratio(out["activated_groups"], out["groups"])
+    out["per_rollout_recovery"] = ratio(out["recovered_rollouts"], out["multi_turn_rollouts"])
+    out["per_group_recovery"] = ratio(out["recovered_groups"], out["debugging_groups"])
+    out["turns_per_pass"] = ratio(out["total_turns"], out["passed_rollouts"])
+    return out
+
+
 def stats_leg(L, torch, s, n_buckets: int = 10, reps: int = 20):
     """The step's training statistics (activated groups, recovery rates,
     turns per pass, advantage-sign composition) from its own gate, outcomes
@@ -531,7 +552,7 @@ def stats_leg(L, torch, s, n_buckets: int = 10, reps: int = 20):
         e1.record(stream)
         torch.cuda.synchronize()
         ms.append(e0.elapsed_time(e1))
-    out = L.rollout_stats_summary(cnt.cpu().numpy(), n_buckets)
+    out = stats_report(cnt.cpu().numpy(), n_buckets)
     out["call_us"] = float(np.median(ms[1:])) * 1e3
     out["n_buckets"] = n_buckets
     log(f"[bench] rollout stats: activated {out['activated_fraction']:.3f}, per-rollout recovery "

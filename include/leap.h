@@ -11,8 +11,16 @@
  *    stream) and returns.
  *  - The returned leap_status reports what the host can check before
  *    launching: argument values, pointer alignment, workspace size, and a
- *    launch error from the HIP runtime (LEAP_ERR_HIP).  On any status other
- *    than LEAP_OK nothing has been enqueued.
+ *    launch error from the HIP runtime (LEAP_ERR_HIP).  Every host-side check
+ *    precedes the call's first launch, so on LEAP_ERR_INVALID_ARG,
+ *    LEAP_ERR_MISALIGNED, LEAP_ERR_WORKSPACE and LEAP_ERR_UNSUPPORTED nothing
+ *    has been enqueued.  On LEAP_ERR_HIP the kernels of the call launched
+ *    before the failing one may already be enqueued (the calls made of
+ *    several launches: the fused objective, the fused LM head, the
+ *    vocabulary merge and the rollout statistics); the outputs are then
+ *    undefined.  LEAP_ERR_HIP is returned only for an error raised by one of
+ *    the call's own launches: an error the caller's earlier HIP work left
+ *    pending is neither reported nor cleared.
  *  - Errors that depend on device data (a token id outside [0, V), a
  *    pass_turn outside [0, M], a rollout index out of range, a row whose
  *    logits are all -inf) add 1 per offending item to the optional device

@@ -44,12 +44,14 @@ AGG_SEQ_MEAN_TOKEN_MEAN, AGG_TOKEN_MEAN, AGG_SUM = 0, 1, 2
 KL_K3, KL_K1, KL_K2 = 0, 1, 2
 
 
-def build() -> str:
-    """Compile the oracle with gcc (no fast-math: IEEE double throughout)."""
+def build(src: str = _SRC, out: str = _LIB_PATH) -> str:
+    """Compile the oracle with gcc (no fast-math: IEEE double throughout).
+    ``src`` / ``out`` default to this package's source and library; the
+    mutation check of the test suite builds altered copies elsewhere."""
     cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared",
-           "-fno-fast-math", "-Wall", "-o", _LIB_PATH, _SRC, "-lm"]
+           "-fno-fast-math", "-Wall", "-o", out, src, "-lm"]
     subprocess.run(cmd, check=True)
-    return _LIB_PATH
+    return out
 
 
 _lib = None

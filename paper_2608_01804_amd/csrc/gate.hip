@@ -37,6 +37,7 @@ __global__ __launch_bounds__(kGroupsPerBlock * kWave) void dcp_gate_kernel(
 LEAP_API leap_status leap_dcp_gate(const uint8_t* first_turn_pass, int64_t n_groups, int32_t G,
                                    int32_t tau_min, int32_t tau_max, int32_t* n_fail,
                                    uint8_t* gate, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 1 || G > 1024) return LEAP_ERR_INVALID_ARG;
     if (tau_min < 0 || tau_max > G || tau_min > tau_max) return LEAP_ERR_INVALID_ARG;
@@ -47,7 +48,7 @@ LEAP_API leap_status leap_dcp_gate(const uint8_t* first_turn_pass, int64_t n_gro
     hipLaunchKernelGGL(dcp_gate_kernel, dim3(static_cast<unsigned>(grid)),
                        dim3(kGroupsPerBlock * kWave), 0, stream, first_turn_pass, n_groups, G,
                        tau_min, tau_max, n_fail, gate);
-    return launch_status();
+    return lc.status();
 }
 
 // Pass-rate window -> inclusive failure-count window, exactly.  With

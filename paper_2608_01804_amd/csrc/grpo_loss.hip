@@ -366,6 +366,7 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
     float* loss_out, void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err,
     hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V < 1 || ld < V || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     const leap_grpo_params& pp = *params;
@@ -401,10 +402,10 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
                            V, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
                            tok_loss_out, entropy_out, row_loss,
                            static_cast<uint16_t*>(dlogits_bf16), dev_err);
-        const leap_status st = launch_status();
+        const leap_status st = lc.status();
         if (st != LEAP_OK) return st;
     }
     hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(kReduceBlock), 0, stream, row_loss, N,
                        loss_out);
-    return launch_status();
+    return lc.status();
 }

@@ -12,11 +12,25 @@ namespace leap {
 
 constexpr int kWave = 64;
 
-// Map the launch result of the HIP runtime onto the library's status.
-inline leap_status launch_status() {
-    hipError_t e = hipGetLastError();
-    return e == hipSuccess ? LEAP_OK : LEAP_ERR_HIP;
-}
+// Launch errors of one entry point's own kernels.  Constructed before the
+// call's first launch, it records the error the HIP runtime holds pending
+// for this thread (without clearing it); status() reports LEAP_ERR_HIP only
+// for a pending error that differs from it, i.e. one a launch of this call
+// raised, and consumes that error.  An error the caller left pending before
+// the call is neither reported nor cleared.
+class LaunchCheck {
+  public:
+    LaunchCheck() : prior_(hipPeekAtLastError()) {}
+    leap_status status() const {
+        const hipError_t e = hipPeekAtLastError();
+        if (e == hipSuccess || e == prior_) return LEAP_OK;
+        (void)hipGetLastError();
+        return LEAP_ERR_HIP;
+    }
+
+  private:
+    hipError_t prior_;
+};
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

@@ -556,13 +556,13 @@ uint32_t extent32(uint64_t bytes) {
 template <bool AKM = false, class Epi>
 leap_status gemm_nt(const uint16_t* A, int64_t lda, uint64_t a_bytes, const uint16_t* B, int64_t ldb,
                     uint64_t b_bytes, int K, int64_t M, int64_t Ncols, const Epi& epi,
-                    hipStream_t stream) {
+                    hipStream_t stream, const LaunchCheck& lc) {
     const int tiles_m = static_cast<int>((M + kTile - 1) / kTile);
     const int tiles_n = static_cast<int>((Ncols + kTile - 1) / kTile);
     hipLaunchKernelGGL((gemm::gemm_nt_kernel<Epi, AKM>), dim3(gemm::gemm_grid(tiles_m, tiles_n)),
                        dim3(gemm::kThreads), 0, stream, A, lda, extent32(a_bytes), B, ldb,
                        extent32(b_bytes), K, tiles_m, tiles_n, epi);
-    return launch_status();
+    return lc.status();
 }
 
 }  // namespace
@@ -580,6 +580,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
     float* loss_out, float* dhidden, float* dweight, int32_t accumulate_dweight, void* workspace,
     size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || N > 0x7fffffffLL - kTile || V < 1 || H < 1 || !params || !loss_out)
         return LEAP_ERR_INVALID_ARG;
@@ -622,11 +623,11 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
         if (dweight && !accumulate_dweight) {
             hipLaunchKernelGGL(fill_zero_f32_kernel, dim3(1024), dim3(256), 0, stream, dweight,
                                static_cast<int64_t>(V) * H);
-            if ((st = launch_status()) != LEAP_OK) return st;
+            if ((st = lc.status()) != LEAP_OK) return st;
         }
         hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
                            row_loss, int64_t{0}, loss_out);
-        return launch_status();
+        return lc.status();
     }
 
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
@@ -638,7 +639,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     if (dweight) {
         hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.N_pad / kTr), (H + kTr - 1) / kTr),
                            dim3(256), 0, stream, Hm, N, H, static_cast<int64_t>(H), ht, d.N_pad);
-        if ((st = launch_status()) != LEAP_OK) return st;
+        if ((st = lc.status()) != LEAP_OK) return st;
     }
     if (dhidden) {
         for (int c = 0; c < d.n_chunks; ++c) {
@@ -648,23 +649,23 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
                                dim3(256), 0, stream, Wm + static_cast<int64_t>(c0) * H,
                                static_cast<int64_t>(rows), H, static_cast<int64_t>(H),
                                wt + static_cast<int64_t>(c) * H * d.Vc, static_cast<int64_t>(d.Vc));
-            if ((st = launch_status()) != LEAP_OK) return st;
+            if ((st = lc.status()) != LEAP_OK) return st;
         }
     }
 
     // 2. row statistics and the token logit
     {
         const StatsEpi epi{part, N, V, d.tiles_v, c2};
-        if ((st = gemm_nt(Hm, H, h_bytes, Wm, H, w_bytes, H, N, V, epi, stream)) != LEAP_OK) return st;
+        if ((st = gemm_nt(Hm, H, h_bytes, Wm, H, w_bytes, H, N, V, epi, stream, lc)) != LEAP_OK) return st;
     }
     // 3. per-token objective
     hipLaunchKernelGGL(lm_combine_kernel, dim3(static_cast<unsigned>(d.N_pad / 4)), dim3(256), 0,
                        stream, part, d.tiles_v, Hm, Wm, H, N, d.N_pad, V, token_ids, old_logp, ref_logp,
                        adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
-    if ((st = launch_status()) != LEAP_OK) return st;
+    if ((st = lc.status()) != LEAP_OK) return st;
     hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
                        row_loss, N, loss_out);
-    if ((st = launch_status()) != LEAP_OK) return st;
+    if ((st = lc.status()) != LEAP_OK) return st;
     if (!dhidden && !dweight) return LEAP_OK;
 
     // 4. gradients, one vocabulary chunk at a time
@@ -674,7 +675,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
             const DzEpi epi{token_ids, lse2, g, dz, d.Vc, N, V, c0, c2};
             const uint64_t wb = static_cast<uint64_t>(V - c0) * H * 2;
             if ((st = gemm_nt(Hm, H, h_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
-                              epi, stream)) != LEAP_OK)
+                              epi, stream, lc)) != LEAP_OK)
                 return st;
         }
         if (dweight) {
@@ -686,9 +687,9 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
             const int K = static_cast<int>(d.N_pad);
             st = accumulate_dweight
                      ? gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
-                                     StoreF32Epi<true>{C, H, rows, H}, stream)
+                                     StoreF32Epi<true>{C, H, rows, H}, stream, lc)
                      : gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
-                                     StoreF32Epi<false>{C, H, rows, H}, stream);
+                                     StoreF32Epi<false>{C, H, rows, H}, stream, lc);
             if (st != LEAP_OK) return st;
         }
         if (dhidden) {
@@ -696,9 +697,9 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
             const uint64_t bb = static_cast<uint64_t>(H) * d.Vc * 2;
             const uint16_t* wc = wt + static_cast<int64_t>(c0 / d.Vc) * H * d.Vc;
             st = c0 > 0 ? gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
-                                  StoreF32Epi<true>{dhidden, H, N, H}, stream)
+                                  StoreF32Epi<true>{dhidden, H, N, H}, stream, lc)
                         : gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
-                                  StoreF32Epi<false>{dhidden, H, N, H}, stream);
+                                  StoreF32Epi<false>{dhidden, H, N, H}, stream, lc);
             if (st != LEAP_OK) return st;
         }
     }

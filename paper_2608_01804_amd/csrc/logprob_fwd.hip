@@ -219,6 +219,7 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
                                       const int32_t* token_ids, const float* w_tok,
                                       float inv_temperature, float* logp_out,
                                       float* entropy_out, int32_t* dev_err, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V < 1 || ld < V) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -231,5 +232,5 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
     hipLaunchKernelGGL(entropy_out ? fc.fn_ent : fc.fn, dim3(static_cast<unsigned>(N)),
                        dim3(fc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld, V,
                        token_ids, w_tok, inv_temperature, logp_out, entropy_out, dev_err);
-    return launch_status();
+    return lc.status();
 }

@@ -48,6 +48,7 @@ __global__ __launch_bounds__(kProbeBlock) void hbm_probe_kernel(const u32x4* __r
 
 LEAP_API leap_status leap_probe_hbm(const void* src, void* dst, size_t bytes, int32_t mode,
                                     hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (mode < 0 || mode > 2 || (bytes & 15u) != 0) return LEAP_ERR_INVALID_ARG;
     if (bytes == 0) return LEAP_OK;
@@ -70,5 +71,5 @@ LEAP_API leap_status leap_probe_hbm(const void* src, void* dst, size_t bytes, in
         hipLaunchKernelGGL(hbm_probe_kernel<1>, dim3(grid), dim3(kProbeBlock), 0, stream, s, d, n16);
     else
         hipLaunchKernelGGL(hbm_probe_kernel<2>, dim3(grid), dim3(kProbeBlock), 0, stream, s, d, n16);
-    return launch_status();
+    return lc.status();
 }

@@ -130,6 +130,7 @@ LEAP_API leap_status leap_rank_advantages(const int32_t* pass_turn, const int32_
                                           int32_t* n_worse, int32_t* n_better, int32_t* rank_r,
                                           float* reward, float* advantage, int32_t* dev_err,
                                           hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 2 || G > 1024 || M < 1) return LEAP_ERR_INVALID_ARG;
     if (!(eps >= 0.0f) || !__builtin_isfinite(eps)) return LEAP_ERR_INVALID_ARG;
@@ -155,5 +156,5 @@ LEAP_API leap_status leap_rank_advantages(const int32_t* pass_turn, const int32_
                            norm, eps, tpg, gpb, n_worse, n_better, rank_r, reward, advantage,
                            dev_err);
     }
-    return launch_status();
+    return lc.status();
 }

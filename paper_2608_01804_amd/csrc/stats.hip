@@ -122,6 +122,7 @@ LEAP_API leap_status leap_rollout_stats(const int32_t* pass_turn, const int32_t*
                                         const uint8_t* gate, const float* advantage,
                                         int64_t n_groups, int32_t G, int32_t M, int32_t n_buckets,
                                         int64_t* counters, int32_t* dev_err, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 1 || G > 1024 || M < 1 || n_buckets < 1 || n_buckets > kMaxBuckets ||
         !counters)
@@ -132,11 +133,11 @@ LEAP_API leap_status leap_rollout_stats(const int32_t* pass_turn, const int32_t*
     const int n = kHead + 6 * n_buckets;
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(counters);
     hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, stream, cnt, n, n_groups, G);
-    leap_status st = launch_status();
+    leap_status st = lc.status();
     if (st != LEAP_OK || n_groups == 0) return st;
     const int64_t blocks = (n_groups + kGroupsPerBlock - 1) / kGroupsPerBlock;
     hipLaunchKernelGGL(rollout_stats_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kStatsBlock), 0,
                        stream, pass_turn, n_turns, gate, advantage, n_groups, G, M, n_buckets, cnt,
                        dev_err);
-    return launch_status();
+    return lc.status();
 }

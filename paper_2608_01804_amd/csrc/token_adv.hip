@@ -61,6 +61,7 @@ LEAP_API leap_status leap_token_advantages(const float* advantage, const int32_t
                                            int64_t N, float gamma, int32_t agg,
                                            double denominator, float* adv_tok, float* w_tok,
                                            int32_t* dev_err, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || n_rollouts < 0) return LEAP_ERR_INVALID_ARG;
     if (!(gamma > 0.0f && gamma <= 1.0f)) return LEAP_ERR_INVALID_ARG;
@@ -78,5 +79,5 @@ LEAP_API leap_status leap_token_advantages(const float* advantage, const int32_t
                        stream, advantage, tok_rollout, tok_turn, n_turns, n_gen_tokens,
                        n_rollouts, N, static_cast<double>(gamma), agg, denominator, adv_tok,
                        w_tok, dev_err);
-    return launch_status();
+    return lc.status();
 }

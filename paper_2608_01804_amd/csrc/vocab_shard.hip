@@ -350,6 +350,7 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
                                             const int32_t* token_ids, const float* w_tok,
                                             float inv_temperature, float* partial,
                                             float* partial_t, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -363,7 +364,7 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
                        dim3(sc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
                        V_shard, vocab_start, token_ids, w_tok, inv_temperature,
                        reinterpret_cast<float4*>(partial), partial_t);
-    return launch_status();
+    return lc.status();
 }
 
 LEAP_API size_t leap_vocab_merge_workspace_size(int64_t N) {
@@ -377,6 +378,7 @@ LEAP_API leap_status leap_vocab_merge_objective(
     const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
     float* entropy_out, float* loss_out, float* row_state, void* workspace, size_t ws_bytes,
     int32_t* dev_err, hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || n_shards < 1 || V_total < 1 || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     if (!params_ok(*params)) return LEAP_ERR_INVALID_ARG;
@@ -402,12 +404,12 @@ LEAP_API leap_status leap_vocab_merge_objective(
                            V_total, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
                            tok_loss_out, entropy_out, row_loss,
                            reinterpret_cast<float2*>(row_state), dev_err);
-        const leap_status st = launch_status();
+        const leap_status st = lc.status();
         if (st != LEAP_OK) return st;
     }
     hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
                        row_loss, N, loss_out);
-    return launch_status();
+    return lc.status();
 }
 
 LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, int64_t N,
@@ -415,6 +417,7 @@ LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, i
                                           const int32_t* token_ids, const float* row_state,
                                           float inv_temperature, void* dlogits_bf16,
                                           hipStream_t stream) {
+    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -433,5 +436,5 @@ LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, i
                        static_cast<const uint16_t*>(logits_bf16), ld, V_shard, vocab_start,
                        token_ids, reinterpret_cast<const float2*>(row_state), inv_temperature,
                        static_cast<uint16_t*>(dlogits_bf16));
-    return launch_status();
+    return lc.status();
 }

@@ -322,26 +322,6 @@ def leap_rollout_stats(pass_turn, n_turns, gate, advantage, n_groups, G, M, n_bu
     _check(st, "leap_rollout_stats")
 
 
-STAT_FIELDS = ("groups", "rollouts", "activated_groups", "multi_turn_rollouts",
-               "recovered_rollouts", "debugging_groups", "recovered_groups", "total_turns",
-               "passed_rollouts")
-
-
-def rollout_stats_summary(counters, n_buckets):
-    """Named counters and derived rates from the int64 counter array that
-    leap_rollout_stats wrote (host-side arithmetic on its output only)."""
-    c = [int(v) for v in counters]
-    out = dict(zip(STAT_FIELDS, c[:9]))
-    out["composition"] = [[c[9 + (b * 3 + o) * 2: 9 + (b * 3 + o) * 2 + 2] for o in range(3)]
-                          for b in range(n_buckets)]
-    ratio = lambda a, b: (a / b) if b else None  # noqa: E731
-    out["activated_fraction"] = ratio(out["activated_groups"], out["groups"])
-    out["per_rollout_recovery"] = ratio(out["recovered_rollouts"], out["multi_turn_rollouts"])
-    out["per_group_recovery"] = ratio(out["recovered_groups"], out["debugging_groups"])
-    out["turns_per_pass"] = ratio(out["total_turns"], out["passed_rollouts"])
-    return out
-
-
 def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:
     st = lib().leap_probe_hbm(_ptr(src, None, "src"), _ptr(dst, None, "dst"), int(nbytes),
                               int(mode), _stream(stream))

@@ -331,11 +331,3 @@ def test_rollout_stats_rejects(kw, status):
     with pytest.raises(L.LeapError) as e:
         L.leap_rollout_stats(**a)
     assert e.value.status == status
-
-
-def test_rollout_stats_summary_is_host_arithmetic_on_counters():
-    c = [4, 16, 3, 7, 2, 2, 1, 29, 9] + [0] * 24
-    c[9 + (3 * 3 + 0) * 2 + 0] = 1
-    s = L.rollout_stats_summary(c, 4)
-    assert s["activated_fraction"] == 0.75 and s["per_group_recovery"] == 0.5
-    assert s["turns_per_pass"] == 29 / 9 and s["composition"][3][0] == [1, 0]

@@ -7,6 +7,8 @@ ratio-one, KL-free special case), the exact KL divergence of two categorical
 distributions (scipy.stats.entropy) as the expectation of the k3 and k1
 estimators, and central finite differences of the oracle's own loss.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -14,6 +16,8 @@ from scipy import stats
 
 import oracle
 import workloads as wl
+
+HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def _rand_rows(rng, N, V, scale=2.0):
@@ -47,6 +51,10 @@ def test_logp_matches_torch_log_softmax():
     xb = wl.bf16_bits_to_f32(lg).astype(np.float64)
     assert bad == 0
     np.testing.assert_allclose(lp, _logp_torch(xb, y), rtol=0, atol=1e-12)
+    for inv_temp in (0.5, 1.7):  # softmax of the scaled logits
+        lp_t, bad = oracle.logprob_rows(lg, y, inv_temp=inv_temp)
+        assert bad == 0
+        np.testing.assert_allclose(lp_t, _logp_torch(inv_temp * xb, y), rtol=0, atol=1e-12)
 
 
 def test_large_logits_are_shift_invariant():
@@ -108,27 +116,37 @@ def test_k2_is_half_squared_log_ratio_mean():
     assert out["loss"] == pytest.approx(float(np.sum(p * 0.5 * (np.log(p) - ref) ** 2)), rel=1e-10)
 
 
+# Ratio placements: well inside the clip window, above and below it, and --
+# for the asymmetric bounds (0.2, 0.28) -- inside the windows 1.2 < rho < 1.28
+# and 0.72 < rho < 0.8 that only the correct assignment of the two bounds
+# treats as it should (unclipped above 1.2, clipped below 0.8).
+RHO = {"inside": 1.05, "above": 1.6, "below": 0.5, "hi_window": 1.25, "lo_window": 0.76}
+
+
 def _fd_case(seed, kl_type, inv_temp, branch):
     rng = np.random.default_rng(seed)
     N, V = 4, 12
     x = _rand_rows(rng, N, V, 1.5)
     y = rng.integers(0, V, N)
     lp = _logp_torch(x * inv_temp, y)
-    # place rho = exp(lp - old) well inside or well outside the clip window
-    rho = {"inside": 1.05, "above": 1.6, "below": 0.5}[branch]
-    old = lp - np.log(rho) + rng.normal(0, 0.01, N)
+    # place rho = exp(lp - old) at the branch's value (within 1 %)
+    old = lp - np.log(RHO[branch]) + rng.normal(0, 0.003, N)
     ref = lp + rng.normal(0, 0.3, N)
-    A = rng.choice([-1.3, 0.8], N)
+    A = np.array([-1.3, 0.8, -0.6, 1.1])
     w = rng.uniform(0.5, 2.0, N)
     return x, y, old, ref, A, w
 
 
+FD_CASES = [(b, (0.2, 0.2)) for b in ("inside", "above", "below")] + \
+           [(b, (0.2, 0.28)) for b in ("inside", "above", "below", "hi_window", "lo_window")]
+
+
 @pytest.mark.parametrize("kl_type", [oracle.KL_K3, oracle.KL_K1, oracle.KL_K2])
 @pytest.mark.parametrize("inv_temp", [1.0, 0.7])
-@pytest.mark.parametrize("branch", ["inside", "above", "below"])
-def test_gradient_matches_central_differences(kl_type, inv_temp, branch):
+@pytest.mark.parametrize("branch,eps", FD_CASES, ids=[f"{b}-{e[0]}-{e[1]}" for b, e in FD_CASES])
+def test_gradient_matches_central_differences(kl_type, inv_temp, branch, eps):
     x, y, old, ref, A, w = _fd_case(11, kl_type, inv_temp, branch)
-    kw = dict(eps_lo=0.2, eps_hi=0.2, kl_coef=0.05, kl_type=kl_type, inv_temp=inv_temp)
+    kw = dict(eps_lo=eps[0], eps_hi=eps[1], kl_coef=0.05, kl_type=kl_type, inv_temp=inv_temp)
     out = oracle.grpo_rows(x, y, old, ref, A, w, **kw)
     h = 1e-6
     fd = np.zeros_like(x)
@@ -156,6 +174,52 @@ def test_clipped_ratio_passes_no_surrogate_gradient():
     out = oracle.grpo_rows(x, y, old, np.zeros(2), A, np.ones(2), kl_coef=0.0)
     assert np.all(out["dlogits"] == 0.0)
     np.testing.assert_allclose(out["tok_loss"], [-(1.2 * 2.0), -(0.8 * -2.0)], rtol=1e-12)
+
+
+def _clip_higher_rows():
+    rows = []
+    for line in open(os.path.join(HERE, "golden", "clip_higher_examples.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            rows.append(tuple(float(v) for v in line.split()))
+    return rows
+
+
+@pytest.mark.parametrize("row", _clip_higher_rows())
+def test_clip_higher_golden(row):
+    """Hand-worked loss and gradient of the surrogate with eps_lo != eps_hi
+    (tests/golden/clip_higher_examples.txt): one row of 4 equal logits."""
+    eps_lo, eps_hi, beta, A, rho, q, loss, dl, d_tok, d_other = row
+    V = 4
+    lp = -np.log(4.0)
+    out = oracle.grpo_rows(np.zeros((1, V)), [0], [lp - np.log(rho)], [lp + np.log(q)], [A], [1.0],
+                           eps_lo=eps_lo, eps_hi=eps_hi, kl_coef=beta, kl_type=oracle.KL_K3)
+    assert out["logp"][0] == pytest.approx(lp, abs=1e-15)
+    assert out["tok_loss"][0] == pytest.approx(loss, rel=1e-12, abs=1e-13)
+    assert out["loss"] == pytest.approx(loss, rel=1e-12, abs=1e-13)
+    d = out["dlogits"][0]
+    assert d[0] == pytest.approx(d_tok, rel=1e-12, abs=1e-14)
+    np.testing.assert_allclose(d[1:], d_other, rtol=1e-12, atol=1e-14)
+    # the gradient with respect to logp is the token column over (1 - 1/4)
+    assert d[0] / 0.75 == pytest.approx(dl, rel=1e-12, abs=1e-14)
+
+
+def test_clip_bounds_are_not_interchangeable():
+    """The two bounds act on opposite sides: with (eps_lo, eps_hi) = (0.2,
+    0.28) a ratio of 1.25 with A > 0 is unclipped and 0.78 with A < 0 is
+    clipped; swapping the two bounds reverses both decisions."""
+    lp = -np.log(4.0)
+    args = lambda rho, A: (np.zeros((1, 4)), [0], [lp - np.log(rho)], [lp], [A], [1.0])  # noqa: E731
+    a = oracle.grpo_rows(*args(1.25, 1.5), eps_lo=0.2, eps_hi=0.28, kl_coef=0.0)
+    b = oracle.grpo_rows(*args(1.25, 1.5), eps_lo=0.28, eps_hi=0.2, kl_coef=0.0)
+    assert a["tok_loss"][0] == pytest.approx(-1.875, rel=1e-13)
+    assert b["tok_loss"][0] == pytest.approx(-1.8, rel=1e-13)
+    assert np.any(a["dlogits"] != 0) and np.all(b["dlogits"] == 0)
+    c = oracle.grpo_rows(*args(0.78, -1.5), eps_lo=0.2, eps_hi=0.28, kl_coef=0.0)
+    d = oracle.grpo_rows(*args(0.78, -1.5), eps_lo=0.28, eps_hi=0.2, kl_coef=0.0)
+    assert c["tok_loss"][0] == pytest.approx(1.2, rel=1e-13)
+    assert d["tok_loss"][0] == pytest.approx(1.17, rel=1e-13)
+    assert np.all(c["dlogits"] == 0) and np.any(d["dlogits"] != 0)
 
 
 def test_bf16_entry_equals_f64_entry_on_representable_values():
