@@ -37,7 +37,6 @@ __global__ __launch_bounds__(kGroupsPerBlock * kWave) void dcp_gate_kernel(
 LEAP_API leap_status leap_dcp_gate(const uint8_t* first_turn_pass, int64_t n_groups, int32_t G,
                                    int32_t tau_min, int32_t tau_max, int32_t* n_fail,
                                    uint8_t* gate, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 1 || G > 1024) return LEAP_ERR_INVALID_ARG;
     if (tau_min < 0 || tau_max > G || tau_min > tau_max) return LEAP_ERR_INVALID_ARG;
@@ -45,6 +44,7 @@ LEAP_API leap_status leap_dcp_gate(const uint8_t* first_turn_pass, int64_t n_gro
     if (!first_turn_pass || !gate) return LEAP_ERR_INVALID_ARG;
     const int64_t grid = (n_groups + kGroupsPerBlock - 1) / kGroupsPerBlock;
     if (grid > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     hipLaunchKernelGGL(dcp_gate_kernel, dim3(static_cast<unsigned>(grid)),
                        dim3(kGroupsPerBlock * kWave), 0, stream, first_turn_pass, n_groups, G,
                        tau_min, tau_max, n_fail, gate);

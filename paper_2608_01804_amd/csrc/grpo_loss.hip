@@ -366,7 +366,6 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
     float* loss_out, void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err,
     hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V < 1 || ld < V || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     const leap_grpo_params& pp = *params;
@@ -393,6 +392,7 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
 
+    const leap::LaunchCheck lc;
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     float* row_loss = static_cast<float*>(workspace);
     if (N > 0) {

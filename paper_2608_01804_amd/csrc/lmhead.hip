@@ -580,7 +580,6 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
     float* loss_out, float* dhidden, float* dweight, int32_t accumulate_dweight, void* workspace,
     size_t ws_bytes, int32_t* dev_err, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || N > 0x7fffffffLL - kTile || V < 1 || H < 1 || !params || !loss_out)
         return LEAP_ERR_INVALID_ARG;
@@ -607,6 +606,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     if (!workspace || ws_bytes < L.total) return LEAP_ERR_WORKSPACE;
     if (!aligned16(workspace)) return LEAP_ERR_MISALIGNED;
 
+    const leap::LaunchCheck lc;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     uint16_t* ht = reinterpret_cast<uint16_t*>(ws + L.ht);
     uint16_t* wt = reinterpret_cast<uint16_t*>(ws + L.wt);

@@ -219,7 +219,6 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
                                       const int32_t* token_ids, const float* w_tok,
                                       float inv_temperature, float* logp_out,
                                       float* entropy_out, int32_t* dev_err, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V < 1 || ld < V) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -228,6 +227,7 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
     if (!logits_bf16 || !token_ids || !logp_out) return LEAP_ERR_INVALID_ARG;
     if (!aligned16(logits_bf16) || (ld & 7) != 0) return LEAP_ERR_MISALIGNED;
     if (N > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     const FwdConfig fc = pick_fwd_config(V);
     hipLaunchKernelGGL(entropy_out ? fc.fn_ent : fc.fn, dim3(static_cast<unsigned>(N)),
                        dim3(fc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld, V,

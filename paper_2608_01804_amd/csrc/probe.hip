@@ -48,12 +48,12 @@ __global__ __launch_bounds__(kProbeBlock) void hbm_probe_kernel(const u32x4* __r
 
 LEAP_API leap_status leap_probe_hbm(const void* src, void* dst, size_t bytes, int32_t mode,
                                     hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (mode < 0 || mode > 2 || (bytes & 15u) != 0) return LEAP_ERR_INVALID_ARG;
     if (bytes == 0) return LEAP_OK;
     if ((mode != 2 && !src) || !dst) return LEAP_ERR_INVALID_ARG;
     if ((mode != 2 && !aligned16(src)) || !aligned16(dst)) return LEAP_ERR_MISALIGNED;
+    const leap::LaunchCheck lc;
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)

@@ -130,7 +130,6 @@ LEAP_API leap_status leap_rank_advantages(const int32_t* pass_turn, const int32_
                                           int32_t* n_worse, int32_t* n_better, int32_t* rank_r,
                                           float* reward, float* advantage, int32_t* dev_err,
                                           hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 2 || G > 1024 || M < 1) return LEAP_ERR_INVALID_ARG;
     if (!(eps >= 0.0f) || !__builtin_isfinite(eps)) return LEAP_ERR_INVALID_ARG;
@@ -145,6 +144,7 @@ LEAP_API leap_status leap_rank_advantages(const int32_t* pass_turn, const int32_
     const int block = tpg * gpb;
     const int64_t grid = (n_groups + gpb - 1) / gpb;
     if (grid > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     if (key == LEAP_KEY_LEX) {
         hipLaunchKernelGGL(rank_tournament_kernel<true>, dim3(static_cast<unsigned>(grid)),
                            dim3(block), 0, stream, pass_turn, speedup_q, n_tokens, n_groups, G, M,

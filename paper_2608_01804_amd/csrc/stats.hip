@@ -122,7 +122,6 @@ LEAP_API leap_status leap_rollout_stats(const int32_t* pass_turn, const int32_t*
                                         const uint8_t* gate, const float* advantage,
                                         int64_t n_groups, int32_t G, int32_t M, int32_t n_buckets,
                                         int64_t* counters, int32_t* dev_err, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (n_groups < 0 || G < 1 || G > 1024 || M < 1 || n_buckets < 1 || n_buckets > kMaxBuckets ||
         !counters)
@@ -130,6 +129,7 @@ LEAP_API leap_status leap_rollout_stats(const int32_t* pass_turn, const int32_t*
     if (n_groups > 0 && (!pass_turn || !n_turns || !gate)) return LEAP_ERR_INVALID_ARG;
     if ((reinterpret_cast<uintptr_t>(counters) & 7u) != 0) return LEAP_ERR_MISALIGNED;
     if (n_groups > 0x7fffffffLL) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     const int n = kHead + 6 * n_buckets;
     unsigned long long* cnt = reinterpret_cast<unsigned long long*>(counters);
     hipLaunchKernelGGL(stats_init_kernel, dim3(1), dim3(256), 0, stream, cnt, n, n_groups, G);

@@ -61,7 +61,6 @@ LEAP_API leap_status leap_token_advantages(const float* advantage, const int32_t
                                            int64_t N, float gamma, int32_t agg,
                                            double denominator, float* adv_tok, float* w_tok,
                                            int32_t* dev_err, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || n_rollouts < 0) return LEAP_ERR_INVALID_ARG;
     if (!(gamma > 0.0f && gamma <= 1.0f)) return LEAP_ERR_INVALID_ARG;
@@ -75,6 +74,7 @@ LEAP_API leap_status leap_token_advantages(const float* advantage, const int32_t
     const int block = 256;
     int64_t grid = (N + block - 1) / block;
     if (grid > 65536) grid = 65536;
+    const leap::LaunchCheck lc;
     hipLaunchKernelGGL(token_advantages_kernel, dim3(static_cast<unsigned>(grid)), dim3(block), 0,
                        stream, advantage, tok_rollout, tok_turn, n_turns, n_gen_tokens,
                        n_rollouts, N, static_cast<double>(gamma), agg, denominator, adv_tok,

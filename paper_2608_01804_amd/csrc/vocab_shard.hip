@@ -350,7 +350,6 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
                                             const int32_t* token_ids, const float* w_tok,
                                             float inv_temperature, float* partial,
                                             float* partial_t, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -359,6 +358,7 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
     if (!logits_bf16 || !token_ids || !partial) return LEAP_ERR_INVALID_ARG;
     if (!aligned16(logits_bf16) || (ld & 7) != 0 || !aligned16(partial)) return LEAP_ERR_MISALIGNED;
     if (N > 0x7fffffff) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     const StatsConfig sc = pick_stats_config(V_shard);
     hipLaunchKernelGGL(partial_t ? sc.fn_ent : sc.fn, dim3(static_cast<unsigned>(N)),
                        dim3(sc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
@@ -378,7 +378,6 @@ LEAP_API leap_status leap_vocab_merge_objective(
     const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
     float* entropy_out, float* loss_out, float* row_state, void* workspace, size_t ws_bytes,
     int32_t* dev_err, hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || n_shards < 1 || V_total < 1 || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     if (!params_ok(*params)) return LEAP_ERR_INVALID_ARG;
@@ -395,6 +394,7 @@ LEAP_API leap_status leap_vocab_merge_objective(
     }
     if (!workspace || ws_bytes < leap_vocab_merge_workspace_size(N)) return LEAP_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
+    const leap::LaunchCheck lc;
     const obj::Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     float* row_loss = static_cast<float*>(workspace);
     if (N > 0) {
@@ -417,7 +417,6 @@ LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, i
                                           const int32_t* token_ids, const float* row_state,
                                           float inv_temperature, void* dlogits_bf16,
                                           hipStream_t stream) {
-    const leap::LaunchCheck lc;
     using namespace leap;
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
@@ -432,6 +431,7 @@ LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, i
     const uintptr_t b0 = reinterpret_cast<uintptr_t>(dlogits_bf16);
     const uintptr_t bytes = static_cast<uintptr_t>(N) * static_cast<uintptr_t>(ld) * 2u;
     if (a0 != b0 && a0 < b0 + bytes && b0 < a0 + bytes) return LEAP_ERR_INVALID_ARG;
+    const leap::LaunchCheck lc;
     hipLaunchKernelGGL(shard_bwd_kernel, dim3(static_cast<unsigned>(N)), dim3(kBwdBlock), 0, stream,
                        static_cast<const uint16_t*>(logits_bf16), ld, V_shard, vocab_start,
                        token_ids, reinterpret_cast<const float2*>(row_state), inv_temperature,

@@ -199,6 +199,61 @@ def test_lmhead_narrow_chunks():
     _sampled_rows_and_dw_check(inp, gpu, kw, 5001, "narrow")
 
 
+def _oracle_by_row_blocks(inp, kw, block=2048):
+    """The oracle's fused LM head over every row, evaluated a block of rows
+    at a time (``oracle.lmhead`` with ``rows``) so that Z and dZ never exist
+    whole; dW = dZ^T H summed over the blocks in order.  Returns logp,
+    tok_loss, loss, dH, dW and the bounds |dZ| |W| and |dZ|^T |H| of the
+    gradient check."""
+    N, H = inp["hid"].shape
+    V = inp["wt"].shape[0]
+    Hf, Wf = U.bf16_f64(inp["h_u16"]), U.bf16_f64(inp["w_u16"])
+    aW, aH = np.abs(Wf), np.abs(Hf)
+    out = {"logp": np.empty(N), "tok_loss": np.empty(N), "loss": 0.0, "bad": 0,
+           "dH": np.empty((N, H)), "bH": np.empty((N, H)), "dW": np.zeros((V, H)),
+           "bW": np.zeros((V, H))}
+    for r0 in range(0, N, block):
+        rows = np.arange(r0, min(N, r0 + block))
+        o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"],
+                          inp["adv"], inp["w"], rows=rows, **kw)
+        out["logp"][rows], out["tok_loss"][rows] = o["logp"], o["tok_loss"]
+        out["loss"] += o["loss"]
+        out["bad"] += o["bad"]
+        out["dH"][rows] = o["dH"]
+        aZ = np.abs(o["dZ"])
+        out["bH"][rows] = aZ @ aW
+        out["dW"] += o["dZ"].T @ Hf[rows]
+        out["bW"] += aZ.T @ aH[rows]
+    return out
+
+
+@pytest.mark.parametrize("N,V,H", [
+    (16384, 4096, 128),   # dW pass: K = 16384, one 4096-column chunk
+    (65281, 20000, 64),   # K = 65536, two 16384-column chunks (the second 3840 wide)
+])
+def test_lmhead_long_k_dw_oracle(N, V, H):
+    """dW = dZ^T H on the k-major dW pass at the reduction lengths of the
+    full-size calls (K = N_pad = 16384 and 65536), and the narrow-chunk
+    split, element by element against the fp64 oracle over every row."""
+    U.log(f"lmhead long-K N={N} V={V} H={H}: inputs")
+    inp = U.lmhead_inputs(6000 + H, N, V, H, cur="torch", bad_rows=(3,))
+    kw = _kw()
+    U.log("  fused call")
+    gpu = U.run_lmhead(inp, **kw)
+    U.log("  oracle by row blocks")
+    o = _oracle_by_row_blocks(inp, kw)
+    valid = (inp["w"] != 0) & (inp["y"] < V)
+    assert gpu["bad"] == o["bad"] == 1
+    err = np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]))
+    U.log(f"  logp max err {err:.3e}")
+    assert err < 2e-3
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
+    U.check_grad(gpu["dH"], o["dH"], o["bH"], f"long-K N={N} dH")
+    U.check_grad(gpu["dW"], o["dW"], o["bW"], f"long-K N={N} dW")
+    assert np.all(gpu["dH"][~valid] == 0.0)
+
+
 def test_lmhead_full_shape_sampled_rows():
     N, V, H = 16384, 151936, 4096
     U.log(f"lmhead full N={N} V={V} H={H}: inputs")

@@ -108,9 +108,10 @@ def test_rank_all_equal_gives_zero():
 # ----------------------------------------------------------------------------
 # Token advantages
 # ----------------------------------------------------------------------------
-def _step_tokens(name):
+def _step_tokens(name, layout="packed"):
     lat, ro = _step(name)
-    mbs = wl.pack(ro, lat.cfg["rows_per_mb"])
+    pack = wl.pack if layout == "packed" else wl.pack_right_padded
+    mbs = pack(ro, lat.cfg["rows_per_mb"])
     tok_r = np.concatenate([m.tok_rollout for m in mbs])
     tok_t = np.concatenate([m.tok_turn for m in mbs])
     ora = oracle.rank_tournament(ro.pass_turn, ro.G, ro.M, eps=U.EPS_ADV)
@@ -172,23 +173,86 @@ def _tiny_weights(agg):
     return adv.astype(np.float32), w.astype(np.float32)
 
 
-@pytest.mark.parametrize("mode", ["sum", "seq_mean", "clip"])
+@pytest.mark.parametrize("mode", ["sum", "seq_mean", "clip", "clip_higher"])
 def test_grpo_tiny_full_parity(mode):
+    """Every row of the tiny workload.  The clip modes draw the old-policy
+    log-probs with sigma 0.3, so a third of the rows are clipped;
+    clip_higher runs the asymmetric bounds eps_lo = 0.2, eps_hi = 0.28."""
     N, V = 2048, 32768
-    old_sigma = wl.CLIP_CASE_OLD_SIGMA if mode == "clip" else wl.OLD_SIGMA
+    old_sigma = wl.CLIP_CASE_OLD_SIGMA if mode.startswith("clip") else wl.OLD_SIGMA
+    kw = dict(KW, eps_hi=0.28) if mode == "clip_higher" else KW
     lg, tok, old, ref = U.make_inputs_host(1001, N, V, old_sigma=old_sigma)
     adv, w = _tiny_weights(oracle.AGG_SEQ_MEAN_TOKEN_MEAN if mode == "seq_mean" else oracle.AGG_SUM)
     U.log(f"grpo tiny {mode}")
-    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
-    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **kw)
     valid = w != 0
     _check_rows(gpu, o, valid, mode)
     assert gpu["bad"] == 0
+    if mode == "clip_higher":
+        # rows whose ratio sits in the windows where the two bounds' roles
+        # matter: 1.2 < rho < 1.28 with A > 0, 0.72 < rho < 0.8 with A < 0
+        rho = np.exp(o["logp"] - old.astype(np.float64))
+        win = ((rho > 1.2) & (rho < 1.28) & (adv > 0)) | ((rho > 0.72) & (rho < 0.8) & (adv < 0))
+        U.log(f"  {int(win.sum())} rows in the asymmetric windows")
+        assert win.sum() >= 20
     for r0 in range(0, N, 256):
         rows = np.arange(r0, r0 + 256)
         U.check_dlogits(U.dl_rows(gpu["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
-                        atol=1e-2 if mode == "seq_mean" else 2e-2, kw=KW,
+                        atol=1e-2 if mode == "seq_mean" else 2e-2, kw=kw,
                         rel_to_max=(mode == "seq_mean"))
+
+
+@pytest.mark.parametrize("V", [32768, 151936])
+def test_grpo_wide_range_and_peaked_rows(V):
+    """Entry-wise relative check of dlogits on rows whose probabilities span
+    many orders of magnitude: logits of std 6 and 12, and rows with one
+    logit 30 above the rest (the token on the spike, or away from it).  The
+    kernel keeps each lane's 2^(x c - m_lane c) in [0, 1] as fp16 between
+    its two register passes: relative precision 2^-11 down to 2^-14, an
+    absolute step of 2^-24 below (subnormals), 0 below 2^-25.  With the
+    per-lane scale 2^(m_lane c - lse2) <= 1 and the bf16 store (2^-9), every
+    entry of the gradient is within 2^-8 |d| + 2^-24 |g| of the oracle, g
+    the row's d loss / d logp; the token's own column, g (1 - p_y), carries
+    the fp32 log-prob's error instead: 2^-8 |d| + 2^-12 |g|."""
+    N = 64
+    rng = np.random.default_rng(V + 6)
+
+    def edit(lg, tok):
+        x = wl.bf16_bits_to_f32(lg[:, :V]).astype(np.float32)
+        x[:16] *= 3.0                       # std 6
+        x[48:] *= 6.0                       # std 12
+        spike = rng.integers(0, V, N)
+        for k in range(16, 48):
+            x[k, spike[k]] += 30.0
+            tok[k] = spike[k] if k < 32 else (spike[k] + 1 + rng.integers(0, V - 1)) % V
+        lg[:, :V] = wl.f32_to_bf16_bits(x)
+        for k in list(range(16)) + list(range(48, N)):  # tokens of the rescaled rows
+            tok[k] = rng.integers(0, V)
+
+    lg, tok, old, ref = U.make_inputs_host(V + 6, N, V, edit=edit)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = np.ones(N, np.float32)
+    kw = dict(KW, kl_coef=0.05)
+    U.log(f"grpo wide-range / peaked rows V={V}")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, **kw)
+    assert gpu["bad"] == o["bad"] == 0
+    _check_rows(gpu, o, w != 0)
+    got = U.dl_rows(gpu["dl_dev"], np.arange(N), V)
+    want = o["dlogits"]
+    # |g| <= w (|A| rho + beta |d KL / d logp|), k3: d KL / d logp = 1 - e^(ref - logp)
+    rho = np.exp(o["logp"] - old.astype(np.float64))
+    g_max = w * (np.abs(adv) * rho + kw["kl_coef"] * np.abs(1.0 - np.exp(ref - o["logp"])))
+    tol = 2.0 ** -8 * np.abs(want) + 2.0 ** -24 * g_max[:, None]
+    tol[np.arange(N), tok] = 2.0 ** -8 * np.abs(want[np.arange(N), tok]) + 2.0 ** -12 * g_max
+    ratio = np.abs(got - want) / tol
+    k, v = np.unravel_index(np.argmax(ratio), ratio.shape)
+    U.log(f"  max |err| / bound {ratio.max():.3f} at row {k}, column {v}")
+    assert ratio.max() <= 1.0
+    # the check is not vacuous: entries below fp16's normal range are present
+    p = np.abs(want) / np.maximum(g_max[:, None], 1e-300)
+    assert np.sum((p > 2.0 ** -24) & (p < 2.0 ** -14)) > 1000
 
 
 SHAPES = [(16, 16, 64), (100, 104, 64), (1000, 1008, 64), (4093, 4096, 32), (8192, 8192, 32),
@@ -304,9 +368,9 @@ def test_grpo_all_masked_and_empty():
 # ----------------------------------------------------------------------------
 # Full-size microbatches (sampled rows), in the benchmark's configuration
 # ----------------------------------------------------------------------------
-def _full_size_case(name, mb_index, seed):
+def _full_size_case(name, mb_index, seed, layout="packed"):
     import torch
-    lat, ro, mbs, tok_r, tok_t, A32 = _step_tokens(name)
+    lat, ro, mbs, tok_r, tok_t, A32 = _step_tokens(name, layout)
     mb = mbs[mb_index]
     V = lat.cfg["V"]
     N = mb.tok_rollout.size
@@ -327,23 +391,31 @@ def _full_size_case(name, mb_index, seed):
     return lg_dev, lg, tok, old, ref, adv.astype(np.float32), w.astype(np.float32), V, N
 
 
-@pytest.mark.parametrize("name,mb_index", [("mid", 0), ("mid", -1), ("full", 0)])
-def test_grpo_full_size_microbatch(name, mb_index):
+@pytest.mark.parametrize("name,mb_index,layout", [
+    ("mid", 0, "packed"), ("mid", -1, "packed"), ("full", 0, "packed"),
+    ("mid", 5, "right_padded"),  # three 2304-row slots and a 1280-row tail
+    ("full", -1, "right_padded"),  # one 11840-row slot holding the step's last sequence
+])
+def test_grpo_full_size_microbatch(name, mb_index, layout):
     import torch
-    seed = 4242 + (mb_index % 7)
-    lg_dev, lg, tok, old, ref, adv, w, V, N = _full_size_case(name, mb_index, seed)
+    seed = 4242 + (mb_index % 7) + (100 if layout != "packed" else 0)
+    lg_dev, lg, tok, old, ref, adv, w, V, N = _full_size_case(name, mb_index, seed, layout)
     valid = w != 0
     rng = np.random.default_rng(seed)
     sample = np.unique(np.concatenate([rng.choice(np.flatnonzero(valid), 24, replace=False),
                                        rng.choice(N, 8, replace=False), [0, N - 1]]))
     # (1) the configuration the benchmark runs: sample-level weights
-    U.log(f"{name}[{mb_index}] GPU run, default weights")
+    U.log(f"{name}[{mb_index}] {layout}: {int(valid.sum())} of {N} rows live; GPU run, default weights")
     gpu = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, **KW)
     U.log("oracle over every row (log-probs and loss)")
     o = oracle.grpo_rows(lg, tok, old, ref, adv, w, want_dlogits=False, **KW)
     _check_rows(gpu, o, valid, name)
     U.check_dlogits(U.dl_rows(gpu["dl_dev"], sample, V), lg, sample, tok, old, ref, adv, w, V,
                     atol=1e-2, kw=KW, rel_to_max=True)
+    # every excluded row (feedback, slot and tail padding) is written as zeros
+    masked = torch.as_tensor(np.flatnonzero(~valid), device=lg_dev.device)
+    if masked.numel():
+        assert int(gpu["dl_dev"].index_select(0, masked).view(torch.int16).abs().max().item()) == 0
     del gpu
     torch.cuda.empty_cache()
     # (2) unit weights, where a 2e-2 absolute bound on dlogits is meaningful

@@ -109,3 +109,34 @@ def test_bf16_round_trip_and_rounding():
     t = np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8], np.float32)
     np.testing.assert_array_equal(wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(t)),
                                   np.array([1.0, 1.0 + 2.0 ** -6], np.float32))
+
+
+@pytest.mark.parametrize("name", ["mid", "full"])
+def test_right_padded_layout(name):
+    """Right-padded microbatches hold the same generated rows as the packed
+    layout, each sequence at the start of its own slot with the slot's tail
+    and the microbatch's tail excluded."""
+    lat, gate, ro = _gated(name)
+    R = lat.cfg["rows_per_mb"]
+    packed = wl.pack(ro, R)
+    rp = wl.pack_right_padded(ro, R)
+    seq_len = np.array([wl._sequence(ro, i)[0].size for i in range(ro.n_rollouts)])
+    slot = (seq_len.max() + 63) // 64 * 64
+    per_mb = R // slot
+    assert len(rp) == -(-ro.n_rollouts // per_mb)
+    assert sum(m.n_valid for m in rp) == sum(m.n_valid for m in packed) == int(ro.n_tokens.sum())
+    for b, m in enumerate(rp):
+        assert m.tok_rollout.size == R and m.first_row == b * R
+        assert np.all(m.tok_rollout[per_mb * slot:] == -1)
+        for j in range(per_mb):
+            i = b * per_mb + j
+            cell = m.tok_rollout[j * slot:(j + 1) * slot]
+            if i >= ro.n_rollouts:
+                assert np.all(cell == -1)
+                continue
+            r, t = wl._sequence(ro, i)
+            np.testing.assert_array_equal(cell[:r.size], r)
+            np.testing.assert_array_equal(m.tok_turn[j * slot:j * slot + r.size], t)
+            assert np.all(cell[r.size:] == -1)
+    if name == "mid":
+        assert slot == 2304 and per_mb == 3 and len(rp) == 86

@@ -14,7 +14,8 @@ five shapes this library is measured on):
 * ``tiny``   -- 2 prompts x G=8, one turn of 128 tokens (2048 rows), V=32768.
 * ``mid``    -- 16 prompts x G=16, up to 2 turns of U[256,1024] tokens with
   U[64,512] masked environment-feedback rows between turns, V=151936,
-  packed into 8192-row microbatches (tail padding masked).
+  packed into 8192-row microbatches (tail padding masked); a second,
+  right-padded layout puts every sequence in a fixed-length slot.
 * ``full``   -- 64 prompts x G=16, up to 3 turns of U[512,4096] tokens,
   V=151936, 16384-row microbatches.
 * ``stress`` -- 4096 groups x G=64, M=3, outcome tuples with many ties
@@ -173,6 +174,49 @@ def stress_token_counts(lat: Latent, seed: int | None = None) -> np.ndarray:
     return rng.integers(200, 8001, size=lat.turn_pass.shape[0]).astype(np.int32)
 
 
+def _sequence(ro: Rollouts, i: int):
+    """Rows of rollout i's sequence: turn 0, then for each later turn its
+    environment-feedback rows (excluded, -1) followed by its generated rows.
+    Returns (rollout index per row, turn per row)."""
+    segs_r, segs_t = [], []
+    for t in range(int(ro.n_turns[i])):
+        fb = int(ro.fb_len[i, t])
+        if fb:
+            segs_r.append(np.full(fb, -1, np.int32))
+            segs_t.append(np.zeros(fb, np.int32))
+        ln = int(ro.turn_len[i, t])
+        segs_r.append(np.full(ln, i, np.int32))
+        segs_t.append(np.full(ln, t, np.int32))
+    return np.concatenate(segs_r), np.concatenate(segs_t)
+
+
+def pack_right_padded(ro: Rollouts, rows_per_mb: int, slot_rows: int | None = None
+                      ) -> list[Microbatch]:
+    """Right-padded layout: each rollout's sequence starts a slot of
+    ``slot_rows`` rows (default: the step's longest sequence rounded up to a
+    multiple of 64) and the rest of the slot is excluded padding; a
+    microbatch of ``rows_per_mb`` rows holds floor(rows_per_mb / slot_rows)
+    slots in rollout order, and its rows past the last slot are excluded
+    too.  ``first_row`` is the microbatch's first row in the step."""
+    seqs = [_sequence(ro, i) for i in range(ro.n_rollouts)]
+    if slot_rows is None:
+        longest = max((r.size for r, _ in seqs), default=1)
+        slot_rows = (longest + 63) // 64 * 64
+    assert 0 < slot_rows <= rows_per_mb, "slot longer than a microbatch"
+    per_mb = rows_per_mb // slot_rows
+    mbs: list[Microbatch] = []
+    for m0 in range(0, len(seqs), per_mb):
+        tr = np.full(rows_per_mb, -1, np.int32)
+        tt = np.zeros(rows_per_mb, np.int32)
+        for j, (r, t) in enumerate(seqs[m0:m0 + per_mb]):
+            assert r.size <= slot_rows, "sequence longer than its slot"
+            tr[j * slot_rows: j * slot_rows + r.size] = r
+            tt[j * slot_rows: j * slot_rows + t.size] = t
+        mbs.append(Microbatch(tok_rollout=tr, tok_turn=tt, first_row=len(mbs) * rows_per_mb,
+                              n_valid=int((tr >= 0).sum())))
+    return mbs
+
+
 def pack(ro: Rollouts, rows_per_mb: int) -> list[Microbatch]:
     """Pack whole rollout sequences, in rollout order, into microbatches of
     ``rows_per_mb`` rows.  A sequence is turn 0, then for each later turn its
@@ -199,17 +243,7 @@ def pack(ro: Rollouts, rows_per_mb: int) -> list[Microbatch]:
         cur_r, cur_t, used = [], [], 0
 
     for i in range(ro.n_rollouts):
-        segs_r, segs_t = [], []
-        for t in range(int(ro.n_turns[i])):
-            fb = int(ro.fb_len[i, t])
-            if fb:
-                segs_r.append(np.full(fb, -1, np.int32))
-                segs_t.append(np.zeros(fb, np.int32))
-            ln = int(ro.turn_len[i, t])
-            segs_r.append(np.full(ln, i, np.int32))
-            segs_t.append(np.full(ln, t, np.int32))
-        seq_r = np.concatenate(segs_r)
-        seq_t = np.concatenate(segs_t)
+        seq_r, seq_t = _sequence(ro, i)
         assert seq_r.size <= rows_per_mb, "sequence longer than a microbatch"
         if used + seq_r.size > rows_per_mb:
             flush()
