@@ -1,9 +1,6 @@
 """Benchmark of the LEAP GRPO hot path on one MI355X.
 
-One step = one pass of the whole hot path over one RL training step of the
-"mid" workload (16 prompts x G=16 rollouts, up to 2 turns of U[256,1024]
-generated tokens with masked environment-feedback rows between turns,
-vocabulary 151936, 8192-row microbatches):
+One step = one pass of the whole hot path over one RL training step:
 
   leap_dcp_gate                    first-turn outcomes -> multi-turn gate
   leap_rank_advantages             final outcomes -> tournament reward, advantage
@@ -11,9 +8,22 @@ vocabulary 151936, 8192-row microbatches):
   leap_grpo_logprob_loss_fwd_bwd   per microbatch: log-softmax, surrogate, KL,
                                    loss and bf16 dlogits
 
-Every input (all microbatches' bf16 logits included) is resident in HBM
-before the timed region; dlogits go to separate buffers, so every step sees
-the same inputs.  Prints one JSON line on stdout; progress goes to stderr.
+The headline workload is the "full" paper-shaped step: 64 prompts x G=16
+rollouts, up to 3 turns of U[512,4096] generated tokens with masked
+environment-feedback rows between turns, vocabulary 151936, 305 microbatches
+of 16384 rows (about 5 GB of bf16 logits each, 1.5 TB for the step).  The
+step's logits cannot all be resident, so three 16384-row logits buffers (and
+three dlogits buffers) are cycled: microbatch i reads buffer i mod 3 with its
+own rows' side inputs (token ids sampled from that buffer's logits, old /
+reference log-probs from them plus noise, and the token advantages and
+weights the step's own gate, tournament and token-advantage calls produce
+for the microbatch's rows, masked rows included).  The "mid" step (16 x 16,
+up to 2 turns, 38 microbatches of 8192 rows) runs as a secondary leg with
+every microbatch's logits resident.
+
+Every input is resident in HBM before a timed region; dlogits go to separate
+buffers, so every step sees the same inputs.  Prints one JSON line on
+stdout; progress goes to stderr.
 """
 from __future__ import annotations
 
@@ -69,7 +79,10 @@ def row_bytes(V: int, valid: bool) -> int:
     return 4 * V + 28 if valid else 2 * V + 16
 
 
-def build_step(L, torch, dev, name, seed):
+def build_step(L, torch, dev, name, seed, n_buffers=None):
+    """The step's rollouts, gate, layout and inputs.  ``n_buffers`` logits
+    buffers of one microbatch each are generated (default: one per
+    microbatch, all resident); microbatch i reads buffer i mod n_buffers."""
     import workloads as wl
     lat = wl.draw_latent(name)
     cfg = lat.cfg
@@ -82,15 +95,18 @@ def build_step(L, torch, dev, name, seed):
     ro = wl.realize(lat, gate_d.cpu().numpy())
     mbs = wl.pack(ro, R)
     n_mb = len(mbs)
+    n_buf = n_mb if n_buffers is None else min(n_buffers, n_mb)
     rows = n_mb * R
     tok_r = np.concatenate([m.tok_rollout for m in mbs])
     tok_t = np.concatenate([m.tok_turn for m in mbs])
     valid = tok_r >= 0
     log(f"[bench] workload {name}: {ro.n_rollouts} rollouts, {n_mb} microbatches x {R} rows, "
-        f"{int(valid.sum())} generated tokens, V={V}; logits {rows * V * 2 / 1e9:.1f} GB")
+        f"{int(valid.sum())} generated tokens, V={V}; {n_buf} resident logits buffers "
+        f"({n_buf * R * V * 2 / 1e9:.1f} GB)")
 
-    s = {"lat": lat, "ro": ro, "mbs": mbs, "V": V, "R": R, "rows": rows, "n_mb": n_mb,
-         "G": G, "M": M, "tau": (tmin, tmax), "valid": valid, "gamma": cfg["gamma"]}
+    s = {"name": name, "lat": lat, "ro": ro, "mbs": mbs, "V": V, "R": R, "rows": rows,
+         "n_mb": n_mb, "n_buf": n_buf, "G": G, "M": M, "tau": (tmin, tmax), "valid": valid,
+         "gamma": cfg["gamma"]}
     s["ftp"] = ftp_d
     s["gate"] = gate_d
     s["n_fail"] = nf_d
@@ -105,34 +121,44 @@ def build_step(L, torch, dev, name, seed):
     s["adv_tok"] = torch.empty(rows, dtype=torch.float32, device=dev)
     s["w_tok"] = torch.empty(rows, dtype=torch.float32, device=dev)
 
-    # every microbatch's logits, resident; dlogits in separate buffers
+    # the logits buffers, resident; dlogits in separate buffers
     t0 = time.time()
-    s["logits"] = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
-    s["dlogits"] = torch.empty((rows, V), dtype=torch.bfloat16, device=dev)
-    tok = torch.empty(rows, dtype=torch.int32, device=dev)
-    for i in range(n_mb):
-        sl = slice(i * R, (i + 1) * R)
-        wl.logits_device(seed + i, R, V, device=dev, out=s["logits"][sl])
-        tok[sl] = wl.sample_tokens_device(s["logits"][sl], V, seed + i)
-    s["tok"] = tok
+    s["logits"] = torch.empty((n_buf * R, V), dtype=torch.bfloat16, device=dev)
+    s["dlogits"] = torch.empty((n_buf * R, V), dtype=torch.bfloat16, device=dev)
+    tok_buf = torch.empty(n_buf * R, dtype=torch.int32, device=dev)
+    for b in range(n_buf):
+        sl = slice(b * R, (b + 1) * R)
+        wl.logits_device(seed + b, R, V, device=dev, out=s["logits"][sl])
+        tok_buf[sl] = wl.sample_tokens_device(s["logits"][sl], V, seed + b)
     torch.cuda.synchronize()
     log(f"[bench] logits and sampled tokens ready in {time.time() - t0:.1f} s")
 
-    # current log-probs from the library's forward-only pass, then
-    # old / reference = current + N(0, 0.05^2) / N(0, 0.1^2)
-    cur = torch.empty(rows, dtype=torch.float32, device=dev)
-    L.leap_logprob_fwd(s["logits"], V, rows, V, tok, None, 1.0, cur)
+    # current log-probs from the library's forward-only pass, then, per row
+    # of the step, old / reference = current + N(0, 0.05^2) / N(0, 0.1^2)
+    cur_buf = torch.empty(n_buf * R, dtype=torch.float32, device=dev)
+    L.leap_logprob_fwd(s["logits"], V, n_buf * R, V, tok_buf, None, 1.0, cur_buf)
+    reps = -(-n_mb // n_buf)
+    s["tok"] = tok_buf.view(n_buf, R).repeat(reps, 1)[:n_mb].reshape(-1).contiguous()
+    cur = cur_buf.view(n_buf, R).repeat(reps, 1)[:n_mb].reshape(-1)
+    n_old, n_ref = wl.logp_noise(seed, rows)
+    s["old"] = (cur + torch.from_numpy(n_old.astype(np.float32)).to(dev)).contiguous()
+    s["ref"] = (cur + torch.from_numpy(n_ref.astype(np.float32)).to(dev)).contiguous()
+    del cur, cur_buf, tok_buf
     ws_bytes = L.leap_grpo_workspace_size(R, V)
     s["ws"] = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     s["ws_bytes"] = ws_bytes
     s["loss"] = torch.empty(n_mb, dtype=torch.float32, device=dev)
-    n_old, n_ref = wl.logp_noise(seed, rows)
-    s["old"] = cur + torch.from_numpy(n_old.astype(np.float32)).to(dev)
-    s["ref"] = cur + torch.from_numpy(n_ref.astype(np.float32)).to(dev)
     s["err"] = torch.zeros(1, dtype=torch.int32, device=dev)
     s["params"] = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
     torch.cuda.synchronize()
     return s
+
+
+def mb_logits(s, i):
+    """(logits, dlogits) buffers microbatch i reads and writes."""
+    R = s["R"]
+    b = i % s["n_buf"]
+    return s["logits"][b * R:(b + 1) * R], s["dlogits"][b * R:(b + 1) * R]
 
 
 def run_step(L, s, events=None):
@@ -151,14 +177,15 @@ def run_step(L, s, events=None):
     stream = torch.cuda.current_stream()
     for i in range(s["n_mb"]):
         sl = slice(i * R, (i + 1) * R)
+        lg, dl = mb_logits(s, i)
         if events is not None:
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-        L.leap_grpo_logprob_loss_fwd_bwd(s["logits"][sl], V, R, V, s["tok"][sl], s["old"][sl],
+        L.leap_grpo_logprob_loss_fwd_bwd(lg, V, R, V, s["tok"][sl], s["old"][sl],
                                          s["ref"][sl], s["adv_tok"][sl], s["w_tok"][sl],
                                          s["params"], None, None, None, s["loss"][i:i + 1],
-                                         s["dlogits"][sl], s["ws"], s["ws_bytes"], s["err"])
+                                         dl, s["ws"], s["ws_bytes"], s["err"])
         if events is not None:
             e1.record(stream)
             events.append((e0, e1))
@@ -211,71 +238,79 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(s, seconds: float):
+def _oracle_rows_inputs(s, rows):
+    """Host copies of the given step rows' inputs: bf16 logits (from the
+    buffer each row's microbatch reads), token ids, old / reference log-probs."""
+    import torch
+    R, nb = s["R"], s["n_buf"]
+    brow = (rows // R) % nb * R + rows % R
+    dev = s["logits"].device
+    lg = s["logits"].index_select(0, torch.as_tensor(brow, device=dev))
+    idx = torch.as_tensor(rows, device=dev)
+    return (lg.view(torch.int16).cpu().numpy().view(np.uint16), s["tok"][idx].cpu().numpy(),
+            s["old"][idx].cpu().numpy(), s["ref"][idx].cpu().numpy())
+
+
+def cpu_baseline(s, seconds: float, samples: int = 3):
     """The fp64 oracle (as it is) on the host cores over a bounded sample of
     the same step: the tournament, gate and token advantages over the whole
-    step, then fused rows of microbatch 0 until `seconds` have passed."""
-    import torch
-
+    step, then the fused objective with dlogits on generated-token rows of
+    the step for about seconds / samples each, `samples` times (different
+    rows each time); the whole-step time at the median per-row rate.  Then
+    the same on one thread over a shorter sample."""
     import oracle
-    ro, lat, V, R = s["ro"], s["lat"], s["V"], s["R"]
+    ro, lat = s["ro"], s["lat"]
     cores = oracle.get_threads()
-    t0 = time.perf_counter()
-    nf, gate = oracle.dcp_gate(lat.first_turn_pass, s["G"], *s["tau"])
-    rk = oracle.rank_tournament(ro.pass_turn, s["G"], s["M"], eps=float(np.float32(1e-6)))
     tok_r = s["tok_r"].cpu().numpy()
     tok_t = s["tok_t"].cpu().numpy()
-    adv, w, _ = oracle.token_advantages(rk["A"], tok_r, tok_t, ro.n_turns, ro.n_tokens,
-                                        s["gamma"], oracle.AGG_SEQ_MEAN_TOKEN_MEAN,
-                                        float(ro.n_rollouts))
-    t_small = time.perf_counter() - t0
-    valid_rows = np.flatnonzero(w != 0)  # generated-token rows of the whole step
-    chunk = 4 * cores
-    done = 0
-    t_rows = 0.0  # oracle time only; device->host copies of the sample are excluded
-    while done < valid_rows.size and t_rows < seconds:
-        rows = valid_rows[done:done + chunk]
-        idx = torch.as_tensor(rows, device=s["logits"].device)
-        lg = s["logits"].index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)
-        tok = s["tok"][idx].cpu().numpy()
-        old = s["old"][idx].cpu().numpy()
-        ref = s["ref"][idx].cpu().numpy()
-        tc = time.perf_counter()
-        oracle.grpo_rows(lg, tok, old, ref, adv[rows], w[rows])
-        t_rows += time.perf_counter() - tc
-        done += rows.size
-    n_valid = int(s["valid"].sum())
-    # whole-step time at the measured per-row rate, plus the small steps
-    step_time = t_small + t_rows / max(done, 1) * n_valid
 
-    # the same on one thread, over a shorter sample of the same rows
-    oracle.set_threads(1)
-    try:
+    def small_steps():
         t0 = time.perf_counter()
         oracle.dcp_gate(lat.first_turn_pass, s["G"], *s["tau"])
-        rk1 = oracle.rank_tournament(ro.pass_turn, s["G"], s["M"], eps=float(np.float32(1e-6)))
-        oracle.token_advantages(rk1["A"], tok_r, tok_t, ro.n_turns, ro.n_tokens, s["gamma"],
-                                oracle.AGG_SEQ_MEAN_TOKEN_MEAN, float(ro.n_rollouts))
-        t_small1 = time.perf_counter() - t0
-        done1, t_rows1 = 0, 0.0
-        while done1 < done and t_rows1 < seconds / 3:
-            rows = valid_rows[done1:done1 + 8]
-            idx = torch.as_tensor(rows, device=s["logits"].device)
-            lg = s["logits"].index_select(0, idx).view(torch.int16).cpu().numpy().view(np.uint16)
-            tok = s["tok"][idx].cpu().numpy()
-            old = s["old"][idx].cpu().numpy()
-            ref = s["ref"][idx].cpu().numpy()
+        rk = oracle.rank_tournament(ro.pass_turn, s["G"], s["M"], eps=float(np.float32(1e-6)))
+        adv, w, _ = oracle.token_advantages(rk["A"], tok_r, tok_t, ro.n_turns, ro.n_tokens,
+                                            s["gamma"], oracle.AGG_SEQ_MEAN_TOKEN_MEAN,
+                                            float(ro.n_rollouts))
+        return time.perf_counter() - t0, adv, w
+
+    t_small, adv, w = small_steps()
+    valid_rows = np.flatnonzero(w != 0)  # generated-token rows of the whole step
+    n_valid = valid_rows.size
+
+    def row_rate(start, budget, chunk):
+        """Oracle seconds per row over rows from `start` until `budget` s
+        of oracle time (device->host copies of the sample excluded)."""
+        done, t = 0, 0.0
+        while t < budget and start + done < n_valid:
+            rows = valid_rows[start + done:start + done + chunk]
+            lg, tok, old, ref = _oracle_rows_inputs(s, rows)
             tc = time.perf_counter()
             oracle.grpo_rows(lg, tok, old, ref, adv[rows], w[rows])
-            t_rows1 += time.perf_counter() - tc
-            done1 += rows.size
+            t += time.perf_counter() - tc
+            done += rows.size
+        return t / max(done, 1), done, t
+
+    rates = []
+    start = 0
+    for _ in range(samples):
+        r, done, t = row_rate(start, seconds / samples, 4 * cores)
+        rates.append((r, done, t))
+        start += done
+    per_row = float(np.median([r for r, _, _ in rates]))
+    step_time = t_small + per_row * n_valid
+
+    oracle.set_threads(1)
+    try:
+        t_small1, _, _ = small_steps()
+        per_row1, done1, t_rows1 = row_rate(0, seconds / 4, 8)
     finally:
         oracle.set_threads(cores)
-    step_time1 = t_small1 + t_rows1 / max(done1, 1) * n_valid
+    step_time1 = t_small1 + per_row1 * n_valid
     return {"value": n_valid / step_time, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s) and "
-                      f"the fused objective with dlogits on the first {done} generated-token rows "
-                      f"({t_rows:.1f} s), scaled to the step's {n_valid} tokens",
+            "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s), "
+                      f"then the fused objective with dlogits on {samples} samples of "
+                      f"generated-token rows ({', '.join(f'{d} rows in {t:.1f} s' for _, d, t in rates)}); "
+                      f"median per-row rate scaled to the step's {n_valid} tokens",
             "cpu_model": _cpu_model(), "nproc": os.cpu_count(),
             "value_1_thread": n_valid / step_time1,
             "sample_1_thread": f"the same on one thread: small steps {t_small1:.2f} s, fused "
@@ -671,21 +706,103 @@ def blas_reference(torch, dev):
     return out
 
 
+def time_step(L, torch, s, steps: int, warmup: int) -> dict:
+    """`warmup` untimed steps, then exactly `steps` timed steps between two
+    device synchronisations (host clock), with HIP events on the launch
+    stream around every fused call.  Rates use the step's algorithmic bytes
+    (row_bytes per row of each microbatch)."""
+    log(f"[bench] {s['name']}: warmup {warmup} steps")
+    for _ in range(warmup):
+        run_step(L, s)
+    torch.cuda.synchronize()
+    assert int(s["err"].item()) == 0, "data errors reported by the kernels"
+    events = []
+    log(f"[bench] {s['name']}: timing {steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run_step(L, s, events)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    V, R = s["V"], s["R"]
+    k4_ms = np.array([a.elapsed_time(b) for a, b in events])
+    mb_bytes = np.array([m.n_valid * row_bytes(V, True) + (R - m.n_valid) * row_bytes(V, False)
+                         for m in s["mbs"]], np.float64)
+    bytes_per_launch = float(mb_bytes.mean())
+    k4_avg_s = float(k4_ms.mean()) / 1e3
+    achieved = bytes_per_launch / k4_avg_s
+    n_valid = int(s["valid"].sum())
+    out = {"value": n_valid * steps / elapsed, "ms_per_step": elapsed / steps * 1e3,
+           "k4_avg_s": k4_avg_s, "k4_median_us": float(np.median(k4_ms)) * 1e3,
+           "achieved": achieved, "bytes_per_launch": bytes_per_launch,
+           "step_bytes": float(mb_bytes.sum()), "n_valid": n_valid,
+           "masked_row_fraction": 1.0 - n_valid / s["rows"]}
+    log(f"[bench] {s['name']}: {out['ms_per_step']:.3f} ms/step; fused call {k4_avg_s * 1e6:.1f} us "
+        f"avg over {len(k4_ms)} launches (median {out['k4_median_us']:.1f}); "
+        f"{achieved / 1e9:.0f} GB/s algorithmic = {achieved / HBM_PEAK:.3f} of 8 TB/s")
+    return out
+
+
+def all_live_leg(L, torch, s, reps: int = 20):
+    """The fused call on microbatch 0's logits with every row live (weight
+    1/R, the microbatch's own advantages): the pure 1:1 read / write pattern,
+    without the write-only masked rows of the real layout."""
+    V, R = s["V"], s["R"]
+    lg, dl = mb_logits(s, 0)
+    w = torch.full((R,), 1.0 / R, dtype=torch.float32, device=lg.device)
+    stream = torch.cuda.current_stream()
+
+    def call():
+        L.leap_grpo_logprob_loss_fwd_bwd(lg, V, R, V, s["tok"][:R], s["old"][:R], s["ref"][:R],
+                                         s["adv_tok"][:R], w, s["params"], None, None, None,
+                                         s["loss"][:1], dl, s["ws"], s["ws_bytes"], s["err"])
+
+    settle(torch, call)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps / 1e3
+    nbytes = R * row_bytes(V, True)
+    log(f"[bench] fused call, every row live ({R} x {V}): {t * 1e6:.1f} us, "
+        f"{nbytes / t / 1e9:.0f} GB/s = {nbytes / t / HBM_PEAK:.3f} of 8 TB/s")
+    return {"workload": f"fused call on microbatch 0's logits ({R} x {V}), every row live",
+            "call_us": t * 1e6, "GBps": nbytes / t / 1e9, "frac": nbytes / t / HBM_PEAK,
+            "bytes_per_call": nbytes}
+
+
+WORKLOAD_TEXT = {
+    "full": "full: 64 prompts x G=16, up to 3 turns, U[512,4096] tokens/turn with U[64,512] "
+            "masked feedback rows between turns, V={V}, {n_mb} microbatches x {R} rows "
+            "(3 resident 16384-row logits buffers cycled through the step's per-microbatch "
+            "side inputs)",
+    "mid": "mid: 16 prompts x G=16, up to 2 turns, U[256,1024] tokens/turn with U[64,512] "
+           "masked feedback rows between turns, V={V}, {n_mb} microbatches x {R} rows (every "
+           "microbatch's logits resident)",
+}
+SEEDS = {"full": 1003, "mid": 1002}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    # ~3 s of the real step: a fresh device settles its clocks over the first
-    # seconds of sustained traffic (the first process on a new box measured
-    # ~5% slower with 3 warm-up steps)
-    ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="mid", choices=["mid", "full"])
-    ap.add_argument("--seed", type=int, default=1002)
+    # one full step is ~0.5 s of HBM traffic: 10 timed steps
+    ap.add_argument("--steps", type=int, default=10)
+    # ~3 s of the real step first: a fresh device settles its clocks over the
+    # first seconds of sustained traffic
+    ap.add_argument("--warmup", type=int, default=6)
+    ap.add_argument("--workload", default="full", choices=["full", "mid"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lmhead-reps", type=int, default=5,
                     help="timed calls of the fused LM-head variant (0 skips it)")
     ap.add_argument("--no-shard", action="store_true", help="skip the vocabulary-shard leg")
+    ap.add_argument("--no-mid", action="store_true", help="skip the secondary mid-step leg")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="only the headline step (for profiling its kernel)")
     ap.add_argument("--lmhead-only", action="store_true",
                     help="run only the fused LM-head leg and print its JSON object")
     ap.add_argument("--blas-reference", action="store_true",
@@ -704,8 +821,6 @@ def main():
     L.lib()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    if args.workload == "full":
-        raise SystemExit("the full workload does not fit resident; bench runs 'mid'")
 
     if args.lmhead_only:
         out = {"lmhead": lmhead_leg(L, torch, dev, 1005, max(1, args.lmhead_reps))}
@@ -715,95 +830,78 @@ def main():
         return
 
     probe = hbm_probe(L, torch, dev)
-    log(f"[bench] HBM probe: " + ", ".join(f"{k} {v:.0f}" for k, v in probe.items()))
-    s = build_step(L, torch, dev, args.workload, args.seed)
+    log("[bench] HBM probe: " + ", ".join(f"{k} {v:.0f}" for k, v in probe.items()))
+    name = args.workload
+    s = build_step(L, torch, dev, name, SEEDS[name], n_buffers=3 if name == "full" else None)
     copy_probe(torch, dev)
-
-    log(f"[bench] warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        run_step(L, s)
-    torch.cuda.synchronize()
-    assert int(s["err"].item()) == 0, "data errors reported by the kernels"
-
-    events = []
-    log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run_step(L, s, events)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-
+    m = time_step(L, torch, s, args.steps, args.warmup)
     V, R = s["V"], s["R"]
-    k4_ms = np.array([a.elapsed_time(b) for a, b in events])
-    per_mb_bytes = []
-    for m in s["mbs"]:
-        nv = m.n_valid
-        per_mb_bytes.append(nv * row_bytes(V, True) + (R - nv) * row_bytes(V, False))
-    bytes_per_launch = float(np.mean(per_mb_bytes))
-    k4_avg_s = float(k4_ms.mean()) / 1e3
-    achieved = bytes_per_launch / k4_avg_s
-    n_valid = int(s["valid"].sum())
-    value = n_valid * args.steps / elapsed
-    log(f"[bench] {elapsed / args.steps * 1e3:.3f} ms/step; fused call {k4_avg_s * 1e6:.1f} us avg "
-        f"over {len(k4_ms)} launches; {achieved / 1e9:.0f} GB/s algorithmic")
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
-        if t.get("k4_source_sha256_16") == k4_source_hash() and t.get("workload") == args.workload:
+        if t.get("k4_source_sha256_16") == k4_source_hash() and t.get("workload") == name:
             traffic = t.get("bytes_per_launch")
 
+    legs = {}
     cpu = None
-    if not args.no_cpu_baseline:
-        log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
-        cpu = cpu_baseline(s, args.cpu_seconds)
-
-    shard = shard_leg(L, torch, s) if not args.no_shard else None
-    fwd = logprob_leg(L, torch, s)
-    ent = entropy_leg(L, torch, s)
-    small = small_leg(L, torch, s)
-    graph = graph_leg(L, torch, s, args.steps)
-    rstats = stats_leg(L, torch, s)
+    if not args.no_legs:
+        if not args.no_cpu_baseline:
+            log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
+            cpu = cpu_baseline(s, args.cpu_seconds)
+        legs["all_live"] = all_live_leg(L, torch, s)
+        legs["vocab_shard"] = shard_leg(L, torch, s) if not args.no_shard else None
+        legs["logprob_fwd"] = logprob_leg(L, torch, s)
+        legs["entropy"] = entropy_leg(L, torch, s)
+        legs["small_kernels"] = small_leg(L, torch, s)
+        legs["graph_replay"] = graph_leg(L, torch, s, max(2, args.steps // 2))
+        legs["rollout_stats"] = stats_leg(L, torch, s)
     meta = {k: s[k] for k in ("n_mb", "rows", "G", "M")}
-    lm = None
-    if args.lmhead_reps > 0:
-        del s
+    del s
+    torch.cuda.empty_cache()
+    if not args.no_legs and not args.no_mid and name != "mid":
+        sm = build_step(L, torch, dev, "mid", SEEDS["mid"])
+        mm = time_step(L, torch, sm, 20, 30)
+        legs["mid_step"] = {
+            "workload": WORKLOAD_TEXT["mid"].format(V=sm["V"], n_mb=sm["n_mb"], R=sm["R"]),
+            "value": mm["value"], "unit": "tokens/s", "ms_per_step": mm["ms_per_step"],
+            "steps": 20, "warmup": 30, "generated_tokens_per_step": mm["n_valid"],
+            "masked_row_fraction": mm["masked_row_fraction"],
+            "fused_call_avg_us": mm["k4_avg_s"] * 1e6, "fused_call_median_us": mm["k4_median_us"],
+            "achieved_GBps": mm["achieved"] / 1e9, "frac": mm["achieved"] / HBM_PEAK}
+        del sm
         torch.cuda.empty_cache()
+    lm = None
+    if args.lmhead_reps > 0 and not args.no_legs:
         lm = lmhead_leg(L, torch, dev, 1005, args.lmhead_reps)
 
     out = {
         "metric": "rollout tokens/sec for fused GRPO logprob+loss+dlogits; % of HBM roofline",
-        "value": value,
+        "value": m["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": elapsed / args.steps * 1e3,
+        "ms_per_step": m["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: 16 prompts x G=16, up to 2 turns, "
-                               f"U[256,1024] tokens/turn, V={V}, {meta['n_mb']} microbatches x {R} rows",
-                   "generated_tokens_per_step": n_valid, "rows_per_step": meta["rows"],
+        "config": {"workload": WORKLOAD_TEXT[name].format(V=V, n_mb=meta["n_mb"], R=R),
+                   "generated_tokens_per_step": m["n_valid"], "rows_per_step": meta["rows"],
+                   "masked_row_fraction": m["masked_row_fraction"],
                    "vocab": V, "microbatch_rows": R, "G": meta["G"], "max_turns": meta["M"]},
-        "roofline": {"bound": "hbm", "achieved": achieved / 1e9, "peak": HBM_PEAK / 1e9,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK, "traffic": traffic,
+        "roofline": {"bound": "hbm", "achieved": m["achieved"] / 1e9, "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": m["achieved"] / HBM_PEAK, "traffic": traffic,
                      "kernel": "grpo_rows_resident<1024,19,16,false> + loss_reduce (one fused call)",
-                     "avg_launch_us": k4_avg_s * 1e6, "bytes_per_launch": bytes_per_launch,
-                     "probe_GBps": probe,
-                     "frac_of_probe_copy": achieved / 1e9 / probe["copy_GBps"]},
+                     "avg_launch_us": m["k4_avg_s"] * 1e6, "median_launch_us": m["k4_median_us"],
+                     "bytes_per_launch": m["bytes_per_launch"], "probe_GBps": probe,
+                     "frac_of_probe_copy": m["achieved"] / 1e9 / probe["copy_GBps"]},
         "cpu_baseline": cpu,
         "lmhead": lm,
-        "vocab_shard": shard,
-        "logprob_fwd": fwd,
-        "entropy": ent,
-        "small_kernels": small,
-        "graph_replay": graph,
-        "rollout_stats": rstats,
     }
+    out.update(legs)
     print(json.dumps(out), flush=True)
 
 
