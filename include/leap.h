@@ -239,6 +239,35 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
                                            size_t ws_bytes, int32_t *dev_err,
                                            hipStream_t stream);
 
+/* Largest N that leap_grpo_logprob_loss_fwd_bwd_noalloc accepts. */
+#define LEAP_NOALLOC_MAX_ROWS 1048576
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * call as leap_grpo_logprob_loss_fwd_bwd (same kernels, same results bit for
+ * bit, same argument rules) without the workspace arguments.  Its per-row
+ * scratch is a library-owned device array of LEAP_NOALLOC_MAX_ROWS floats
+ * (4 MiB) per device, held until the process ends; the call itself
+ * allocates and frees nothing.  The first call on a device looks up that
+ * device's array (the device must be current).
+ * All calls on one device share its array: calls that may overlap on one
+ * device (unordered streams) race and must be serialised by the caller.
+ * Errors: as leap_grpo_logprob_loss_fwd_bwd, plus LEAP_ERR_UNSUPPORTED for
+ * N > LEAP_NOALLOC_MAX_ROWS (or a device index of 64 or more), and
+ * LEAP_ERR_HIP if the device array cannot be found.
+ */
+leap_status leap_grpo_logprob_loss_fwd_bwd_noalloc(const void *logits_bf16, int64_t ld,
+                                                   int64_t N, int32_t V,
+                                                   const int32_t *token_ids,
+                                                   const float *old_logp, const float *ref_logp,
+                                                   const float *adv_tok, const float *w_tok,
+                                                   const leap_grpo_params *params,
+                                                   float *logp_out, float *tok_loss_out,
+                                                   float *entropy_out, float *loss_out,
+                                                   void *dlogits_bf16, int32_t *dev_err,
+                                                   hipStream_t stream);
+
 /*
  * Forward-only log-probability of each row's token: the old-policy and
  * reference forward passes whose outputs enter the ratio and the KL term of

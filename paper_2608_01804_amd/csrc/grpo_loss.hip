@@ -31,6 +31,8 @@
 // Optional output: each row's entropy H = -sum_v p_v ln p_v (nats), from a
 // third accumulator t = sum 2^d * d beside the sum-exp (the ENT variants;
 // without it the kernels are unchanged).
+#include <mutex>
+
 #include "objective.h"
 #include "row_common.h"
 
@@ -360,13 +362,16 @@ LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
     return (b + 255) & ~static_cast<size_t>(255);
 }
 
-LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
-    const void* logits_bf16, int64_t ld, int64_t N, int32_t V, const int32_t* token_ids,
-    const float* old_logp, const float* ref_logp, const float* adv_tok, const float* w_tok,
-    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
-    float* loss_out, void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err,
-    hipStream_t stream) {
-    using namespace leap;
+namespace leap {
+namespace {
+
+// Host-side checks of the fused call's arguments (everything but the
+// workspace).
+leap_status check_fused_args(const void* logits_bf16, int64_t ld, int64_t N, int32_t V,
+                             const int32_t* token_ids, const float* old_logp,
+                             const float* ref_logp, const float* adv_tok, const float* w_tok,
+                             const leap_grpo_params* params, const float* loss_out,
+                             const void* dlogits_bf16) {
     if (N < 0 || V < 1 || ld < V || !params || !loss_out) return LEAP_ERR_INVALID_ARG;
     const leap_grpo_params& pp = *params;
     if (!(pp.clip_eps_low >= 0.0f) || !(pp.clip_eps_high >= 0.0f) || !(pp.kl_coef >= 0.0f) ||
@@ -389,12 +394,19 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
         const uintptr_t bytes = static_cast<uintptr_t>(N) * static_cast<uintptr_t>(ld) * 2u;
         if (a0 != b0 && a0 < b0 + bytes && b0 < a0 + bytes) return LEAP_ERR_INVALID_ARG;
     }
-    if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
-    if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
+    return LEAP_OK;
+}
 
-    const leap::LaunchCheck lc;
+// The row kernel, then the fixed-order loss sum, with the per-row weighted
+// losses in row_loss (N floats).
+leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t V,
+                         const int32_t* token_ids, const float* old_logp, const float* ref_logp,
+                         const float* adv_tok, const float* w_tok, const leap_grpo_params& pp,
+                         float* logp_out, float* tok_loss_out, float* entropy_out, float* loss_out,
+                         void* dlogits_bf16, float* row_loss, int32_t* dev_err,
+                         hipStream_t stream) {
+    const LaunchCheck lc;
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
-    float* row_loss = static_cast<float*>(workspace);
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
         hipLaunchKernelGGL(entropy_out ? rc.fn_ent : rc.fn, dim3(static_cast<unsigned>(N)),
@@ -408,4 +420,70 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(kReduceBlock), 0, stream, row_loss, N,
                        loss_out);
     return lc.status();
+}
+
+// Per-row loss scratch of the no-allocation entry point: one array per
+// device, held from the library's load until the process ends.  Every call
+// on a device reuses it, so calls that overlap on one device (different
+// streams without ordering) race on it.  Nothing needs clearing: the row
+// kernel writes all N entries before the loss sum reads them.
+static __device__ __align__(256) float scratch[LEAP_NOALLOC_MAX_ROWS];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device with that device current.  (The host-side name of the array is
+// only a stand-in handle; kernels must receive this address.)
+leap_status scratch_for_current_device(float** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return LEAP_ERR_HIP;
+    if (dev >= kMaxDevices) return LEAP_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return LEAP_ERR_HIP;
+        g_scratch_ptr[dev] = static_cast<float*>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return LEAP_OK;
+}
+
+}  // namespace
+}  // namespace leap
+
+LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
+    const void* logits_bf16, int64_t ld, int64_t N, int32_t V, const int32_t* token_ids,
+    const float* old_logp, const float* ref_logp, const float* adv_tok, const float* w_tok,
+    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
+    float* loss_out, void* dlogits_bf16, void* workspace, size_t ws_bytes, int32_t* dev_err,
+    hipStream_t stream) {
+    using namespace leap;
+    const leap_status st = check_fused_args(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp,
+                                            adv_tok, w_tok, params, loss_out, dlogits_bf16);
+    if (st != LEAP_OK) return st;
+    if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
+    return launch_fused(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
+                        *params, logp_out, tok_loss_out, entropy_out, loss_out, dlogits_bf16,
+                        static_cast<float*>(workspace), dev_err, stream);
+}
+
+LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd_noalloc(
+    const void* logits_bf16, int64_t ld, int64_t N, int32_t V, const int32_t* token_ids,
+    const float* old_logp, const float* ref_logp, const float* adv_tok, const float* w_tok,
+    const leap_grpo_params* params, float* logp_out, float* tok_loss_out, float* entropy_out,
+    float* loss_out, void* dlogits_bf16, int32_t* dev_err, hipStream_t stream) {
+    using namespace leap;
+    leap_status st = check_fused_args(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp,
+                                      adv_tok, w_tok, params, loss_out, dlogits_bf16);
+    if (st != LEAP_OK) return st;
+    if (N > LEAP_NOALLOC_MAX_ROWS) return LEAP_ERR_UNSUPPORTED;
+    float* row_loss = nullptr;
+    if ((st = scratch_for_current_device(&row_loss)) != LEAP_OK) return st;
+    return launch_fused(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
+                        *params, logp_out, tok_loss_out, entropy_out, loss_out, dlogits_bf16,
+                        row_loss, dev_err, stream);
 }

@@ -36,6 +36,7 @@ EXPORTED = (
     "leap_token_advantages",
     "leap_grpo_workspace_size",
     "leap_grpo_logprob_loss_fwd_bwd",
+    "leap_grpo_logprob_loss_fwd_bwd_noalloc",
     "leap_logprob_fwd",
     "leap_lmhead_workspace_size",
     "leap_grpo_lmhead_fwd_bwd",
@@ -96,6 +97,10 @@ def lib() -> ctypes.CDLL:
     L.leap_grpo_logprob_loss_fwd_bwd.argtypes = [P, i64, i64, i32, P, P, P, P, P,
                                                  ctypes.POINTER(leap_grpo_params), P, P, P, P,
                                                  P, P, ctypes.c_size_t, P, P]
+    L.leap_grpo_logprob_loss_fwd_bwd_noalloc.restype = ctypes.c_int
+    L.leap_grpo_logprob_loss_fwd_bwd_noalloc.argtypes = [P, i64, i64, i32, P, P, P, P, P,
+                                                         ctypes.POINTER(leap_grpo_params), P, P,
+                                                         P, P, P, P, P]
     L.leap_logprob_fwd.restype = ctypes.c_int
     L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P, P]
     L.leap_lmhead_workspace_size.restype = ctypes.c_size_t
@@ -237,6 +242,25 @@ def leap_grpo_logprob_loss_fwd_bwd(logits, ld, N, V, token_ids, old_logp, ref_lo
         _ptr(workspace, None, "workspace"), int(ws_bytes), _ptr(dev_err, "int32", "dev_err"),
         _stream(stream))
     _check(st, "leap_grpo_logprob_loss_fwd_bwd")
+
+
+LEAP_NOALLOC_MAX_ROWS = 1048576
+
+
+def leap_grpo_logprob_loss_fwd_bwd_noalloc(logits, ld, N, V, token_ids, old_logp, ref_logp,
+                                           adv_tok, w_tok, params: leap_grpo_params, logp_out,
+                                           tok_loss_out, entropy_out, loss_out, dlogits,
+                                           dev_err=None, stream=None) -> None:
+    st = lib().leap_grpo_logprob_loss_fwd_bwd_noalloc(
+        _ptr(logits, "bfloat16", "logits"), int(ld), int(N), int(V),
+        _ptr(token_ids, "int32", "token_ids"), _ptr(old_logp, "float32", "old_logp"),
+        _ptr(ref_logp, "float32", "ref_logp"), _ptr(adv_tok, "float32", "adv_tok"),
+        _ptr(w_tok, "float32", "w_tok"), ctypes.byref(params) if params is not None else None,
+        _ptr(logp_out, "float32", "logp_out"), _ptr(tok_loss_out, "float32", "tok_loss_out"),
+        _ptr(entropy_out, "float32", "entropy_out"), _ptr(loss_out, "float32", "loss_out"),
+        _ptr(dlogits, "bfloat16", "dlogits"), _ptr(dev_err, "int32", "dev_err"),
+        _stream(stream))
+    _check(st, "leap_grpo_logprob_loss_fwd_bwd_noalloc")
 
 
 def leap_logprob_fwd(logits, ld, N, V, token_ids, w_tok, inv_temperature, logp_out,

@@ -154,6 +154,26 @@ def test_grpo_rejects(kw, status):
     assert e.value.status == status
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=L.LEAP_NOALLOC_MAX_ROWS + 1), L.LEAP_ERR_UNSUPPORTED),
+    (dict(N=-1), L.LEAP_ERR_INVALID_ARG),
+    (dict(loss_out=None), L.LEAP_ERR_INVALID_ARG),
+    (dict(logits=FAKE + 2), L.LEAP_ERR_MISALIGNED),
+    (dict(dlogits=FAKE + 2048), L.LEAP_ERR_INVALID_ARG),
+])
+def test_grpo_noalloc_rejects(kw, status):
+    """The no-allocation form checks its arguments like the workspace form
+    and refuses more rows than its device array holds, all on the host."""
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+    a = dict(logits=FAKE, ld=1024, N=8, V=1000, token_ids=FAKE, old_logp=FAKE, ref_logp=FAKE,
+             adv_tok=FAKE, w_tok=FAKE, params=p, logp_out=None, tok_loss_out=None,
+             entropy_out=None, loss_out=FAKE, dlogits=FAKE + (1 << 40), dev_err=None, stream=0)
+    a.update(kw)
+    with pytest.raises(L.LeapError) as e:
+        L.leap_grpo_logprob_loss_fwd_bwd_noalloc(**a)
+    assert e.value.status == status
+
+
 @pytest.mark.parametrize("field,value,status", [
     ("clip_eps_low", -0.1, L.LEAP_ERR_INVALID_ARG),
     ("kl_coef", float("inf"), L.LEAP_ERR_INVALID_ARG),

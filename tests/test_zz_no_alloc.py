@@ -1,0 +1,88 @@
+"""The no-allocation form of the fused objective
+(leap_grpo_logprob_loss_fwd_bwd_noalloc), through the C ABI, against the
+workspace form on the same inputs: two calls in a row on one device, the
+second smaller than the first (the library-owned scratch keeps the first
+call's contents), then a call at the largest accepted size.  The two forms
+run the same kernels, so the bar is bit-for-bit equality of every output;
+the workspace form itself is held to the oracle by the parity suite."""
+import numpy as np
+import pytest
+
+from tests import _gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+KW = dict(eps_lo=0.2, eps_hi=0.28, kl_coef=0.01)
+
+
+def _run_both(N, V, seed, want_entropy):
+    import torch
+    from paper_2608_01804_amd import leap as L
+    lg, tok, old, ref = U.make_inputs_host(seed, N, V, old_sigma=0.3)
+    rng = np.random.default_rng(seed)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = rng.choice([0.0, 1.0, 0.5], N).astype(np.float32)
+    lg_d = U.bf16_device(lg)
+    dev = U.dev()
+    args = [U.T(tok), U.T(old), U.T(ref), U.T(adv), U.T(w)]
+    p = L.leap_grpo_params(KW["eps_lo"], KW["eps_hi"], KW["kl_coef"], 0, 1.0)
+    outs = []
+    for form in ("workspace", "noalloc"):
+        dl = torch.full_like(lg_d, float("nan"))
+        lp = torch.full((N,), float("nan"), dtype=torch.float32, device=dev)
+        tl = torch.full((N,), float("nan"), dtype=torch.float32, device=dev)
+        ent = torch.full((N,), float("nan"), dtype=torch.float32, device=dev) if want_entropy else None
+        loss = torch.full((1,), float("nan"), dtype=torch.float32, device=dev)
+        err = U.zeros_i32(1)
+        if form == "workspace":
+            ws_bytes = L.leap_grpo_workspace_size(N, V)
+            ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+            L.leap_grpo_logprob_loss_fwd_bwd(lg_d, V, N, V, *args, p, lp, tl, ent, loss, dl, ws,
+                                             ws_bytes, err)
+        else:
+            L.leap_grpo_logprob_loss_fwd_bwd_noalloc(lg_d, V, N, V, *args, p, lp, tl, ent, loss,
+                                                     dl, err)
+        torch.cuda.synchronize()
+        outs.append({"dl": dl.view(torch.int16).cpu().numpy(), "lp": lp.cpu().numpy(),
+                     "tl": tl.cpu().numpy(), "loss": loss.cpu().numpy(),
+                     "ent": None if ent is None else ent.cpu().numpy(), "err": int(err.item())})
+    return outs
+
+
+def _assert_same(a, b):
+    np.testing.assert_array_equal(a["dl"], b["dl"])
+    np.testing.assert_array_equal(a["lp"], b["lp"])
+    np.testing.assert_array_equal(a["tl"], b["tl"])
+    np.testing.assert_array_equal(a["loss"], b["loss"])
+    if a["ent"] is not None:
+        np.testing.assert_array_equal(a["ent"], b["ent"])
+    assert a["err"] == b["err"] == 0
+    assert np.isfinite(a["loss"]).all()
+
+
+def test_noalloc_matches_workspace_form_two_calls():
+    # 1: 3000 rows of a 151936-column vocabulary; 2: 700 rows of 32768
+    U.log("noalloc call 1: N=3000 V=151936")
+    a, b = _run_both(3000, 151936, 71, want_entropy=True)
+    _assert_same(a, b)
+    U.log("noalloc call 2: N=700 V=32768 (smaller)")
+    a, b = _run_both(700, 32768, 72, want_entropy=False)
+    _assert_same(a, b)
+
+
+def test_noalloc_largest_size_and_rejections():
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N, V = L.LEAP_NOALLOC_MAX_ROWS, 64
+    U.log(f"noalloc at the limit: N={N} V={V}")
+    a, b = _run_both(N, V, 73, want_entropy=False)
+    _assert_same(a, b)
+    one = torch.zeros(1, dtype=torch.float32, device=U.dev())
+    one_i = torch.zeros(1, dtype=torch.int32, device=U.dev())
+    lg = torch.zeros((1, V), dtype=torch.bfloat16, device=U.dev())
+    dl = torch.zeros((1, V), dtype=torch.bfloat16, device=U.dev())
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, 0, 1.0)
+    with pytest.raises(L.LeapError) as e:  # rejected on the host before any launch
+        L.leap_grpo_logprob_loss_fwd_bwd_noalloc(lg, V, N + 1, V, one_i, one, one, one, one, p,
+                                                 None, None, None, one, dl.data_ptr() + (1 << 40))
+    assert e.value.status == L.LEAP_ERR_UNSUPPORTED
