@@ -2,7 +2,7 @@
 // token), over bf16 [rows x vocab] logits.
 //
 // Design (gfx950, wave64):
-//  * One workgroup per row.  For V up to 196608 the whole row is held in
+//  * One workgroup holds one row at a time.  For V up to 196608 the whole row is held in
 //    VGPRs: each lane owns CH 16-byte chunks (8 bf16 each) at chunk index
 //    j*BLOCK + lane, so every load and store instruction of a wave covers
 //    1 KiB of contiguous HBM, and the row is read from HBM exactly once.
@@ -25,6 +25,11 @@
 //    value directly, packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and stored
 //    16 bytes at a time; the token's own column gets g * (1 - p_y).
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
+//  * For 1024-lane rows (one workgroup per compute unit) the kernel is
+//    persistent: a grid of one workgroup per CU walks the rows and issues
+//    the next row's loads right behind the current row's stores, so each
+//    CU's reads overlap its writes instead of waiting for a new workgroup
+//    to be dispatched after each row.
 //  * Larger vocabularies use a streaming variant that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
 // kernel sums them in a fixed order (bitwise reproducible).
@@ -42,50 +47,60 @@ namespace {
 using namespace row;
 using namespace obj;
 
-// Zero the dlogits row of an excluded token.
+// Zero the dlogits row of an excluded token: 16-byte non-temporal stores
+// through a buffer descriptor over the row's whole chunks, the partial last
+// chunk element by element.
 template <int BLOCK>
 __device__ __forceinline__ void zero_row(uint16_t* drow, int V, int tid) {
     const int nfull = V >> 3;
-    u32x4* d4 = reinterpret_cast<u32x4*>(drow);
-    for (int c = tid; c < nfull; c += BLOCK) d4[c] = u32x4_of(0u, 0u, 0u, 0u);
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+    const u32x4 z = u32x4_of(0u, 0u, 0u, 0u);
+    for (int c = tid; c < nfull; c += BLOCK)
+        __builtin_amdgcn_raw_buffer_store_b128(z, rd, c * 16, 0, kStorePolicy);
     for (int e = (nfull << 3) + tid; e < V; e += BLOCK) drow[e] = 0;
 }
 
+// Row outputs of an excluded row (weight 0, or counted as a data error) and
+// its zero-filled dlogits row.
+template <int BLOCK, bool ENT>
+__device__ __forceinline__ void excluded_row(int64_t row, uint16_t* drow, int V, bool count,
+                                             float* logp_out, float* tok_loss_out,
+                                             float* entropy_out, float* row_loss,
+                                             int32_t* dev_err, int tid) {
+    if (tid == 0) {
+        if (count) count_error(dev_err);
+        write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
+        if (ENT) entropy_out[row] = 0.0f;
+    }
+    zero_row<BLOCK>(drow, V, tid);
+}
+
+// LDS of one block-wide (max, sum[, t]) merge.
+template <int BLOCK, bool ENT>
+struct RowLds {
+    float m[BLOCK / kWave];
+    float s[BLOCK / kWave];
+    float t[ENT ? BLOCK / kWave : 1];
+};
+
+// Passes A-C of one live row whose loads into x have been issued: the
+// lane maximum, the exponentials (kept as fp16 in x), the block merge, the
+// scalar epilogue, the dlogits stores and the row's outputs.  A row whose
+// logits are all -inf is counted and zero-filled instead.  One barrier
+// (inside the block merge) in every call.
 template <int BLOCK, int CH, int SAFE, bool ENT>
-__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
-grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
-                   const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
-                   const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
-                   const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
-                   float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
-                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
-    __shared__ float s_m[BLOCK / kWave];
-    __shared__ float s_s[BLOCK / kWave];
-    __shared__ float s_t[ENT ? BLOCK / kWave : 1];
-    const int tid = threadIdx.x;
+__device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row, uint16_t* drow,
+                                          int V, int y, float w, const float* __restrict__ old_logp,
+                                          const float* __restrict__ ref_logp,
+                                          const float* __restrict__ adv_tok, const Params& p,
+                                          float* __restrict__ logp_out,
+                                          float* __restrict__ tok_loss_out,
+                                          float* __restrict__ entropy_out,
+                                          float* __restrict__ row_loss, int32_t* __restrict__ dev_err,
+                                          RowLds<BLOCK, ENT>& lds, int tid) {
     const int lane16 = tid * 16;
-    const int64_t row = blockIdx.x;
     const int nchunks = (V + 7) >> 3;
     const int nfull = V >> 3;
-    const uint16_t* xrow = logits + row * ld;
-    uint16_t* drow = dlogits + row * ld;
-
-    const float w = w_tok[row];
-    const int y = token_ids[row];
-    if (!row_live(w, y, V)) {
-        if (tid == 0) {
-            if (w != 0.0f) count_error(dev_err);  // token id out of range
-            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-            if (ENT) entropy_out[row] = 0.0f;
-        }
-        zero_row<BLOCK>(drow, V, tid);
-        return;
-    }
-
-    // The whole row into registers: one read of HBM.
-    u32x4 x[CH];
-    load_row<BLOCK, CH, SAFE>(x, xrow, nchunks, lane16);
-    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
     mask_row_tail<BLOCK, CH, SAFE>(x, V, tid);
 
     // Pass A: lane maximum over the raw bf16 words.
@@ -133,16 +148,12 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
     float S = s;
     float T = t;
     if constexpr (ENT)
-        block_mst_reduce<BLOCK>(M, S, T, s_m, s_s, s_t, tid);
+        block_mst_reduce<BLOCK>(M, S, T, lds.m, lds.s, lds.t, tid);
     else
-        block_ms_reduce<BLOCK>(M, S, s_m, s_s, tid);
+        block_ms_reduce<BLOCK>(M, S, lds.m, lds.s, tid);
     if (M == -INFINITY) {  // every logit of the row is -inf
-        if (tid == 0) {
-            count_error(dev_err);
-            write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-            if (ENT) entropy_out[row] = 0.0f;
-        }
-        zero_row<BLOCK>(drow, V, tid);
+        excluded_row<BLOCK, ENT>(row, drow, V, true, logp_out, tok_loss_out, entropy_out, row_loss,
+                                 dev_err, tid);
         return;
     }
     const float lse2 = M + __builtin_amdgcn_logf(S);
@@ -190,6 +201,97 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
     }
 }
 
+// One workgroup per row.
+template <int BLOCK, int CH, int SAFE, bool ENT>
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
+grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, int64_t N,
+                   const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+                   const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+                   const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+                   float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
+                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    __shared__ RowLds<BLOCK, ENT> lds;
+    const int tid = threadIdx.x;
+    const int64_t row = blockIdx.x;
+    (void)N;
+    const uint16_t* xrow = logits + row * ld;
+    uint16_t* drow = dlogits + row * ld;
+    const float w = w_tok[row];
+    const int y = token_ids[row];
+    if (!row_live(w, y, V)) {  // excluded; a weighted row with a bad token id is counted
+        excluded_row<BLOCK, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
+                                 row_loss, dev_err, tid);
+        return;
+    }
+    // The whole row into registers: one read of HBM.
+    u32x4 x[CH];
+    load_row<BLOCK, CH, SAFE>(x, xrow, (V + 7) >> 3, tid * 16);
+    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+    fused_row<BLOCK, CH, SAFE, ENT>(x, xy, row, drow, V, y, w, old_logp, ref_logp, adv_tok, p,
+                                    logp_out, tok_loss_out, entropy_out, row_loss, dev_err, lds,
+                                    tid);
+}
+
+// Persistent form: workgroup b takes rows b, b + G, b + 2G, ... (G = the
+// grid).  The next row's token id and weight are fetched while the current
+// row is processed, and its logits loads are issued as soon as the current
+// row's registers are free: after the dlogits stores of a live row, before
+// the zero fill of an excluded one.  On each compute unit the next row's
+// reads thus overlap the current row's writes draining to HBM.  The block
+// merges of consecutive rows alternate between two LDS areas: a wave that
+// runs ahead into the next row's merge cannot overwrite values a slower wave
+// has yet to read from the previous one.
+template <int BLOCK, int CH, int SAFE, bool ENT>
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
+grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
+                  const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+                  const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+                  const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+                  float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
+                  float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    __shared__ RowLds<BLOCK, ENT> lds[2];
+    const int tid = threadIdx.x;
+    const int nchunks = (V + 7) >> 3;
+    int64_t row = blockIdx.x;
+    if (row >= N) return;
+    u32x4 x[CH];
+    float xy = 0.0f;
+    // Issue the loads of row r (live) into x; its token logit into xy.
+    auto issue_row = [&](int64_t r, int yr) {
+        const uint16_t* xrow = logits + r * ld;
+        load_row<BLOCK, CH, SAFE>(x, xrow, nchunks, tid * 16);
+        xy = __uint_as_float(static_cast<uint32_t>(xrow[yr]) << 16);
+    };
+    float w = w_tok[row];
+    int y = token_ids[row];
+    bool live = row_live(w, y, V);
+    if (live) issue_row(row, y);
+    int parity = 0;
+    while (true) {
+        const int64_t next = row + gridDim.x;
+        const bool more = next < N;
+        const float w_next = more ? w_tok[next] : 0.0f;
+        const int y_next = more ? token_ids[next] : 0;
+        const bool live_next = more && row_live(w_next, y_next, V);
+        uint16_t* drow = dlogits + row * ld;
+        if (live) {
+            fused_row<BLOCK, CH, SAFE, ENT>(x, xy, row, drow, V, y, w, old_logp, ref_logp, adv_tok,
+                                            p, logp_out, tok_loss_out, entropy_out, row_loss,
+                                            dev_err, lds[parity], tid);
+            parity ^= 1;
+        }
+        if (live_next) issue_row(next, y_next);
+        if (!live)
+            excluded_row<BLOCK, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
+                                     row_loss, dev_err, tid);
+        if (!more) break;
+        row = next;
+        w = w_next;
+        y = y_next;
+        live = live_next;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Streaming variant for any V: online (max, sum) over the row, then a second
 // read to form dlogits.  Each chunk is read and written by one thread only,
@@ -197,7 +299,7 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V,
 // ---------------------------------------------------------------------------
 template <int BLOCK, bool ENT>
 __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
-    const uint16_t* logits, int64_t ld, int V, const int32_t* __restrict__ token_ids,
+    const uint16_t* logits, int64_t ld, int V, int64_t N, const int32_t* __restrict__ token_ids,
     const float* __restrict__ old_logp, const float* __restrict__ ref_logp,
     const float* __restrict__ adv_tok, const float* __restrict__ w_tok, Params p,
     float* __restrict__ logp_out, float* __restrict__ tok_loss_out,
@@ -208,6 +310,7 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
     __shared__ float s_t[ENT ? BLOCK / kWave : 1];
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
+    (void)N;
     const int nchunks = (V + 7) >> 3;
     const int nfull = V >> 3;
     const uint16_t* xrow = logits + row * ld;
@@ -320,7 +423,7 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
 // ---------------------------------------------------------------------------
 // Host dispatch
 // ---------------------------------------------------------------------------
-using RowKernel = void (*)(const uint16_t*, int64_t, int, const int32_t*, const float*,
+using RowKernel = void (*)(const uint16_t*, int64_t, int, int64_t, const int32_t*, const float*,
                            const float*, const float*, const float*, Params, float*, float*,
                            float*, float*, uint16_t*, int32_t*);
 
@@ -328,29 +431,38 @@ struct RowConfig {
     RowKernel fn;      // without the entropy output
     RowKernel fn_ent;  // with it
     int block;
-    int ch;  // 0: streaming variant
+    int ch;           // 0: streaming variant
+    bool persistent;  // one workgroup per compute unit, rows strided by the grid
 };
 
 #define LEAP_RES(B, C, S) \
-    RowConfig{grpo_rows_resident<B, C, S, false>, grpo_rows_resident<B, C, S, true>, B, C}
+    RowConfig{grpo_rows_resident<B, C, S, false>, grpo_rows_resident<B, C, S, true>, B, C, false}
+#define LEAP_PER(B, C, S) \
+    RowConfig{grpo_rows_persist<B, C, S, false>, grpo_rows_persist<B, C, S, true>, B, C, true}
 
 // The kernel for V: the resident shape row::pick_resident_shape chooses, or
-// the streaming variant.
+// the streaming variant.  The 1024-lane shapes up to 19 chunks per lane
+// (32768 < V <= 155648), whose register footprint leaves one workgroup per
+// compute unit, run persistent; at 20 and 24 chunks the persistent loop's
+// extra live state would spill, so those keep one workgroup per row.
 RowConfig pick_row_config(int V) {
     static const RowConfig table[] = {
         LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
         LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
-        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_RES(1024, 8, 0),
-        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_RES(1024, 19, 16),
+        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_PER(1024, 8, 0),
+        LEAP_PER(1024, 12, 8),  LEAP_PER(1024, 16, 12), LEAP_PER(1024, 19, 16),
         LEAP_RES(1024, 20, 19), LEAP_RES(1024, 24, 20),
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i < 0) return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0};
+    if (i < 0)
+        return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0,
+                         false};
     return table[i];
 }
 
 #undef LEAP_RES
+#undef LEAP_PER
 
 }  // namespace
 }  // namespace leap
@@ -409,9 +521,18 @@ leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
-        hipLaunchKernelGGL(entropy_out ? rc.fn_ent : rc.fn, dim3(static_cast<unsigned>(N)),
+        int64_t grid = N;
+        if (rc.persistent) {
+            int dev = 0, cus = 0;
+            if (hipGetDevice(&dev) != hipSuccess ||
+                hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                    hipSuccess)
+                return LEAP_ERR_HIP;
+            if (cus > 0 && grid > cus) grid = cus;
+        }
+        hipLaunchKernelGGL(entropy_out ? rc.fn_ent : rc.fn, dim3(static_cast<unsigned>(grid)),
                            dim3(rc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
-                           V, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
+                           V, N, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
                            tok_loss_out, entropy_out, row_loss,
                            static_cast<uint16_t*>(dlogits_bf16), dev_err);
         const leap_status st = lc.status();
