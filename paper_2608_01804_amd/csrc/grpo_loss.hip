@@ -25,7 +25,7 @@
 //    value directly, packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and stored
 //    16 bytes at a time; the token's own column gets g * (1 - p_y).
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
-//  * For 1024-lane rows (one workgroup per compute unit) the kernel is
+//  * For the 19-chunk shape (one workgroup per compute unit) the kernel is
 //    persistent: a grid of one workgroup per CU walks the rows and issues
 //    the next row's loads right behind the current row's stores, so each
 //    CU's reads overlap its writes instead of waiting for a new workgroup
@@ -441,16 +441,19 @@ struct RowConfig {
     RowConfig{grpo_rows_persist<B, C, S, false>, grpo_rows_persist<B, C, S, true>, B, C, true}
 
 // The kernel for V: the resident shape row::pick_resident_shape chooses, or
-// the streaming variant.  The 1024-lane shapes up to 19 chunks per lane
-// (32768 < V <= 155648), whose register footprint leaves one workgroup per
-// compute unit, run persistent; at 20 and 24 chunks the persistent loop's
-// extra live state would spill, so those keep one workgroup per row.
+// the streaming variant.  The 19-chunk shape (131072 < V <= 155648, which
+// holds the 151936- and 152064-column vocabularies) runs persistent: measured
+// on the MI355X it is 2-3% faster there than one workgroup per row.  At 8,
+// 12 and 16 chunks it measured equal or slower (at 8 chunks the one-row
+// kernel fits two workgroups per compute unit, the persistent loop one), and
+// at 20 and 24 chunks the loop's extra live state would spill, so those
+// shapes keep one workgroup per row.
 RowConfig pick_row_config(int V) {
     static const RowConfig table[] = {
         LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
         LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
-        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_PER(1024, 8, 0),
-        LEAP_PER(1024, 12, 8),  LEAP_PER(1024, 16, 12), LEAP_PER(1024, 19, 16),
+        LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_RES(1024, 8, 0),
+        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_PER(1024, 19, 16),
         LEAP_RES(1024, 20, 19), LEAP_RES(1024, 24, 20),
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
@@ -522,15 +525,20 @@ leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t
     if (N > 0) {
         const RowConfig rc = pick_row_config(V);
         int64_t grid = N;
+        const RowKernel fn = entropy_out ? rc.fn_ent : rc.fn;
         if (rc.persistent) {
-            int dev = 0, cus = 0;
+            // as many workgroups as the device holds at once
+            int dev = 0, cus = 0, per_cu = 0;
             if (hipGetDevice(&dev) != hipSuccess ||
                 hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
-                    hipSuccess)
+                    hipSuccess ||
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                    &per_cu, reinterpret_cast<const void*>(fn), rc.block, 0) != hipSuccess)
                 return LEAP_ERR_HIP;
-            if (cus > 0 && grid > cus) grid = cus;
+            const int64_t resident = static_cast<int64_t>(cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
+            if (grid > resident) grid = resident;
         }
-        hipLaunchKernelGGL(entropy_out ? rc.fn_ent : rc.fn, dim3(static_cast<unsigned>(grid)),
+        hipLaunchKernelGGL(fn, dim3(static_cast<unsigned>(grid)),
                            dim3(rc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
                            V, N, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
                            tok_loss_out, entropy_out, row_loss,
