@@ -30,7 +30,9 @@
 //    the next row's loads right behind the current row's stores, so each
 //    CU's reads overlap its writes instead of waiting for a new workgroup
 //    to be dispatched after each row.
-//  * Larger vocabularies use a streaming variant that re-reads the row.
+//  * Up to 270336 columns the part of the row past 196608 columns is held in
+//    LDS (the hybrid kernel); larger vocabularies use a streaming variant
+//    that re-reads the row.
 // The per-row weighted losses go to a workspace and a single-workgroup
 // kernel sums them in a fixed order (bitwise reproducible).
 // Optional output: each row's entropy H = -sum_v p_v ln p_v (nats), from a
@@ -83,40 +85,13 @@ struct RowLds {
     float t[ENT ? BLOCK / kWave : 1];
 };
 
-// Passes A-C of one live row whose loads into x have been issued: the
-// lane maximum, the exponentials (kept as fp16 in x), the block merge, the
-// scalar epilogue, the dlogits stores and the row's outputs.  A row whose
-// logits are all -inf is counted and zero-filled instead.  One barrier
-// (inside the block merge) in every call.
-template <int BLOCK, int CH, int SAFE, bool ENT>
-__device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row, uint16_t* drow,
-                                          int V, int y, float w, const float* __restrict__ old_logp,
-                                          const float* __restrict__ ref_logp,
-                                          const float* __restrict__ adv_tok, const Params& p,
-                                          float* __restrict__ logp_out,
-                                          float* __restrict__ tok_loss_out,
-                                          float* __restrict__ entropy_out,
-                                          float* __restrict__ row_loss, int32_t* __restrict__ dev_err,
-                                          RowLds<BLOCK, ENT>& lds, int tid) {
-    const int lane16 = tid * 16;
-    const int nchunks = (V + 7) >> 3;
-    const int nfull = V >> 3;
-    mask_row_tail<BLOCK, CH, SAFE>(x, V, tid);
-
-    // Pass A: lane maximum over the raw bf16 words.
-    const float m = row_lane_max<CH>(x);
-
-    // Keep the bf16 words as the only live copy of the row.
-#pragma unroll
-    for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
-
-    // Pass B: e = 2^(x c - m c) summed in fp32 and kept as fp16 in place.
-    // Chunk j's inputs are tied to chunk j-1's output so about one chunk of
-    // fp32 temporaries is live at once.
-    const float c2 = kLog2e * p.inv_temp;
-    const float mc = (m == -INFINITY) ? 0.0f : m * c2;
-    float s = 0.0f;
-    float t = 0.0f;  // ENT: sum of 2^d * d
+// Pass B over the register-resident chunks: e = 2^(x c - mc) summed into s
+// (and e * d into t with ENT) in fp32, the values re-packed as fp16 in place.
+// Chunk j's inputs are tied to chunk j-1's output so about one chunk of fp32
+// temporaries is live at once.
+template <int CH, bool ENT>
+__device__ __forceinline__ void exp_pass_vgpr(u32x4 (&x)[CH], float c2, float mc, float& s,
+                                              float& t) {
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
         if (j > 0) asm volatile("" : "+v"(x[j]) : "v"(x[j - 1]));
@@ -143,25 +118,17 @@ __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row,
         }
         x[j] = u32x4_of(wv[0], wv[1], wv[2], wv[3]);
     }
+}
 
-    float M = (m == -INFINITY) ? -INFINITY : mc;
-    float S = s;
-    float T = t;
-    if constexpr (ENT)
-        block_mst_reduce<BLOCK>(M, S, T, lds.m, lds.s, lds.t, tid);
-    else
-        block_ms_reduce<BLOCK>(M, S, lds.m, lds.s, tid);
-    if (M == -INFINITY) {  // every logit of the row is -inf
-        excluded_row<BLOCK, ENT>(row, drow, V, true, logp_out, tok_loss_out, entropy_out, row_loss,
-                                 dev_err, tid);
-        return;
-    }
-    const float lse2 = M + __builtin_amdgcn_logf(S);
-    const RowOut o = row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
-
-    // Pass C: dlogits = -g * p_v = sc * e_v; the token's column gets g (1 - p_y).
-    const float sc = -o.g * __builtin_amdgcn_exp2f(mc - lse2);
-    const float dy = o.g * (1.0f - hw_exp(o.logp));
+// Pass C over the register-resident chunks (fp16 e from pass B):
+// dlogits = sc * e, the token's own column dy, bf16 (RNE), 16-byte stores;
+// the partial last chunk (V % 8 columns) element by element.
+template <int BLOCK, int CH, int SAFE>
+__device__ __forceinline__ void dlogits_pass_vgpr(u32x4 (&x)[CH], float sc, float dy, int y,
+                                                  uint16_t* drow, int V, int tid) {
+    const int lane16 = tid * 16;
+    const int nchunks = (V + 7) >> 3;
+    const int nfull = V >> 3;
     const int cy_rel = (y >> 3) - tid;  // chunk of the token, relative to this lane
     const int ey = y & 7;
     const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
@@ -195,6 +162,58 @@ __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row,
         }
         prev = out;
     }
+}
+
+// Passes A-C of one live row whose loads into x have been issued: the
+// lane maximum, the exponentials (kept as fp16 in x), the block merge, the
+// scalar epilogue, the dlogits stores and the row's outputs.  A row whose
+// logits are all -inf is counted and zero-filled instead.  One barrier
+// (inside the block merge) in every call.
+template <int BLOCK, int CH, int SAFE, bool ENT>
+__device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row, uint16_t* drow,
+                                          int V, int y, float w, const float* __restrict__ old_logp,
+                                          const float* __restrict__ ref_logp,
+                                          const float* __restrict__ adv_tok, const Params& p,
+                                          float* __restrict__ logp_out,
+                                          float* __restrict__ tok_loss_out,
+                                          float* __restrict__ entropy_out,
+                                          float* __restrict__ row_loss, int32_t* __restrict__ dev_err,
+                                          RowLds<BLOCK, ENT>& lds, int tid) {
+    mask_row_tail<BLOCK, CH, SAFE>(x, V, tid);
+
+    // Pass A: lane maximum over the raw bf16 words.
+    const float m = row_lane_max<CH>(x);
+
+    // Keep the bf16 words as the only live copy of the row.
+#pragma unroll
+    for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
+
+    // Pass B: e = 2^(x c - m c) summed in fp32 and kept as fp16 in place.
+    const float c2 = kLog2e * p.inv_temp;
+    const float mc = (m == -INFINITY) ? 0.0f : m * c2;
+    float s = 0.0f;
+    float t = 0.0f;  // ENT: sum of 2^d * d
+    exp_pass_vgpr<CH, ENT>(x, c2, mc, s, t);
+
+    float M = (m == -INFINITY) ? -INFINITY : mc;
+    float S = s;
+    float T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, lds.m, lds.s, lds.t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, lds.m, lds.s, tid);
+    if (M == -INFINITY) {  // every logit of the row is -inf
+        excluded_row<BLOCK, ENT>(row, drow, V, true, logp_out, tok_loss_out, entropy_out, row_loss,
+                                 dev_err, tid);
+        return;
+    }
+    const float lse2 = M + __builtin_amdgcn_logf(S);
+    const RowOut o = row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
+
+    // Pass C: dlogits = -g * p_v = sc * e_v; the token's column gets g (1 - p_y).
+    const float sc = -o.g * __builtin_amdgcn_exp2f(mc - lse2);
+    const float dy = o.g * (1.0f - hw_exp(o.logp));
+    dlogits_pass_vgpr<BLOCK, CH, SAFE>(x, sc, dy, y, drow, V, tid);
     if (tid == 0) {
         write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
         if (ENT) entropy_out[row] = entropy_of(S, T);
@@ -289,6 +308,167 @@ grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
         w = w_next;
         y = y_next;
         live = live_next;
+    }
+}
+
+// Rows wider than the register file holds (196608 < V <= 270336): the first
+// 24 chunks per lane stay in VGPRs as in the resident kernel, and the rest
+// of the row -- up to 9 more chunks per lane, 144 KiB -- goes into LDS by
+// LDS-DMA loads, so the row is still read from HBM once.  The LDS part keeps
+// the bf16 logits: pass A takes its lane maximum, pass B sums its
+// exponentials without storing them, and pass C recomputes each one from
+// the row's log-sum-exp.  Each lane reads back only the chunks its own wave
+// wrote, so the DMA needs no workgroup barrier, only the wave's own wait.
+constexpr int kHybridCH = 24;
+constexpr int kHybridLdsSlots = 9;
+constexpr int64_t kHybridMaxV = static_cast<int64_t>(kHybridCH + kHybridLdsSlots) * 1024 * 8;
+
+template <bool ENT>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(4))) void
+grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
+                 const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+                 const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+                 const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+                 float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
+                 float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    constexpr int BLOCK = 1024;
+    constexpr int CH = kHybridCH;
+    __shared__ RowLds<BLOCK, ENT> red;
+    __shared__ __attribute__((aligned(16))) u32x4 xs[kHybridLdsSlots * BLOCK];
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave;
+    const int64_t row = blockIdx.x;
+    (void)N;
+    const uint16_t* xrow = logits + row * ld;
+    uint16_t* drow = dlogits + row * ld;
+    const float w = w_tok[row];
+    const int y = token_ids[row];
+    if (!row_live(w, y, V)) {
+        excluded_row<BLOCK, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
+                                 row_loss, dev_err, tid);
+        return;
+    }
+    const int nchunks = (V + 7) >> 3;
+    const int nfull = V >> 3;
+    const int nl = (nchunks - CH * BLOCK + BLOCK - 1) / BLOCK;  // LDS slots in use, 1..9
+
+    // One read of HBM: CH chunks per lane into VGPRs (all of them inside the
+    // row, V > 196608), the rest into this wave's 1 KiB of each LDS slot.
+    u32x4 x[CH];
+    load_row<BLOCK, CH, CH>(x, xrow, nchunks, tid * 16);
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(xrow, nchunks * 16);
+    for (int k = 0; k < nl; ++k)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void*)(&xs[k * BLOCK + wave * kWave]), 16,
+            tid * 16 + (CH + k) * BLOCK * 16, 0, 0, kLoadPolicy);
+    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads, LDS-DMA included, have landed
+    asm volatile("" ::: "memory");
+
+    // LDS chunk k of this lane, columns past V as -inf.
+    auto lds_chunk = [&](int k) -> u32x4 {
+        const int c = (CH + k) * BLOCK + tid;
+        const u32x4 v = xs[k * BLOCK + tid];
+        if (c >= nchunks) return u32x4_of(kNegInfPair, kNegInfPair, kNegInfPair, kNegInfPair);
+        return c == nfull ? mask_tail(v, V & 7) : v;
+    };
+
+    // Pass A: lane maximum over both parts.
+    float m = row_lane_max<CH>(x);
+    {
+        uint32_t mh = kNegInfPair;
+        for (int k = 0; k < nl; ++k) {
+            const u32x4 v = lds_chunk(k);
+            mh = pk_max_f16(pk_max_f16(mh, v.x), pk_max_f16(v.y, pk_max_f16(v.z, v.w)));
+        }
+        m = fmaxf(m, fmaxf(max_half_to_f32(mh), max_half_to_f32(mh >> 16)));
+    }
+#pragma unroll
+    for (int j = 0; j < CH; ++j) asm volatile("" : "+v"(x[j]));
+
+    // Pass B: the register part as in the resident kernel, then the LDS part.
+    const float c2 = kLog2e * p.inv_temp;
+    const float mc = (m == -INFINITY) ? 0.0f : m * c2;
+    float s = 0.0f;
+    float t = 0.0f;
+    exp_pass_vgpr<CH, ENT>(x, c2, mc, s, t);
+    for (int k = 0; k < nl; ++k) {
+        const u32x4 v = lds_chunk(k);
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float lo = bf_lo(wv[q]);
+            const float hi = bf_hi(wv[q]);
+            if constexpr (ENT) {
+                const float da = vmax(fmaf(lo, c2, -mc), kMinExp2Arg);
+                const float db = vmax(fmaf(hi, c2, -mc), kMinExp2Arg);
+                const float a = __builtin_amdgcn_exp2f(da);
+                const float b = __builtin_amdgcn_exp2f(db);
+                s += a;
+                s += b;
+                t = fmaf(a, da, t);
+                t = fmaf(b, db, t);
+            } else {
+                s += __builtin_amdgcn_exp2f(fmaf(lo, c2, -mc));
+                s += __builtin_amdgcn_exp2f(fmaf(hi, c2, -mc));
+            }
+        }
+    }
+
+    float M = (m == -INFINITY) ? -INFINITY : mc;
+    float S = s;
+    float T = t;
+    if constexpr (ENT)
+        block_mst_reduce<BLOCK>(M, S, T, red.m, red.s, red.t, tid);
+    else
+        block_ms_reduce<BLOCK>(M, S, red.m, red.s, tid);
+    if (M == -INFINITY) {
+        excluded_row<BLOCK, ENT>(row, drow, V, true, logp_out, tok_loss_out, entropy_out, row_loss,
+                                 dev_err, tid);
+        return;
+    }
+    const float lse2 = M + __builtin_amdgcn_logf(S);
+    const RowOut o = row_epilogue(lse2, xy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
+
+    // Pass C: the register part, then the LDS part with each probability
+    // recomputed as 2^(x c - lse2).
+    const float dy = o.g * (1.0f - hw_exp(o.logp));
+    dlogits_pass_vgpr<BLOCK, CH, CH>(x, -o.g * __builtin_amdgcn_exp2f(mc - lse2), dy, y, drow, V,
+                                     tid);
+    const __amdgpu_buffer_rsrc_t rd = row_rsrc(drow, nfull * 16);
+    const int cy = y >> 3;
+    const int ey = y & 7;
+    for (int k = 0; k < nl; ++k) {
+        const int c = (CH + k) * BLOCK + tid;
+        if (c >= nchunks) continue;
+        const u32x4 v = xs[k * BLOCK + tid];
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+        float d[8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            d[2 * q] = -o.g * __builtin_amdgcn_exp2f(fmaf(bf_lo(wv[q]), c2, -lse2));
+            d[2 * q + 1] = -o.g * __builtin_amdgcn_exp2f(fmaf(bf_hi(wv[q]), c2, -lse2));
+        }
+        if (c == cy) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e == ey) d[e] = dy;
+        }
+        if (c < nfull) {
+            const u32x4 out = u32x4_of(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]),
+                                       pack_bf16(d[4], d[5]), pack_bf16(d[6], d[7]));
+            __builtin_amdgcn_raw_buffer_store_b128(out, rd, c * 16, 0, kStorePolicy);
+        } else {  // partial last chunk
+            const int rem = V & 7;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (e < rem)
+                    drow[(c << 3) + e] = static_cast<uint16_t>(pack_bf16(d[e], 0.0f) & 0xffffu);
+        }
+    }
+    if (tid == 0) {
+        write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
+        if (ENT) entropy_out[row] = entropy_of(S, T);
     }
 }
 
@@ -458,10 +638,10 @@ RowConfig pick_row_config(int V) {
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i < 0)
-        return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0,
-                         false};
-    return table[i];
+    if (i >= 0) return table[i];
+    if (V <= kHybridMaxV)
+        return RowConfig{grpo_rows_hybrid<false>, grpo_rows_hybrid<true>, 1024, kHybridCH, false};
+    return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0, false};
 }
 
 #undef LEAP_RES
