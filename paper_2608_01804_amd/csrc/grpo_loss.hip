@@ -362,8 +362,6 @@ grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
             rs, (__attribute__((address_space(3))) void*)(&xs[k * BLOCK + wave * kWave]), 16,
             tid * 16 + (CH + k) * BLOCK * 16, 0, 0, kLoadPolicy);
     const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads, LDS-DMA included, have landed
-    asm volatile("" ::: "memory");
 
     // LDS chunk k of this lane, columns past V as -inf.
     auto lds_chunk = [&](int k) -> u32x4 {
@@ -373,8 +371,12 @@ grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
         return c == nfull ? mask_tail(v, V & 7) : v;
     };
 
-    // Pass A: lane maximum over both parts.
+    // Pass A: lane maximum over both parts; the register part first, so its
+    // waits follow its loads one by one, then the wait for the DMA.
     float m = row_lane_max<CH>(x);
+    // this wave's loads, LDS-DMA included, have landed (tied to m so that it
+    // is not scheduled ahead of the register part's maximum)
+    asm volatile("s_waitcnt vmcnt(0)" : "+v"(m) : : "memory");
     {
         uint32_t mh = kNegInfPair;
         for (int k = 0; k < nl; ++k) {
