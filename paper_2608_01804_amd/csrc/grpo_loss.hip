@@ -323,45 +323,51 @@ constexpr int kHybridCH = 24;
 constexpr int kHybridLdsSlots = 9;
 constexpr int64_t kHybridMaxV = static_cast<int64_t>(kHybridCH + kHybridLdsSlots) * 1024 * 8;
 
+// LDS of the hybrid kernel: the row's LDS part and one block merge.
 template <bool ENT>
-__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(4))) void
-grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
-                 const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
-                 const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
-                 const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
-                 float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
-                 float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+struct HybridLds {
+    __attribute__((aligned(16))) u32x4 xs[kHybridLdsSlots * 1024];
+    RowLds<1024, ENT> red;
+};
+
+// Issue the loads of a live row: kHybridCH chunks per lane into x (all of
+// them inside the row, V > 196608) and the rest into this wave's 1 KiB of
+// each LDS slot (LDS-DMA); returns the token logit.
+__device__ __forceinline__ float hybrid_issue(u32x4 (&x)[kHybridCH], u32x4* xs,
+                                              const uint16_t* xrow, int V, int y, int tid) {
     constexpr int BLOCK = 1024;
     constexpr int CH = kHybridCH;
-    __shared__ RowLds<BLOCK, ENT> red;
-    __shared__ __attribute__((aligned(16))) u32x4 xs[kHybridLdsSlots * BLOCK];
-    const int tid = threadIdx.x;
     const int wave = tid / kWave;
-    const int64_t row = blockIdx.x;
-    (void)N;
-    const uint16_t* xrow = logits + row * ld;
-    uint16_t* drow = dlogits + row * ld;
-    const float w = w_tok[row];
-    const int y = token_ids[row];
-    if (!row_live(w, y, V)) {
-        excluded_row<BLOCK, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
-                                 row_loss, dev_err, tid);
-        return;
-    }
     const int nchunks = (V + 7) >> 3;
-    const int nfull = V >> 3;
     const int nl = (nchunks - CH * BLOCK + BLOCK - 1) / BLOCK;  // LDS slots in use, 1..9
-
-    // One read of HBM: CH chunks per lane into VGPRs (all of them inside the
-    // row, V > 196608), the rest into this wave's 1 KiB of each LDS slot.
-    u32x4 x[CH];
     load_row<BLOCK, CH, CH>(x, xrow, nchunks, tid * 16);
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(xrow, nchunks * 16);
     for (int k = 0; k < nl; ++k)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             rs, (__attribute__((address_space(3))) void*)(&xs[k * BLOCK + wave * kWave]), 16,
             tid * 16 + (CH + k) * BLOCK * 16, 0, 0, kLoadPolicy);
-    const float xy = __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+    return __uint_as_float(static_cast<uint32_t>(xrow[y]) << 16);
+}
+
+// Passes A-C of a live row whose loads hybrid_issue has issued, and its
+// outputs; a row whose logits are all -inf is counted and zero-filled.
+template <bool ENT>
+__device__ __forceinline__ void hybrid_row(u32x4 (&x)[kHybridCH], const u32x4* xs, float xy,
+                                           int64_t row, uint16_t* drow, int V, int y, float w,
+                                           const float* __restrict__ old_logp,
+                                           const float* __restrict__ ref_logp,
+                                           const float* __restrict__ adv_tok, const Params& p,
+                                           float* __restrict__ logp_out,
+                                           float* __restrict__ tok_loss_out,
+                                           float* __restrict__ entropy_out,
+                                           float* __restrict__ row_loss,
+                                           int32_t* __restrict__ dev_err, RowLds<1024, ENT>& red,
+                                           int tid) {
+    constexpr int BLOCK = 1024;
+    constexpr int CH = kHybridCH;
+    const int nchunks = (V + 7) >> 3;
+    const int nfull = V >> 3;
+    const int nl = (nchunks - CH * BLOCK + BLOCK - 1) / BLOCK;
 
     // LDS chunk k of this lane, columns past V as -inf.
     auto lds_chunk = [&](int k) -> u32x4 {
@@ -472,6 +478,34 @@ grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
         write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
         if (ENT) entropy_out[row] = entropy_of(S, T);
     }
+}
+
+// One workgroup per row.
+template <bool ENT>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(4))) void
+grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
+                 const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
+                 const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
+                 const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
+                 float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
+                 float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+    __shared__ HybridLds<ENT> lds;
+    const int tid = threadIdx.x;
+    const int64_t row = blockIdx.x;
+    (void)N;
+    const uint16_t* xrow = logits + row * ld;
+    uint16_t* drow = dlogits + row * ld;
+    const float w = w_tok[row];
+    const int y = token_ids[row];
+    if (!row_live(w, y, V)) {
+        excluded_row<1024, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
+                                row_loss, dev_err, tid);
+        return;
+    }
+    u32x4 x[kHybridCH];
+    const float xy = hybrid_issue(x, lds.xs, xrow, V, y, tid);
+    hybrid_row<ENT>(x, lds.xs, xy, row, drow, V, y, w, old_logp, ref_logp, adv_tok, p, logp_out,
+                    tok_loss_out, entropy_out, row_loss, dev_err, lds.red, tid);
 }
 
 // ---------------------------------------------------------------------------
