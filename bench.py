@@ -307,13 +307,13 @@ def cpu_baseline(s, seconds: float, samples: int = 3):
         oracle.set_threads(cores)
     step_time1 = t_small1 + per_row1 * n_valid
     return {"value": n_valid / step_time, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"gate+tournament+token advantages over the whole step ({t_small:.2f} s), "
+            "sample": f"gate+tournament+token advantages over the whole step ({t_small * 1e3:.1f} ms), "
                       f"then the fused objective with dlogits on {samples} samples of "
                       f"generated-token rows ({', '.join(f'{d} rows in {t:.1f} s' for _, d, t in rates)}); "
                       f"median per-row rate scaled to the step's {n_valid} tokens",
             "cpu_model": _cpu_model(), "nproc": os.cpu_count(),
             "value_1_thread": n_valid / step_time1,
-            "sample_1_thread": f"the same on one thread: small steps {t_small1:.2f} s, fused "
+            "sample_1_thread": f"the same on one thread: small steps {t_small1 * 1e3:.1f} ms, fused "
                                f"objective on {done1} rows ({t_rows1:.1f} s)"}
 
 

@@ -338,13 +338,15 @@ def test_grpo_special_values_and_errors():
     U.check_dlogits(got, lg, rows, tok, old, ref, adv, w, V, atol=2e-2, kw=KW)
 
 
-def test_grpo_inplace_and_deterministic():
-    N, V = 256, 151936
+@pytest.mark.parametrize("V,N", [(151936, 300), (230000, 64)])
+def test_grpo_inplace_and_deterministic(V, N):
+    # 151936: the persistent kernel with more rows than one per workgroup for
+    # some workgroups only; 230000: rows held partly in LDS
     lg, tok, old, ref = U.make_inputs_host(9, N, V)
     rng = np.random.default_rng(9)
     adv = rng.normal(0, 1, N).astype(np.float32)
     w = rng.choice([0.0, 1.0], N, p=[0.2, 0.8]).astype(np.float32)
-    U.log("grpo in-place / determinism")
+    U.log(f"grpo in-place / determinism V={V} N={N}")
     a = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, want_entropy=True, **KW)
     b = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, **KW)
     c = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, inplace=True, want_entropy=True,
@@ -355,6 +357,11 @@ def test_grpo_inplace_and_deterministic():
     assert a["loss"] == b["loss"] == c["loss"]
     assert np.array_equal(a["logp"], c["logp"])
     assert np.array_equal(a["entropy"], c["entropy"])  # in place: the row is read before written
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
+    _check_rows(a, o, w != 0, f"V={V}")
+    rows = np.arange(N)
+    U.check_dlogits(U.dl_rows(a["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V, atol=2e-2,
+                    kw=KW)
 
 
 def test_grpo_all_masked_and_empty():
