@@ -28,7 +28,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 PIN_FILES = [os.path.join(HERE, f) for f in (
     "test_oracle_rank.py", "test_oracle_gate_discount.py", "test_oracle_grpo.py",
-    "test_oracle_lmhead.py", "test_oracle_vocab_shard.py", "test_oracle_rollout_stats.py")]
+    "test_oracle_lmhead.py", "test_oracle_vocab_shard.py", "test_oracle_rollout_stats.py",
+    "test_oracle_properties.py")]
 
 C = "leap_oracle.c"
 PY = "__init__.py"
