@@ -644,6 +644,11 @@ def lmhead_leg(L, torch, dev, seed: int, reps: int):
         L.leap_grpo_lmhead_fwd_bwd(hid, wt, R, V, H, y, old, ref, adv_tok, w_tok, p, logp, None,
                                    loss, dH, dW, 0, ws, ws_bytes, err)
 
+    probe = mfma_probe(L, torch, dev, 0)
+    probe_rnd = mfma_probe(L, torch, dev, 1)
+    log(f"[bench] MFMA probe: {probe / 1e12:.0f} TFLOP/s bf16 on ones, {probe_rnd / 1e12:.0f} on "
+        f"random operands ({probe / MFMA_BF16_PEAK:.3f} and {probe_rnd / MFMA_BF16_PEAK:.3f} of "
+        f"the 2.5 PFLOP/s spec)")
     settle(torch, call)
     stream = torch.cuda.current_stream()
     ms = []
@@ -674,7 +679,39 @@ def lmhead_leg(L, torch, dev, seed: int, reps: int):
                          "kernel": "one leap_grpo_lmhead_fwd_bwd call (4 GEMM passes)",
                          "flops_per_call_useful": useful, "flops_per_call_executed": executed,
                          "executed_TFLOPs": executed / t / 1e12,
-                         "executed_frac": executed / t / MFMA_BF16_PEAK}}
+                         "executed_frac": executed / t / MFMA_BF16_PEAK,
+                         "probe_ones_TFLOPs": probe / 1e12,
+                         "probe_random_TFLOPs": probe_rnd / 1e12,
+                         "executed_frac_of_probe_random": executed / t / probe_rnd}}
+
+
+def mfma_probe(L, torch, dev, random_operands: int = 0, iters: int = 500000, reps: int = 3):
+    """Achievable bf16 matrix-core rate of the device from the library's MFMA
+    probe (register operands, no memory traffic; four waves per workgroup,
+    four workgroups per compute unit), median of `reps` launches of about
+    0.1 s each, after 100 ms of the same launches so the clock has settled.
+    random_operands=0 multiplies ones (the least switching power);
+    random_operands=1 hashed random bf16, which switch the multipliers'
+    inputs as a GEMM over random data does: the rate the power limit leaves
+    before any memory traffic, an upper bound for such a GEMM."""
+    wgs = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
+    sink = torch.empty(wgs, dtype=torch.float32, device=dev)
+    settle(torch, lambda: L.leap_probe_mfma(iters, wgs, sink, random_operands), ms=100)
+    ts = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        L.leap_probe_mfma(iters, wgs, sink, random_operands)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) / 1e3)
+    if random_operands:
+        assert bool(torch.isfinite(sink).all().item()), "MFMA probe gave a non-finite sum"
+    else:
+        assert bool((sink == iters * 32).all().item()), "MFMA probe did not run every round"
+    flops = 4.0 * wgs * iters * 8 * 16384
+    return flops / float(np.median(ts))
 
 
 def blas_reference(torch, dev):

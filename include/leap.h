@@ -449,6 +449,26 @@ leap_status leap_rollout_stats(const int32_t *pass_turn, const int32_t *n_turns,
                                int32_t *dev_err, hipStream_t stream);
 
 /*
+ * Measurement helper, not part of the method: the achievable bf16 matrix-core
+ * rate.  n_workgroups workgroups of four waves each run `iters` rounds of
+ * eight independent v_mfma_f32_16x16x32_bf16 (16384 flops each) on register
+ * operands, with no memory traffic in the loop: 4 * n_workgroups * iters *
+ * 8 * 16384 flops in all.
+ * random_operands 0: every operand is 1.0, so the multipliers' inputs never
+ *   change (the lowest switching power); sink float [n_workgroups], device
+ *   memory: entry g receives iters * 32 (exact for iters < 2^19) when every
+ *   chain of workgroup g ran all its rounds.
+ * random_operands 1: each chain's operands are hashed bf16 values of
+ *   magnitude [1, 2) with random signs, different per lane and chain, so
+ *   consecutive MFMAs switch about half of their input bits, as a GEMM over
+ *   random data does; entry g receives a finite sum of accumulators.
+ * Errors: LEAP_ERR_INVALID_ARG for iters < 1, n_workgroups < 1,
+ * random_operands outside 0..1, sink NULL.
+ */
+leap_status leap_probe_mfma(int64_t iters, int32_t n_workgroups, int32_t random_operands,
+                            float *sink, hipStream_t stream);
+
+/*
  * Measurement helper, not part of the method: streams device memory with the
  * access shape of the fused kernel (16-byte non-temporal accesses) so the
  * achievable HBM rate of each access mix can be set beside the published

@@ -46,6 +46,7 @@ EXPORTED = (
     "leap_vocab_shard_bwd",
     "leap_rollout_stats",
     "leap_probe_hbm",
+    "leap_probe_mfma",
 )
 
 
@@ -121,6 +122,8 @@ def lib() -> ctypes.CDLL:
     L.leap_vocab_shard_bwd.argtypes = [P, i64, i64, i32, i32, P, P, f32, P, P]
     L.leap_rollout_stats.restype = ctypes.c_int
     L.leap_rollout_stats.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P]
+    L.leap_probe_mfma.restype = ctypes.c_int
+    L.leap_probe_mfma.argtypes = [i64, i32, i32, P, P]
     L.leap_probe_hbm.restype = ctypes.c_int
     L.leap_probe_hbm.argtypes = [P, P, ctypes.c_size_t, i32, P]
     _lib = L
@@ -350,3 +353,9 @@ def leap_probe_hbm(src, dst, nbytes, mode, stream=None) -> None:
     st = lib().leap_probe_hbm(_ptr(src, None, "src"), _ptr(dst, None, "dst"), int(nbytes),
                               int(mode), _stream(stream))
     _check(st, "leap_probe_hbm")
+
+
+def leap_probe_mfma(iters, n_workgroups, sink, random_operands=0, stream=None) -> None:
+    st = lib().leap_probe_mfma(int(iters), int(n_workgroups), int(random_operands),
+                               _ptr(sink, "float32", "sink"), _stream(stream))
+    _check(st, "leap_probe_mfma")

@@ -230,6 +230,11 @@ def test_probe_rejects():
     with pytest.raises(L.LeapError) as e:
         L.leap_probe_hbm(FAKE + 4, FAKE, 16, 0, stream=0)
     assert e.value.status == L.LEAP_ERR_MISALIGNED
+    for iters, wgs, sink, rnd in ((0, 4, FAKE, 0), (10, 0, FAKE, 0), (10, 4, None, 0),
+                                  (10, 4, FAKE, 2), (10, 4, FAKE, -1)):
+        with pytest.raises(L.LeapError) as e:
+            L.leap_probe_mfma(iters, wgs, sink, random_operands=rnd, stream=0)
+        assert e.value.status == L.LEAP_ERR_INVALID_ARG
 
 
 def _lmhead(**kw):
