@@ -275,13 +275,16 @@ def test_entropy_closed_forms():
     # uniform logits: ln V; a point mass: 0; two finite columns: the binary
     # entropy of p = 1 / (1 + e^b)
     V = 4096
+    def bits(v):  # one bf16 bit pattern
+        return int(wl.f32_to_bf16_bits(np.float32(v))[0])
+
     lg = np.full((4, V), NEG_INF, np.uint16)
-    lg[0, :] = wl.f32_to_bf16_bits(np.float32(1.5))
-    lg[1, 17] = wl.f32_to_bf16_bits(np.float32(-3.0))
+    lg[0, :] = bits(1.5)
+    lg[1, 17] = bits(-3.0)
     b = 1.25  # exact in bf16
-    lg[2, 3] = wl.f32_to_bf16_bits(np.float32(0.0))
-    lg[2, 4000] = wl.f32_to_bf16_bits(np.float32(b))
-    lg[3, :] = wl.f32_to_bf16_bits(np.float32(0.0))
+    lg[2, 3] = bits(0.0)
+    lg[2, 4000] = bits(b)
+    lg[3, :] = bits(0.0)
     lg[3, 0] = NEG_INF  # V - 1 equal columns
     h, bad = oracle.entropy_rows(lg)
     assert bad == 0
