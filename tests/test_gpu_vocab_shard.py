@@ -213,3 +213,52 @@ def test_shards_entropy(widths, inv_temp):
     valid = w != 0
     assert np.all(a["entropy"][~valid] == 0)
     np.testing.assert_allclose(a["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)
+
+
+# Shard widths at both ends of every entry of the stats kernel's shape table
+# (chunks of 8 columns: one past the previous entry's cover, and the entry's
+# own cover, the latter with a partial last chunk), plus the streaming form.
+_STATS_COVERS = [64, 128, 256, 512, 1024, 2048, 2560, 3072, 4096, 5120, 6144, 8192, 9728, 12288,
+                 16384, 19456, 20480, 24576]
+_STATS_WIDTHS = sorted({w for lo, hi in zip([0] + _STATS_COVERS[:-1], _STATS_COVERS)
+                        for w in (8 * lo + 1, 8 * hi - 3)} | {8 * 24576 + 8})
+
+
+@pytest.mark.parametrize("width", _STATS_WIDTHS)
+def test_stats_every_shape(width):
+    """Each shape of the shard stats kernel against ``oracle.vocab_shard_stats``,
+    and its entropy partial t against the whole-row entropy, which for a
+    single shard is ln 2 (log2 s - t / s)."""
+    import torch
+    from paper_2608_01804_amd import leap as L
+    N = 24
+    U.log(f"shard stats width {width}")
+    lg = wl.logits_host(3105 + width % 1000, N, width)
+    tok = wl.sample_tokens_host(lg, width, 3105)
+    lg[1, ::5] = 0xFF80  # -inf columns
+    lg[2, :] = 0xFF80  # an all -inf row
+    tok[3] = width - 1  # the last column, inside the partial chunk when there is one
+    w = np.ones(N, np.float32)
+    w[4] = 0.0
+    ld = (width + 7) // 8 * 8
+    buf = np.zeros((N, ld), np.uint16)
+    buf[:, :width] = lg
+    t = torch.from_numpy(buf.view(np.int16)).to(U.dev()).view(torch.bfloat16)
+    tok_d, w_d = U.T(tok.astype(np.int32)), U.T(w)
+    inv_temp = 0.8
+    parts = torch.full((N, 4), float("nan"), dtype=torch.float32, device=U.dev())
+    parts_t = torch.full((N,), float("nan"), dtype=torch.float32, device=U.dev())
+    L.leap_vocab_shard_stats(t, ld, N, width, 0, tok_d, w_d, inv_temp, parts, partial_t=parts_t)
+    q, qt = parts.cpu().numpy(), parts_t.cpu().numpy()
+    m2, s, zy, owned = oracle.vocab_shard_stats(lg, 0, tok, w=w, inv_temp=inv_temp)
+    np.testing.assert_array_equal(q[:, 3], owned)
+    np.testing.assert_array_equal(q[:, 2], np.where(owned == 1, zy, 0))
+    live = np.isfinite(m2)
+    assert not live[2] and not live[4]
+    assert np.all(q[~live, 0] == -np.inf) and np.all(q[~live, 1] == 0) and np.all(qt[~live] == 0)
+    np.testing.assert_allclose(q[live, 0], m2[live], rtol=1e-6, atol=1e-6)
+    np.testing.assert_allclose(q[live, 1], s[live], rtol=2e-5)
+    h, bad = oracle.entropy_rows(lg[live], V=width, inv_temp=inv_temp)
+    assert bad == 0
+    got_h = np.log(2.0) * (np.log2(q[live, 1].astype(np.float64)) - qt[live] / q[live, 1])
+    np.testing.assert_allclose(got_h, h, rtol=1e-4, atol=2e-4)
