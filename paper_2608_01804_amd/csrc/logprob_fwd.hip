@@ -8,6 +8,7 @@
 // streaming online-softmax variant beyond that.  Only 2V bytes are read and 4
 // written per row (8 with the optional per-row entropy, which adds a third
 // accumulator t = sum 2^d * d beside the sum-exp: the ENT variants).
+#include "read_only_shapes.h"
 #include "row_common.h"
 
 namespace leap {
@@ -194,18 +195,12 @@ struct FwdConfig {
 };
 
 #define LEAP_FWD(B, C, S) \
-    FwdConfig{logprob_rows_resident<B, C, S, false>, logprob_rows_resident<B, C, S, true>, B}
+    FwdConfig{logprob_rows_resident<B, C, S, false>, logprob_rows_resident<B, C, S, true>, B},
 
 FwdConfig pick_fwd_config(int V) {
-    static const FwdConfig table[] = {
-        LEAP_FWD(64, 1, 0),     LEAP_FWD(64, 2, 1),     LEAP_FWD(64, 4, 2),
-        LEAP_FWD(64, 8, 4),     LEAP_FWD(256, 4, 0),    LEAP_FWD(256, 8, 4),
-        LEAP_FWD(256, 12, 8),   LEAP_FWD(256, 16, 12),  LEAP_FWD(1024, 8, 0),
-        LEAP_FWD(1024, 12, 8),  LEAP_FWD(1024, 16, 12), LEAP_FWD(1024, 19, 16),
-        LEAP_FWD(1024, 20, 19), LEAP_FWD(1024, 24, 20),
-    };
-    static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
-    const int i = pick_resident_shape(V);
+    static const FwdConfig table[] = {LEAP_READ_ONLY_SHAPES(LEAP_FWD)};
+    static_assert(sizeof(table) / sizeof(table[0]) == kNumReadOnlyShapes, "shape table");
+    const int i = pick_read_only_shape(V);
     if (i < 0) return FwdConfig{logprob_rows_stream<1024, false>, logprob_rows_stream<1024, true>, 1024};
     return table[i];
 }

@@ -17,6 +17,7 @@
 //    dlogits = g * (onehot - 2^(x c - lse2)); excluded rows are zero-filled
 //    without reading the logits.
 #include "objective.h"
+#include "read_only_shapes.h"
 #include "row_common.h"
 
 namespace leap {
@@ -181,34 +182,17 @@ struct StatsConfig {
     StatsKernel fn;      // without the entropy partial
     StatsKernel fn_ent;  // with it
     int block;
-    int cover;  // chunks the shape holds: block * ch
 };
 
-#define LEAP_SHARD(B, C, S)                                                                     \
-    StatsConfig {                                                                               \
-        shard_stats_resident<B, C, S, false>, shard_stats_resident<B, C, S, true>, B, (B) * (C) \
-    }
+#define LEAP_SHARD(B, C, S) \
+    StatsConfig{shard_stats_resident<B, C, S, false>, shard_stats_resident<B, C, S, true>, B},
 
-// The read-only stats pass has its own shape table: from 4096 to 9728
-// chunks per row (shards of 32768-77824 columns) 512-lane workgroups with
-// most of their slots full beat the 1024-lane shapes the fused kernel uses
-// there (37984 columns: 0.80 of 8 TB/s against 0.62), and 512 x 5 beats
-// 256 x 12 just above 2048 chunks.  Each entry serves the rows longer than
-// the entry before it covers; SAFE is that cover divided by the entry's
-// block (rounded down), so its leading slots are provably full.
 StatsConfig pick_stats_config(int V) {
-    static const StatsConfig table[] = {
-        LEAP_SHARD(64, 1, 0),     LEAP_SHARD(64, 2, 1),     LEAP_SHARD(64, 4, 2),
-        LEAP_SHARD(64, 8, 4),     LEAP_SHARD(256, 4, 2),    LEAP_SHARD(256, 8, 4),
-        LEAP_SHARD(512, 5, 4),    LEAP_SHARD(256, 12, 10),  LEAP_SHARD(256, 16, 12),
-        LEAP_SHARD(512, 10, 8),   LEAP_SHARD(512, 12, 10),  LEAP_SHARD(512, 16, 12),
-        LEAP_SHARD(512, 19, 16),  LEAP_SHARD(1024, 12, 9),  LEAP_SHARD(1024, 16, 12),
-        LEAP_SHARD(1024, 19, 16), LEAP_SHARD(1024, 20, 19), LEAP_SHARD(1024, 24, 20),
-    };
-    const int64_t nchunks = (static_cast<int64_t>(V) + 7) / 8;
-    for (const StatsConfig& c : table)
-        if (c.cover >= nchunks) return c;
-    return StatsConfig{shard_stats_stream<1024, false>, shard_stats_stream<1024, true>, 1024, 0};
+    static const StatsConfig table[] = {LEAP_READ_ONLY_SHAPES(LEAP_SHARD)};
+    static_assert(sizeof(table) / sizeof(table[0]) == kNumReadOnlyShapes, "shape table");
+    const int i = pick_read_only_shape(V);
+    if (i < 0) return StatsConfig{shard_stats_stream<1024, false>, shard_stats_stream<1024, true>, 1024};
+    return table[i];
 }
 
 #undef LEAP_SHARD

@@ -96,3 +96,31 @@ def test_logprob_fwd_entropy(V, ld, N):
     ok = np.ones(N, bool)
     ok[[2, 3]] = False
     np.testing.assert_allclose(ent[ok], h[ok], rtol=1e-4, atol=2e-4)
+
+
+# Widths at both ends of every entry of the read-only shape table (chunks of
+# 8 columns: one past the previous entry's cover, and the entry's own cover
+# with a partial last chunk), plus the first streaming width.
+_RO_COVERS = [64, 128, 256, 512, 1024, 2048, 2560, 3072, 4096, 5120, 6144, 8192, 9728, 12288,
+              16384, 19456, 20480, 24576]
+_RO_WIDTHS = sorted({w for lo, hi in zip([0] + _RO_COVERS[:-1], _RO_COVERS)
+                     for w in (8 * lo + 1, 8 * hi - 3)} | {8 * 24576 + 8})
+
+
+@pytest.mark.parametrize("V", _RO_WIDTHS)
+def test_logprob_fwd_every_shape(V):
+    """Every shape of the forward pass: log-probs and entropy against the
+    oracle, the token in the row's last (partial) chunk on one row."""
+    N = 16
+    ld = (V + 7) // 8 * 8
+    lg = wl.logits_host(V + 7, N, V, ld)
+    tok = wl.sample_tokens_host(lg, V, V + 7)
+    tok[0] = V - 1
+    U.log(f"logprob_fwd shape V={V}")
+    got, err, ent = _run(U.bf16_device(lg), V, tok, inv_temp=0.9, want_entropy=True)
+    want, bad = oracle.logprob_rows(lg, tok, V=V, inv_temp=0.9)
+    assert err == bad == 0
+    assert np.max(np.abs(got - want)) < 2e-3
+    h, bad = oracle.entropy_rows(lg, V=V, inv_temp=0.9)
+    assert bad == 0
+    np.testing.assert_allclose(ent, h, rtol=1e-4, atol=2e-4)
