@@ -53,6 +53,12 @@ typedef enum leap_status {
     LEAP_ERR_HIP = 5          /* the HIP runtime reported an error at launch */
 } leap_status;
 
+/* Widest row, in columns, that the row entry points (the fused objective,
+ * the forward-only log-prob and the vocabulary-shard calls) accept: every
+ * per-row byte offset they form then fits in 32 bits.  Wider rows are
+ * refused with LEAP_ERR_UNSUPPORTED. */
+#define LEAP_MAX_V 268435456
+
 /* Ordering key of the tournament. */
 typedef enum leap_key_mode {
     /* The paper's order (Sec. 3.2, Eq. 4): first pass on an earlier turn is
@@ -230,7 +236,7 @@ size_t leap_grpo_workspace_size(int64_t N, int32_t V);
  *            taken on an fp16 reading of the bf16 bits, exact below that).
  * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a parameter out of
  * range, a required pointer NULL; LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE;
- * LEAP_ERR_UNSUPPORTED for an unknown kl_type.
+ * LEAP_ERR_UNSUPPORTED for an unknown kl_type or V > LEAP_MAX_V.
  */
 leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, int64_t N,
                                            int32_t V, const int32_t *token_ids,
@@ -286,7 +292,8 @@ leap_status leap_grpo_logprob_loss_fwd_bwd_noalloc(const void *logits_bf16, int6
  * logits counts in *dev_err and gets NaN (log-prob and entropy).  Alignment and range rules as leap_grpo_logprob_loss_fwd_bwd;
  * no workspace.
  * Errors: LEAP_ERR_INVALID_ARG for N < 0, V < 1, ld < V, a non-positive or
- * non-finite inv_temperature, a required pointer NULL; LEAP_ERR_MISALIGNED.
+ * non-finite inv_temperature, a required pointer NULL; LEAP_ERR_MISALIGNED;
+ * LEAP_ERR_UNSUPPORTED for V > LEAP_MAX_V.
  */
 leap_status leap_logprob_fwd(const void *logits_bf16, int64_t ld, int64_t N, int32_t V,
                              const int32_t *token_ids, const float *w_tok,
@@ -366,6 +373,10 @@ leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight
  *   m2 = -inf); needed by leap_vocab_merge_objective's entropy output.
  *   logits_bf16 [N][ld] bf16 holding the shard's V_shard columns; alignment
  *   and range rules as leap_grpo_logprob_loss_fwd_bwd; vocab_start >= 0.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, V_shard < 1, ld < V_shard,
+ * vocab_start < 0, a non-positive or non-finite inv_temperature, a required
+ * pointer NULL; LEAP_ERR_MISALIGNED (logits or partial not 16-byte aligned,
+ * ld % 8 != 0); LEAP_ERR_UNSUPPORTED for V_shard > LEAP_MAX_V.
  */
 leap_status leap_vocab_shard_stats(const void *logits_bf16, int64_t ld, int64_t N, int32_t V_shard,
                                    int32_t vocab_start, const int32_t *token_ids,
@@ -410,6 +421,11 @@ leap_status leap_vocab_merge_objective(const float *partials, const float *parti
  *   from row_state [N][2] of leap_vocab_merge_objective; a row with g == 0 is
  *   zero-filled without reading its logits.  dlogits_bf16 [N][ld] may equal
  *   logits_bf16, must not otherwise overlap it.
+ * Errors: LEAP_ERR_INVALID_ARG for N < 0, V_shard < 1, ld < V_shard,
+ * vocab_start < 0, a non-positive or non-finite inv_temperature, a required
+ * pointer NULL, overlapping logits and dlogits; LEAP_ERR_MISALIGNED (logits,
+ * dlogits not 16-byte aligned, ld % 8 != 0, row_state not 8-byte aligned);
+ * LEAP_ERR_UNSUPPORTED for V_shard > LEAP_MAX_V.
  */
 leap_status leap_vocab_shard_bwd(const void *logits_bf16, int64_t ld, int64_t N, int32_t V_shard,
                                  int32_t vocab_start, const int32_t *token_ids,

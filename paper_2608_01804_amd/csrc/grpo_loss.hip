@@ -712,6 +712,7 @@ leap_status check_fused_args(const void* logits_bf16, int64_t ld, int64_t N, int
         return LEAP_ERR_INVALID_ARG;
     if (pp.kl_type != LEAP_KL_K3 && pp.kl_type != LEAP_KL_K1 && pp.kl_type != LEAP_KL_K2)
         return LEAP_ERR_UNSUPPORTED;
+    if (V > LEAP_MAX_V) return LEAP_ERR_UNSUPPORTED;
     if (N > 0) {
         if (!logits_bf16 || !dlogits_bf16 || !token_ids || !old_logp || !ref_logp || !adv_tok ||
             !w_tok)

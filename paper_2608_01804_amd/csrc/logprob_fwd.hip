@@ -218,6 +218,7 @@ LEAP_API leap_status leap_logprob_fwd(const void* logits_bf16, int64_t ld, int64
     if (N < 0 || V < 1 || ld < V) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
         return LEAP_ERR_INVALID_ARG;
+    if (V > LEAP_MAX_V) return LEAP_ERR_UNSUPPORTED;
     if (N == 0) return LEAP_OK;
     if (!logits_bf16 || !token_ids || !logp_out) return LEAP_ERR_INVALID_ARG;
     if (!aligned16(logits_bf16) || (ld & 7) != 0) return LEAP_ERR_MISALIGNED;

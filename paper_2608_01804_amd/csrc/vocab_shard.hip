@@ -349,6 +349,7 @@ LEAP_API leap_status leap_vocab_shard_stats(const void* logits_bf16, int64_t ld,
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
         return LEAP_ERR_INVALID_ARG;
+    if (V_shard > LEAP_MAX_V) return LEAP_ERR_UNSUPPORTED;
     if (N == 0) return LEAP_OK;
     if (!logits_bf16 || !token_ids || !partial) return LEAP_ERR_INVALID_ARG;
     if (!aligned16(logits_bf16) || (ld & 7) != 0 || !aligned16(partial)) return LEAP_ERR_MISALIGNED;
@@ -416,6 +417,7 @@ LEAP_API leap_status leap_vocab_shard_bwd(const void* logits_bf16, int64_t ld, i
     if (N < 0 || V_shard < 1 || ld < V_shard || vocab_start < 0) return LEAP_ERR_INVALID_ARG;
     if (!(inv_temperature > 0.0f) || !__builtin_isfinite(inv_temperature))
         return LEAP_ERR_INVALID_ARG;
+    if (V_shard > LEAP_MAX_V) return LEAP_ERR_UNSUPPORTED;
     if (N == 0) return LEAP_OK;
     if (!logits_bf16 || !token_ids || !row_state || !dlogits_bf16) return LEAP_ERR_INVALID_ARG;
     if (!aligned16(logits_bf16) || !aligned16(dlogits_bf16) || (ld & 7) != 0 ||

@@ -248,6 +248,7 @@ def leap_grpo_logprob_loss_fwd_bwd(logits, ld, N, V, token_ids, old_logp, ref_lo
 
 
 LEAP_NOALLOC_MAX_ROWS = 1048576
+LEAP_MAX_V = 268435456
 
 
 def leap_grpo_logprob_loss_fwd_bwd_noalloc(logits, ld, N, V, token_ids, old_logp, ref_logp,

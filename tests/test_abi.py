@@ -147,6 +147,8 @@ def _grpo(**kw):
     (dict(workspace=None), L.LEAP_ERR_WORKSPACE),
     (dict(ws_bytes=16), L.LEAP_ERR_WORKSPACE),
     (dict(dlogits=FAKE + 2048), L.LEAP_ERR_INVALID_ARG),  # partial overlap with logits
+    (dict(V=L.LEAP_MAX_V + 1, ld=L.LEAP_MAX_V + 8), L.LEAP_ERR_UNSUPPORTED),
+    (dict(V=L.LEAP_MAX_V + 1, ld=L.LEAP_MAX_V + 8, N=0), L.LEAP_ERR_UNSUPPORTED),
 ])
 def test_grpo_rejects(kw, status):
     with pytest.raises(L.LeapError) as e:
@@ -160,6 +162,7 @@ def test_grpo_rejects(kw, status):
     (dict(loss_out=None), L.LEAP_ERR_INVALID_ARG),
     (dict(logits=FAKE + 2), L.LEAP_ERR_MISALIGNED),
     (dict(dlogits=FAKE + 2048), L.LEAP_ERR_INVALID_ARG),
+    (dict(V=L.LEAP_MAX_V + 1, ld=L.LEAP_MAX_V + 8), L.LEAP_ERR_UNSUPPORTED),
 ])
 def test_grpo_noalloc_rejects(kw, status):
     """The no-allocation form checks its arguments like the workspace form
@@ -212,6 +215,7 @@ def test_binding_refuses_cpu_tensors():
     (dict(logp_out=None), L.LEAP_ERR_INVALID_ARG),
     (dict(logits=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(ld=1012), L.LEAP_ERR_MISALIGNED),
+    (dict(V=L.LEAP_MAX_V + 1, ld=L.LEAP_MAX_V + 8), L.LEAP_ERR_UNSUPPORTED),
 ])
 def test_logprob_fwd_rejects(kw, status):
     a = dict(logits=FAKE, ld=1024, N=8, V=1000, token_ids=FAKE, w_tok=None, inv_temperature=1.0,
@@ -336,6 +340,14 @@ def test_vocab_shard_entry_points_reject():
     with pytest.raises(L.LeapError) as e:
         L.leap_vocab_shard_bwd(FAKE, 1000, 8, 1000, 0, FAKE, FAKE, 1.0, FAKE + 2048, stream=0)
     assert e.value.status == L.LEAP_ERR_INVALID_ARG  # partial overlap with the logits
+    # rows wider than LEAP_MAX_V columns are refused before anything is read
+    wide, ld = L.LEAP_MAX_V + 1, L.LEAP_MAX_V + 8
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_stats(FAKE, ld, 8, wide, 0, FAKE, None, 1.0, FAKE, stream=0)
+    assert e.value.status == L.LEAP_ERR_UNSUPPORTED
+    with pytest.raises(L.LeapError) as e:
+        L.leap_vocab_shard_bwd(FAKE, ld, 8, wide, 0, FAKE, FAKE, 1.0, FAKE + (1 << 40), stream=0)
+    assert e.value.status == L.LEAP_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("kw,status", [
