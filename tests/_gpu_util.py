@@ -142,13 +142,15 @@ def boundary_rows(logp_o, old, eps_lo, eps_hi, A, rel=1e-4):
     return near & (np.asarray(A) != 0)
 
 
-def check_dlogits(gpu_rows, lg_u16, rows, tok, old, ref, adv, w, V, atol, kw, rel_to_max=False):
-    """Compare GPU dlogits rows with the oracle; rows at a clip boundary may
-    match either one-sided gradient."""
+def check_dlogits(gpu_rows, lg_u16, rows, tok, old, ref, adv, w, V, atol, kw, rel_to_max=False,
+                  floor=0.0):
+    """Compare GPU dlogits rows with the oracle (|difference| <= atol, times
+    the largest oracle entry with rel_to_max, plus `floor`); rows at a clip
+    boundary may match either one-sided gradient."""
     o = oracle.grpo_rows(lg_u16, tok, old, ref, adv, w, V=V, rows=rows, **kw)
     ref_d = o["dlogits"]
     scale = np.max(np.abs(ref_d)) if rel_to_max else 1.0
-    lim = atol * scale
+    lim = atol * scale + floor
     sel = np.asarray(rows)
     near = boundary_rows(o["logp"], np.asarray(old, np.float64)[sel], kw.get("eps_lo", 0.2),
                          kw.get("eps_hi", 0.2), np.asarray(adv)[sel])

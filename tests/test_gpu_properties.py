@@ -61,3 +61,74 @@ def test_token_advantages_match_oracle(lay, agg):
     assert bad_o == bad_g == 0
     np.testing.assert_allclose(adv_g, adv_o, rtol=1.2e-7, atol=0)
     np.testing.assert_allclose(w_g, w_o, rtol=1.2e-7, atol=0)
+
+
+@st.composite
+def objective_cases(draw):
+    """One call of the fused objective: vocabulary width (every register
+    shape of the kernel up to 65536 columns, odd widths included), padded
+    row stride, rows, clip bounds (asymmetric), KL type and weight,
+    temperature, old-policy spread, masked rows, bad token ids, -inf
+    logits and the optional entropy output."""
+    V = draw(st.one_of(st.integers(1, 700), st.integers(701, 40000),
+                       st.sampled_from([16384, 32768, 50257, 65536])))
+    ld = (V + 7) // 8 * 8 + draw(st.sampled_from([0, 8, 64]))
+    return dict(
+        V=V, ld=ld, N=draw(st.integers(1, 40)), seed=draw(st.integers(0, 2**31 - 1)),
+        eps_lo=draw(st.floats(0.0, 0.5)), eps_hi=draw(st.floats(0.0, 0.5)),
+        kl_coef=draw(st.floats(0.0, 0.5)),
+        kl_type=draw(st.sampled_from([oracle.KL_K3, oracle.KL_K1, oracle.KL_K2])),
+        inv_temp=draw(st.floats(0.5, 2.0)), old_sigma=draw(st.sampled_from([0.05, 0.3])),
+        p_masked=draw(st.floats(0.0, 0.5)), n_bad=draw(st.integers(0, 2)),
+        p_ninf=draw(st.sampled_from([0.0, 0.0, 0.01, 0.3])), entropy=draw(st.booleans()))
+
+
+@settings(max_examples=40, deadline=None,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(objective_cases())
+def test_fused_objective_matches_oracle(c):
+    """The fused call against the oracle on random shapes and parameters:
+    log-probs within 2e-3, per-token losses 2e-3 relative, the loss 1e-3
+    relative, dlogits within 1e-2 of the largest entry plus 1e-6 (a
+    boundary row may match either one-sided gradient), the entropy 1e-4
+    relative, and the data-error count exact."""
+    V, ld, N = c["V"], c["ld"], c["N"]
+    rng = np.random.default_rng(c["seed"])
+
+    def edit(lg, tok):
+        if c["p_ninf"] > 0:
+            keep = lg[np.arange(N), np.clip(tok, 0, V - 1)].copy()
+            lg[:, :V][rng.random((N, V)) < c["p_ninf"]] = 0xFF80  # -inf
+            lg[np.arange(N), np.clip(tok, 0, V - 1)] = keep  # the token's own logit stays
+
+    lg, tok, old, ref = U.make_inputs_host(c["seed"] % 100000, N, V, ld=ld,
+                                           old_sigma=c["old_sigma"], edit=edit)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = rng.uniform(0.1, 1.0, N).astype(np.float32)
+    w[rng.random(N) < c["p_masked"]] = 0.0
+    for k in rng.choice(N, size=min(c["n_bad"], N), replace=False):
+        tok[k] = -1 if rng.random() < 0.5 else V
+    kw = dict(eps_lo=c["eps_lo"], eps_hi=c["eps_hi"], kl_coef=c["kl_coef"],
+              kl_type=c["kl_type"], inv_temp=c["inv_temp"])
+    U.log(f"fused objective property case V={V} ld={ld} N={N} {kw}")
+    gpu = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, want_entropy=c["entropy"], **kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **kw)
+    valid = (w != 0) & (tok >= 0) & (tok < V)
+    assert gpu["bad"] == o["bad"] == int(((w != 0) & ~valid).sum())
+    assert np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0) < 2e-3
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-6
+    rows = np.arange(N)
+    d = U.dl_rows(gpu["dl_dev"], rows, V)
+    assert np.all(d[~valid] == 0)
+    # floor: the fp32 log-sum-exp leaves log-probs ~1e-7 of the logits' size
+    # from the fp64 values, which shows as g * 1e-7 in entries the oracle
+    # makes exactly 0 (a one-column row: p = 1, dlogits = 0)
+    U.check_dlogits(d, lg, rows, tok, old, ref, adv, w, V, atol=1e-2, kw=kw, rel_to_max=True,
+                    floor=1e-6)
+    if c["entropy"]:
+        h, _ = oracle.entropy_rows(lg, V=V, inv_temp=c["inv_temp"])
+        assert np.all(gpu["entropy"][~valid] == 0)
+        np.testing.assert_allclose(gpu["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)
