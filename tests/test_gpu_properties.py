@@ -10,6 +10,7 @@ from hypothesis import HealthCheck, given, settings
 from hypothesis import strategies as st
 
 import oracle
+import workloads as wl
 from tests import _gpu_util as U
 from tests.test_oracle_properties import groups, token_layouts
 
@@ -132,3 +133,100 @@ def test_fused_objective_matches_oracle(c):
         h, _ = oracle.entropy_rows(lg, V=V, inv_temp=c["inv_temp"])
         assert np.all(gpu["entropy"][~valid] == 0)
         np.testing.assert_allclose(gpu["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)
+
+
+@st.composite
+def shard_cases(draw):
+    """A vocabulary split into 1-8 shards of random widths (one column
+    upwards), with the objective's parameters drawn as for the fused call
+    (temperature up to 1.5 and advantages within [-2, 2], so that bf16
+    rounding of the largest gradient entries stays inside 2e-2)."""
+    n = draw(st.integers(1, 8))
+    widths = draw(st.lists(st.one_of(st.integers(1, 64), st.integers(65, 12000)), min_size=n,
+                           max_size=n))
+    return dict(widths=widths, V=sum(widths), N=draw(st.integers(1, 24)),
+                seed=draw(st.integers(0, 2**31 - 1)),
+                eps_lo=draw(st.floats(0.0, 0.5)), eps_hi=draw(st.floats(0.0, 0.5)),
+                kl_coef=draw(st.floats(0.0, 0.5)),
+                kl_type=draw(st.sampled_from([oracle.KL_K3, oracle.KL_K1, oracle.KL_K2])),
+                inv_temp=draw(st.floats(0.5, 1.5)), p_masked=draw(st.floats(0.0, 0.5)),
+                inplace=draw(st.booleans()))
+
+
+@settings(max_examples=30, deadline=None,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(shard_cases())
+def test_vocab_shards_match_unsharded_oracle(c):
+    """Any split of the vocabulary: each shard's partial against the shard
+    oracle, the merged objective against the unsharded oracle (log-probs
+    2e-3, per-token losses 2e-3 relative, the loss 1e-3 relative) and the
+    concatenated dlogits within 2e-2 of it (a row at a clip boundary may
+    match either one-sided gradient)."""
+    from tests import test_gpu_vocab_shard as S
+    V, N = c["V"], c["N"]
+    rng = np.random.default_rng(c["seed"])
+    lg = wl.logits_host(c["seed"] % 100000, N, V)
+    tok = wl.sample_tokens_host(lg, V, c["seed"] % 100000)
+    cur, _ = oracle.logprob_rows(lg, tok, V=V)
+    old = (cur + rng.normal(0, 0.2, N)).astype(np.float32)
+    ref = (cur + rng.normal(0, 0.1, N)).astype(np.float32)
+    adv = np.clip(rng.normal(0, 1, N), -2, 2).astype(np.float32)
+    w = np.ones(N, np.float32)
+    w[rng.random(N) < c["p_masked"]] = 0.0
+    kw = dict(eps_lo=c["eps_lo"], eps_hi=c["eps_hi"], kl_coef=c["kl_coef"],
+              kl_type=c["kl_type"], inv_temp=c["inv_temp"])
+    shards = S._shards(V, c["widths"])
+    U.log(f"vocab shard property case widths={c['widths']} N={N} {kw}")
+    gpu = S._run(lg, V, tok, old, ref, adv, w, shards, kw, inplace=c["inplace"])
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **kw)
+    valid = w != 0
+    assert gpu["bad"] == o["bad"] == 0
+    assert np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0) < 2e-3
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-6
+    d = U.bf16_f64(gpu["dl"])
+    assert np.all(d[~valid] == 0)
+    U.check_dlogits(d, lg, np.arange(N), tok, old, ref, adv, w, V, atol=2e-2, kw=kw)
+    for k, (a, width) in enumerate(shards):
+        m2, s, zy, owned = oracle.vocab_shard_stats(lg[:, a:a + width], a, tok, w=w,
+                                                    inv_temp=kw["inv_temp"])
+        q = gpu["parts"][k]
+        np.testing.assert_array_equal(q[:, 3], owned)
+        np.testing.assert_array_equal(q[:, 2], np.where(owned == 1, zy, 0))
+        live = np.isfinite(m2)
+        assert np.all(q[~live, 0] == -np.inf) and np.all(q[~live, 1] == 0)
+        np.testing.assert_allclose(q[live, 0], m2[live], rtol=1e-6, atol=1e-6)
+        np.testing.assert_allclose(q[live, 1], s[live], rtol=2e-5)
+
+
+@settings(max_examples=30, deadline=None,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(st.one_of(st.integers(1, 700), st.integers(701, 70000)), st.sampled_from([0, 8, 64]),
+       st.integers(1, 32), st.integers(0, 2**31 - 1), st.floats(0.5, 2.0),
+       st.sampled_from([0.0, 0.01, 0.3]), st.booleans())
+def test_logprob_fwd_matches_oracle(V, pad, N, seed, inv_temp, p_ninf, masked):
+    """The forward-only pass on random widths, strides, temperatures, -inf
+    logits and weight masks: log-probs within 2e-3 and entropies 1e-4
+    relative of the oracle's; masked rows 0."""
+    from tests import test_gpu_logprob_fwd as F
+    rng = np.random.default_rng(seed)
+    ld = (V + 7) // 8 * 8 + pad
+    lg = wl.logits_host(seed % 100000, N, V, ld)
+    tok = wl.sample_tokens_host(lg, V, seed % 100000)
+    if p_ninf > 0:
+        keep = lg[np.arange(N), tok].copy()
+        lg[:, :V][rng.random((N, V)) < p_ninf] = 0xFF80
+        lg[np.arange(N), tok] = keep
+    w = (rng.random(N) >= 0.3).astype(np.float32) if masked else None
+    U.log(f"logprob_fwd property case V={V} ld={ld} N={N} T^-1={inv_temp}")
+    got, err, ent = F._run(U.bf16_device(lg), V, tok, w=w, inv_temp=inv_temp, want_entropy=True)
+    want, bad = oracle.logprob_rows(lg, tok, V=V, inv_temp=inv_temp)
+    h, _ = oracle.entropy_rows(lg, V=V, inv_temp=inv_temp)
+    assert err == bad == 0
+    live = np.ones(N, bool) if w is None else w != 0
+    assert np.all(got[~live] == 0) and np.all(ent[~live] == 0)
+    assert np.max(np.abs(got[live] - want[live]), initial=0) < 2e-3
+    np.testing.assert_allclose(ent[live], h[live], rtol=1e-4, atol=2e-4)
