@@ -300,8 +300,31 @@ leap_status leap_logprob_fwd(const void *logits_bf16, int64_t ld, int64_t N, int
                              float inv_temperature, float *logp_out, float *entropy_out,
                              int32_t *dev_err, hipStream_t stream);
 
-/* Workspace bytes leap_grpo_lmhead_fwd_bwd needs (0 for invalid sizes). */
+/* Workspace bytes leap_grpo_lmhead_fwd_bwd needs (0 for invalid sizes).
+ * Called with a prepared transposed weight (weight_t_bf16), it needs
+ * leap_lmhead_workspace_size(N, V, H) - leap_lmhead_weight_t_size(V, H)
+ * bytes only. */
 size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
+
+/* Bytes of the transposed weight leap_lmhead_transpose_weight writes:
+ * H x V_pad bf16, V_pad = V rounded up to a multiple of 256 (0 for invalid
+ * sizes). */
+size_t leap_lmhead_weight_t_size(int32_t V, int32_t H);
+
+/*
+ * The transposed LM-head weight that leap_grpo_lmhead_fwd_bwd's dhidden
+ * product reads: weight_t[h][v] = weight[v][h] for v < V, 0 for V <= v <
+ * V_pad, bf16 [H][V_pad].  The weight changes only at an optimizer step, so
+ * one transpose can serve every microbatch of a step (pass it as
+ * weight_t_bf16); without it each call forms its own copy in the workspace.
+ * weight_bf16 [V][H] and weight_t_bf16 16-byte aligned, bytes >=
+ * leap_lmhead_weight_t_size(V, H), caller-owned.
+ * Errors: LEAP_ERR_INVALID_ARG for V < 1, H < 1, a NULL pointer;
+ * LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE for too few bytes;
+ * LEAP_ERR_UNSUPPORTED for H % 64 != 0 or a weight of 4 GiB or more.
+ */
+leap_status leap_lmhead_transpose_weight(const void *weight_bf16, int32_t V, int32_t H,
+                                         void *weight_t_bf16, size_t bytes, hipStream_t stream);
 
 /*
  * Fused LM head + per-token GRPO objective (Sec. 3.1, Eq. 3, per token):
@@ -317,10 +340,18 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  * (RNE) before the two gradient products.  logp, tok_loss, loss and g follow
  * the rules of leap_grpo_logprob_loss_fwd_bwd, including excluded rows
  * (w == 0: zero gradient rows, logp_out = tok_loss_out = 0) and bad token
- * ids (counted in *dev_err, excluded).
+ * ids (counted in *dev_err, excluded).  Excluded rows take no part in the
+ * products: the call lists the rows with w != 0 on the device and runs its
+ * GEMMs over those only, so an excluded row's hidden state is never read
+ * (non-finite values there reach no output) and costs no matrix work.
  *
  * hidden_bf16 [N][H] bf16, weight_bf16 [V][H] bf16, both row-major, 16-byte
  *              aligned.  H % 64 == 0 (else LEAP_ERR_UNSUPPORTED).
+ * weight_t_bf16  nullable: leap_lmhead_transpose_weight's output for this
+ *              weight (16-byte aligned); the call then skips its own
+ *              transpose and does not need the workspace's last
+ *              leap_lmhead_weight_t_size(V, H) bytes.  Results are
+ *              bitwise the same either way.
  * token_ids int32 [N]; old_logp, ref_logp, adv_tok, w_tok float [N].
  * logp_out, tok_loss_out  float [N], nullable.  loss_out float [1], required.
  * dhidden    float [N][H], 16-byte aligned, overwritten; NULL skips it.
@@ -330,8 +361,8 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  * workspace  device buffer of >= leap_lmhead_workspace_size(N, V, H) bytes,
  *            16-byte aligned, scratch for this call only (calls sharing one
  *            workspace must be ordered on one stream).  It holds the
- *            transposed operands, per-tile row statistics and one vocabulary
- *            chunk of dZ (bf16, row-major).
+ *            gathered and transposed operands, per-tile row statistics, the
+ *            live-row list and one vocabulary chunk of dZ (bf16, row-major).
  * Limits: each operand and workspace matrix below 4 GiB (32-bit offsets in
  * the GEMM core): for H = 4096, V up to about 520000, and N up to 130816
  * once V reaches 16384 (a dZ chunk holds N_pad x 16384 bf16; chunks are
@@ -340,8 +371,9 @@ size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H);
  * not 0 or 1, a parameter out of range, a required pointer NULL;
  * LEAP_ERR_MISALIGNED; LEAP_ERR_WORKSPACE; LEAP_ERR_UNSUPPORTED.
  */
-leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight_bf16, int64_t N,
-                                     int32_t V, int32_t H, const int32_t *token_ids,
+leap_status leap_grpo_lmhead_fwd_bwd(const void *hidden_bf16, const void *weight_bf16,
+                                     const void *weight_t_bf16, int64_t N, int32_t V, int32_t H,
+                                     const int32_t *token_ids,
                                      const float *old_logp, const float *ref_logp,
                                      const float *adv_tok, const float *w_tok,
                                      const leap_grpo_params *params, float *logp_out,

@@ -4,23 +4,32 @@
 // gradients dH = dZ W and dW = dZ^T H, where dZ = d(sum_k w_k l_k)/dz.
 //
 // Steps of one call, all on the caller's stream:
-//  1. H and W are transposed once into the workspace (Ht [H][N_pad]; Wt
-//     chunk-major, [chunk][H][chunk width]; both zero padded), because the
-//     GEMM core takes B contiguous along the contraction index (and A either
-//     way: contiguous along it, or k-major through transposing LDS reads).
-//  2. Stats GEMM  Z = H W^T on MFMA.  Its epilogue turns every row of a
+//  0. Excluded rows (w == 0: padding, prompt and feedback tokens) take no
+//     part in the objective or the gradients, so the call drops them first:
+//     a two-kernel compaction lists the live rows in order (rows[j], j <
+//     n_live; -1 after) and gives the excluded rows their zero outputs.
+//     Every GEMM below runs over the n_live compacted rows only; its grid is
+//     sized for N and the tiles past n_live (a device count) exit at once.
+//  1. The live rows of H are gathered into Hc [N_pad][H] and, for dW, into
+//     Ht [H][N_pad]; W is transposed into Wt [H][V_pad] for dH (all zero
+//     padded), because the GEMM core takes B contiguous along the
+//     contraction index (and A either way: contiguous along it, or k-major
+//     through transposing LDS reads).
+//  2. Stats GEMM  Z = Hc W^T on MFMA.  Its epilogue turns every row of a
 //     256 x 256 tile into a partial (max, sum 2^(z c - max)) in base-2 units
-//     (c = log2(e) / T) and picks out the rollout token's logit.
-//  3. Combine: one wave per row merges the row's partials in a fixed order
-//     into the log-sum-exp and evaluates the same per-token objective as the
+//     (c = log2(e) / T).
+//  3. Combine: one wave per live row merges the row's partials in a fixed
+//     order into the log-sum-exp, forms the rollout token's logit as a dot
+//     product and evaluates the same per-token objective as the
 //     logits-resident kernel (log-prob, ratio, surrogate, KL, loss and
 //     g = w dloss/dlogp / T).  A fixed-order reduction sums the loss.
 //  4. Per vocabulary chunk (32768 columns, 16384 for very large N): the Z
 //     tiles are recomputed and the epilogue writes dZ = g (onehot - p) in
-//     bf16, row-major [N_pad][chunk]; then dW[chunk] = dZ^T H (dZ read
+//     bf16, row-major [n_live rows][chunk]; then dW[chunk] = dZ^T Hc (dZ read
 //     k-major) and dH (+)= dZ W[chunk] run as two more GEMMs with fp32
-//     epilogues.
-// Executed work is 8 N H V flops (the forward GEMM is recomputed once).
+//     epilogues, dH scattered back to the live rows' places; the excluded
+//     rows of dH are written as zeros.
+// Executed work is 8 n_live H V flops (the forward GEMM is recomputed once).
 #include "mfma_gemm.h"
 #include "row_common.h"
 
@@ -57,15 +66,111 @@ struct Flag {
 };
 
 // ---------------------------------------------------------------------------
-// Transpose with zero padding: dst[c][r] = src[r][c] for r < R, and 0 for
-// R <= r < ld_dst, for every c < C.  64 x 64 tiles through LDS; C % 8 == 0.
+// Live-row compaction.  Live row: w != 0 (a live row with a bad token id
+// stays in the list; the combine kernel counts and excludes it).  Pass 1
+// counts the live rows of each segment of kSeg rows; pass 2 gives each
+// segment its base (the counts before it, in order), lists its live rows in
+// row order, writes the excluded rows' outputs (log-prob, per-token loss and
+// weighted loss 0), and fills the list's tail with -1 up to N_pad.
+// ---------------------------------------------------------------------------
+constexpr int kSeg = 4096;
+constexpr int kSegThreads = 256;
+constexpr int kSegRowsPerThread = kSeg / kSegThreads;  // 16 consecutive rows
+
+__device__ __forceinline__ int block_sum_256(int v, int* s_part) {
+    v = wave_sum_i32(v);
+    const int tid = threadIdx.x;
+    __syncthreads();  // s_part may still be read by an earlier call
+    if ((tid & (kWave - 1)) == 0) s_part[tid / kWave] = v;
+    __syncthreads();
+    return s_part[0] + s_part[1] + s_part[2] + s_part[3];
+}
+
+__global__ __launch_bounds__(kSegThreads) void live_count_kernel(const float* __restrict__ w_tok,
+                                                                 int64_t N,
+                                                                 int32_t* __restrict__ seg_count) {
+    __shared__ int s_part[kSegThreads / kWave];
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kSeg;
+    int c = 0;
+    for (int i = threadIdx.x; i < kSeg; i += kSegThreads) {
+        const int64_t r = r0 + i;
+        if (r < N && w_tok[r] != 0.0f) ++c;
+    }
+    c = block_sum_256(c, s_part);
+    if (threadIdx.x == 0) seg_count[blockIdx.x] = c;
+}
+
+__global__ __launch_bounds__(kSegThreads) void compact_rows_kernel(
+    const float* __restrict__ w_tok, int64_t N, int64_t N_pad, const int32_t* __restrict__ seg_count,
+    int n_seg, int32_t* __restrict__ rows, int32_t* __restrict__ n_live,
+    float* __restrict__ logp_out, float* __restrict__ tok_loss_out, float* __restrict__ row_loss) {
+    __shared__ int s_part[kSegThreads / kWave];
+    __shared__ int s_scan[kSegThreads / kWave];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int b = blockIdx.x;
+    int before = 0, all = 0;
+    for (int i = tid; i < n_seg; i += kSegThreads) {
+        const int c = seg_count[i];
+        all += c;
+        if (i < b) before += c;
+    }
+    const int base = block_sum_256(before, s_part);
+    const int total = block_sum_256(all, s_part);
+    // this thread's 16 consecutive rows
+    const int64_t r0 = static_cast<int64_t>(b) * kSeg + static_cast<int64_t>(tid) * kSegRowsPerThread;
+    uint32_t live = 0;
+#pragma unroll
+    for (int e = 0; e < kSegRowsPerThread; ++e) {
+        const int64_t r = r0 + e;
+        if (r < N && w_tok[r] != 0.0f) live |= 1u << e;
+    }
+    // exclusive scan of the per-thread counts over the block, in thread order
+    const int cnt = __popc(live);
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int up = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += up;
+    }
+    if (lane == kWave - 1) s_scan[wave] = incl;
+    __syncthreads();
+    int pos = base + incl - cnt;
+    for (int w = 0; w < wave; ++w) pos += s_scan[w];
+#pragma unroll
+    for (int e = 0; e < kSegRowsPerThread; ++e) {
+        const int64_t r = r0 + e;
+        if (r >= N) break;
+        if (live & (1u << e)) {
+            rows[pos++] = static_cast<int32_t>(r);
+        } else {
+            if (logp_out) logp_out[r] = 0.0f;
+            if (tok_loss_out) tok_loss_out[r] = 0.0f;
+            row_loss[r] = 0.0f;
+        }
+    }
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kSegThreads;
+    for (int64_t j = total + static_cast<int64_t>(b) * kSegThreads + tid; j < N_pad; j += stride)
+        rows[j] = -1;
+    if (b == 0 && tid == 0) *n_live = total;
+}
+
+// ---------------------------------------------------------------------------
+// Transpose with zero padding, optionally through a row list:
+// dst[c][r] = src[s(r)][c] for r < R, and 0 for R <= r < ld_dst, for every
+// c < C, where s(r) = r without a list, or s(r) = rows[r] with one (-1: a
+// zero row).  With rows_out, the (gathered) rows are also written as they
+// are: rows_out[r][c] = src[s(r)][c].  dst may be null (rows_out only).
+// 64 x 64 tiles through LDS; C % 8 == 0.
 // ---------------------------------------------------------------------------
 constexpr int kTr = 64;
 
 __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __restrict__ src,
                                                             int64_t R, int C, int64_t ld_src,
+                                                            const int32_t* __restrict__ rows,
                                                             uint16_t* __restrict__ dst,
-                                                            int64_t ld_dst) {
+                                                            int64_t ld_dst,
+                                                            uint16_t* __restrict__ rows_out,
+                                                            int64_t ld_out) {
     __shared__ uint32_t t[kTr][kTr / 2 + 1];  // row r of the tile: 64 bf16 packed in pairs
     const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTr;
     const int c0 = blockIdx.y * kTr;
@@ -73,16 +178,24 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
     {
         const int rr = tid >> 2, cc = (tid & 3) * 16;
         const int64_t r = r0 + rr;
+        int64_t sr = -1;
+        if (r < R) sr = rows ? static_cast<int64_t>(rows[r]) : r;
         u32x4 a = {0u, 0u, 0u, 0u}, b = {0u, 0u, 0u, 0u};
-        if (r < R) {
-            const uint16_t* p = src + r * ld_src + c0 + cc;
+        if (sr >= 0) {
+            const uint16_t* p = src + sr * ld_src + c0 + cc;
             if (c0 + cc < C) a = *reinterpret_cast<const u32x4*>(p);
             if (c0 + cc + 8 < C) b = *reinterpret_cast<const u32x4*>(p + 8);
+        }
+        if (rows_out && r < R) {
+            uint16_t* q = rows_out + r * ld_out + c0 + cc;
+            if (c0 + cc < C) *reinterpret_cast<u32x4*>(q) = a;
+            if (c0 + cc + 8 < C) *reinterpret_cast<u32x4*>(q + 8) = b;
         }
         uint32_t* d = &t[rr][cc / 2];
         d[0] = a.x, d[1] = a.y, d[2] = a.z, d[3] = a.w;
         d[4] = b.x, d[5] = b.y, d[6] = b.z, d[7] = b.w;
     }
+    if (!dst) return;  // uniform: the whole grid writes rows only
     __syncthreads();
     const int cc = tid >> 2, rr = (tid & 3) * 16;
     if (c0 + cc >= C) return;
@@ -95,6 +208,18 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const uint16_t* __re
     uint16_t* q = dst + static_cast<int64_t>(c0 + cc) * ld_dst + r0 + rr;
     *reinterpret_cast<u32x4*>(q) = u32x4{w[0], w[1], w[2], w[3]};
     *reinterpret_cast<u32x4*>(q + 8) = u32x4{w[4], w[5], w[6], w[7]};
+}
+
+// Zero the rows of an [N][H] fp32 matrix whose weight is 0 (the excluded
+// rows of dH); one workgroup per row, 16-byte stores (H % 64 == 0).
+__global__ __launch_bounds__(256) void zero_excluded_rows_kernel(float* __restrict__ C, int H,
+                                                                 const float* __restrict__ w_tok,
+                                                                 int64_t N) {
+    for (int64_t r = blockIdx.x; r < N; r += gridDim.x) {
+        if (w_tok[r] != 0.0f) continue;
+        f32x4* p = reinterpret_cast<f32x4*>(C + r * H);
+        for (int c = threadIdx.x; c < H / 4; c += 256) __builtin_nontemporal_store(f32x4{}, p + c);
+    }
 }
 
 __global__ __launch_bounds__(256) void fill_zero_f32_kernel(float* __restrict__ p, int64_t n) {
@@ -229,21 +354,24 @@ struct StatsEpi {
 // ---------------------------------------------------------------------------
 // Combine: one wave per row.
 // ---------------------------------------------------------------------------
+// Compacted row j (of n_rows = N_pad) is caller row rows[j]; the row's
+// partials and its (g, lse2) are at j, its outputs at rows[j].
 __global__ __launch_bounds__(256) void lm_combine_kernel(
     const float2* __restrict__ part, int tiles_v, const uint16_t* __restrict__ hidden,
-    const uint16_t* __restrict__ weight, int H, int64_t N,
+    const uint16_t* __restrict__ weight, int H, const int32_t* __restrict__ rows,
     int64_t n_rows, int V, const int32_t* __restrict__ token_ids, const float* __restrict__ old_logp,
     const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
     const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
     float* __restrict__ tok_loss_out, float* __restrict__ row_loss, float* __restrict__ g_out,
     float* __restrict__ lse2_out, int32_t* __restrict__ dev_err) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + (threadIdx.x / kWave);
-    if (row >= n_rows) return;
-    // Padding rows and excluded tokens: g = 0 and an infinite log-sum-exp
-    // make every dZ entry of the row exactly zero.
-    if (row >= N) {
-        if (lane == 0) g_out[row] = 0.0f, lse2_out[row] = INFINITY;
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + (threadIdx.x / kWave);
+    if (j >= n_rows) return;
+    // Past the live rows, and excluded tokens: g = 0 and an infinite
+    // log-sum-exp make every dZ entry of the row exactly zero.
+    const int64_t row = rows[j];
+    if (row < 0) {
+        if (lane == 0) g_out[j] = 0.0f, lse2_out[j] = INFINITY;
         return;
     }
     const float w = w_tok[row];
@@ -252,8 +380,8 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
         if (lane == 0) {
             if (w != 0.0f) count_error(dev_err);  // token id out of range
             obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-            g_out[row] = 0.0f;
-            lse2_out[row] = INFINITY;
+            g_out[j] = 0.0f;
+            lse2_out[j] = INFINITY;
         }
         return;
     }
@@ -280,7 +408,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
     }
     float m = -INFINITY, s = 0.0f;
     for (int t = lane; t < tiles_v; t += kWave) {
-        const float2 q = part[row * tiles_v + t];
+        const float2 q = part[j * tiles_v + t];
         ms_merge(m, s, q.x, q.y);
     }
     wave_ms_reduce(m, s);
@@ -288,15 +416,15 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
     if (m == -INFINITY) {  // every logit of the row is -inf
         count_error(dev_err);
         obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
-        g_out[row] = 0.0f;
-        lse2_out[row] = INFINITY;
+        g_out[j] = 0.0f;
+        lse2_out[j] = INFINITY;
         return;
     }
     const float lse2 = m + __builtin_amdgcn_logf(s);
     const RowOut o = obj::row_epilogue(lse2, zy, old_logp[row], ref_logp[row], adv_tok[row], w, p);
     obj::write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
-    g_out[row] = o.g;
-    lse2_out[row] = lse2;
+    g_out[j] = o.g;
+    lse2_out[j] = lse2;
 }
 
 // ---------------------------------------------------------------------------
@@ -361,12 +489,13 @@ __device__ __forceinline__ u32x4 add_to_element(u32x4 x, int e, float gv) {
 }
 
 struct DzEpi {
-    const int32_t* token_ids;
-    const float* lse2;
-    const float* g;
-    uint16_t* dz;  // [N_pad][ld_dz], chunk-local columns
+    const int32_t* token_ids;  // [N], caller rows
+    const int32_t* rows;       // [N_pad], compacted row -> caller row (-1: none)
+    const float* lse2;         // [N_pad], compacted rows
+    const float* g;            // [N_pad], compacted rows
+    uint16_t* dz;              // [N_pad][ld_dz], compacted rows, chunk-local columns
     int64_t ld_dz;
-    int64_t N;
+    int64_t N;                 // rows of lse2 / g / rows (N_pad)
     int V, c0;  // vocabulary size, first column of the chunk
     float c2;
 
@@ -381,7 +510,8 @@ struct DzEpi {
             if (r < N) {
                 s_l[tid] = lse2[r];
                 s_g[tid] = g[r];
-                const int y = token_ids[r];
+                const int src = rows[r];
+                const int y = src >= 0 ? token_ids[src] : -1;
                 s_y[tid] = (y >= c0 && y < V) ? y - c0 : -1;
             } else {
                 s_l[tid] = INFINITY;
@@ -452,25 +582,29 @@ struct DzEpi {
 // (and each load of the accumulating form) moves 16 bytes per lane; the
 // stores are non-temporal (the result is not read again by this call, or
 // only by the next chunk's accumulation).
+// With row_map, result row m goes to C row row_map[m] (-1: dropped).
 template <bool ACCUMULATE>
 struct StoreF32Epi {
     float* C;
     int64_t ldc;
     int64_t rows;
     int cols;
+    const int32_t* row_map;  // nullable
 
     __device__ __forceinline__ void operator()(f32x4 (&acc)[8][8], const Tile& t, uint8_t*) const {
         const int lane = t.lane;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int64_t m = t.row0() + i * 16 + acc_row(lane & 3, lane);
+            int64_t dst = m < rows ? m : -1;
+            if (row_map && dst >= 0) dst = row_map[dst];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 float d[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
                 quad_transpose(d, lane);  // row 4h + lane%4, columns of the lane quad
                 const int n0 = t.col0() + j * 16 + (acc_col(lane) & ~3);
-                if (m >= rows) continue;
-                float* p = C + m * ldc + n0;
+                if (dst < 0) continue;
+                float* p = C + dst * ldc + n0;
                 if (n0 + 3 < cols) {
                     float4 v = make_float4(d[0], d[1], d[2], d[3]);
                     if (ACCUMULATE) {
@@ -493,7 +627,7 @@ struct StoreF32Epi {
 // ---------------------------------------------------------------------------
 struct Dims {
     int64_t N, N_pad;
-    int V, V_pad, H, H_pad, tiles_v, Vc, n_chunks;
+    int V, V_pad, H, H_pad, tiles_v, Vc, n_chunks, n_seg;
 };
 
 Dims dims_of(int64_t N, int V, int H) {
@@ -509,12 +643,16 @@ Dims dims_of(int64_t N, int V, int H) {
     const int vc = wide_fits ? kChunkCols : kChunkColsNarrow;
     d.Vc = d.V_pad < vc ? d.V_pad : vc;
     d.n_chunks = (d.V_pad + d.Vc - 1) / d.Vc;
+    d.n_seg = static_cast<int>((d.N_pad + kSeg - 1) / kSeg);
     return d;
 }
 
 struct Layout {
-    size_t ht, wt, part, lse2, g, row_loss, dz, total;
+    size_t ht, hc, wt, part, lse2, g, row_loss, dz, rows, seg, n_live, total;
 };
+
+// The transposed weight Wt [H][V_pad] bf16, zero padded.
+size_t wt_bytes(const Dims& d) { return static_cast<size_t>(d.H) * d.V_pad * 2; }
 
 Layout layout_of(const Dims& d) {
     Layout L;
@@ -525,12 +663,16 @@ Layout layout_of(const Dims& d) {
         return at;
     };
     L.ht = take(static_cast<size_t>(d.H) * d.N_pad * 2);
-    L.wt = take(static_cast<size_t>(d.n_chunks) * d.H * d.Vc * 2);
+    L.hc = take(static_cast<size_t>(d.N_pad) * d.H * 2);
     L.part = take(static_cast<size_t>(d.N_pad) * d.tiles_v * sizeof(float2));
     L.lse2 = take(static_cast<size_t>(d.N_pad) * 4);
     L.g = take(static_cast<size_t>(d.N_pad) * 4);
     L.row_loss = take(static_cast<size_t>(d.N_pad) * 4);
     L.dz = take(static_cast<size_t>(d.N_pad) * d.Vc * 2);
+    L.rows = take(static_cast<size_t>(d.N_pad) * 4);
+    L.seg = take(static_cast<size_t>(d.n_seg) * 4);
+    L.n_live = take(4);
+    L.wt = take(wt_bytes(d));  // last: not needed with a caller's transposed weight
     L.total = off;
     return L;
 }
@@ -542,26 +684,28 @@ bool fits32(int64_t rows_padded, int64_t ld) {
 }
 
 bool shapes_fit(const Dims& d) {
-    return fits32(d.N_pad, d.H) &&       // H   [N][H]
+    return fits32(d.N_pad, d.H) &&       // H, Hc [N_pad][H]
            fits32(d.V_pad, d.H) &&       // W   [V][H]
            fits32(d.H_pad, d.N_pad) &&   // Ht  [H][N_pad]
            fits32(d.N_pad, d.Vc) &&      // dZ  [N_pad][chunk]
-           fits32(d.H_pad, d.Vc);        // Wt  [H][chunk] per chunk
+           fits32(d.H_pad, d.V_pad);     // Wt  [H][V_pad]
 }
 
 uint32_t extent32(uint64_t bytes) {
     return bytes > 0xffffffffull ? 0xffffffffu : static_cast<uint32_t>(bytes);
 }
 
+// One GEMM C = A B^T: M and K are the largest extents (the grid is sized
+// for them); dyn, if it has a count, shrinks M or K at run time.
 template <bool AKM = false, class Epi>
 leap_status gemm_nt(const uint16_t* A, int64_t lda, uint64_t a_bytes, const uint16_t* B, int64_t ldb,
                     uint64_t b_bytes, int K, int64_t M, int64_t Ncols, const Epi& epi,
-                    hipStream_t stream, const LaunchCheck& lc) {
+                    gemm::DynDim dyn, hipStream_t stream, const LaunchCheck& lc) {
     const int tiles_m = static_cast<int>((M + kTile - 1) / kTile);
     const int tiles_n = static_cast<int>((Ncols + kTile - 1) / kTile);
     hipLaunchKernelGGL((gemm::gemm_nt_kernel<Epi, AKM>), dim3(gemm::gemm_grid(tiles_m, tiles_n)),
                        dim3(gemm::kThreads), 0, stream, A, lda, extent32(a_bytes), B, ldb,
-                       extent32(b_bytes), K, tiles_m, tiles_n, epi);
+                       extent32(b_bytes), K, tiles_m, tiles_n, epi, dyn);
     return lc.status();
 }
 
@@ -574,8 +718,34 @@ LEAP_API size_t leap_lmhead_workspace_size(int64_t N, int32_t V, int32_t H) {
     return layout_of(dims_of(N, V, H)).total;
 }
 
+LEAP_API size_t leap_lmhead_weight_t_size(int32_t V, int32_t H) {
+    using namespace leap;
+    if (V < 1 || H < 1) return 0;
+    return wt_bytes(dims_of(0, V, H));
+}
+
+LEAP_API leap_status leap_lmhead_transpose_weight(const void* weight_bf16, int32_t V, int32_t H,
+                                                  void* weight_t_bf16, size_t bytes,
+                                                  hipStream_t stream) {
+    using namespace leap;
+    if (V < 1 || H < 1 || !weight_bf16 || !weight_t_bf16) return LEAP_ERR_INVALID_ARG;
+    if (H % 64 != 0) return LEAP_ERR_UNSUPPORTED;
+    const Dims d = dims_of(0, V, H);
+    if (!fits32(d.V_pad, d.H) || !fits32(d.H_pad, d.V_pad)) return LEAP_ERR_UNSUPPORTED;
+    if (!aligned16(weight_bf16) || !aligned16(weight_t_bf16)) return LEAP_ERR_MISALIGNED;
+    if (bytes < wt_bytes(d)) return LEAP_ERR_WORKSPACE;
+    const leap::LaunchCheck lc;
+    hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.V_pad / kTr), (H + kTr - 1) / kTr),
+                       dim3(256), 0, stream, static_cast<const uint16_t*>(weight_bf16),
+                       static_cast<int64_t>(V), H, static_cast<int64_t>(H), nullptr,
+                       static_cast<uint16_t*>(weight_t_bf16), static_cast<int64_t>(d.V_pad), nullptr,
+                       int64_t{0});
+    return lc.status();
+}
+
 LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
-    const void* hidden_bf16, const void* weight_bf16, int64_t N, int32_t V, int32_t H,
+    const void* hidden_bf16, const void* weight_bf16, const void* weight_t_bf16, int64_t N, int32_t V,
+    int32_t H,
     const int32_t* token_ids, const float* old_logp, const float* ref_logp, const float* adv_tok,
     const float* w_tok, const leap_grpo_params* params, float* logp_out, float* tok_loss_out,
     float* loss_out, float* dhidden, float* dweight, int32_t accumulate_dweight, void* workspace,
@@ -601,20 +771,28 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
             return LEAP_ERR_INVALID_ARG;
         if (!aligned16(hidden_bf16) || !aligned16(weight_bf16)) return LEAP_ERR_MISALIGNED;
     }
-    if (!aligned16(dhidden) || !aligned16(dweight)) return LEAP_ERR_MISALIGNED;
+    if (!aligned16(dhidden) || !aligned16(dweight) || !aligned16(weight_t_bf16))
+        return LEAP_ERR_MISALIGNED;
     const Layout L = layout_of(d);
-    if (!workspace || ws_bytes < L.total) return LEAP_ERR_WORKSPACE;
+    // a caller's transposed weight stands in for the last region
+    const bool own_wt = dhidden && !weight_t_bf16;
+    if (!workspace || ws_bytes < (own_wt ? L.total : L.wt)) return LEAP_ERR_WORKSPACE;
     if (!aligned16(workspace)) return LEAP_ERR_MISALIGNED;
 
     const leap::LaunchCheck lc;
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     uint16_t* ht = reinterpret_cast<uint16_t*>(ws + L.ht);
-    uint16_t* wt = reinterpret_cast<uint16_t*>(ws + L.wt);
+    uint16_t* hc = reinterpret_cast<uint16_t*>(ws + L.hc);
+    const uint16_t* wt = own_wt ? reinterpret_cast<const uint16_t*>(ws + L.wt)
+                                : static_cast<const uint16_t*>(weight_t_bf16);
     float2* part = reinterpret_cast<float2*>(ws + L.part);
     float* lse2 = reinterpret_cast<float*>(ws + L.lse2);
     float* g = reinterpret_cast<float*>(ws + L.g);
     float* row_loss = reinterpret_cast<float*>(ws + L.row_loss);
     uint16_t* dz = reinterpret_cast<uint16_t*>(ws + L.dz);
+    int32_t* rows = reinterpret_cast<int32_t*>(ws + L.rows);
+    int32_t* seg = reinterpret_cast<int32_t*>(ws + L.seg);
+    int32_t* n_live = reinterpret_cast<int32_t*>(ws + L.n_live);
     const uint16_t* Hm = static_cast<const uint16_t*>(hidden_bf16);
     const uint16_t* Wm = static_cast<const uint16_t*>(weight_bf16);
     leap_status st;
@@ -632,36 +810,46 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
 
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     const float c2 = obj::kLog2e * pp.inv_temperature;
-    const uint64_t h_bytes = static_cast<uint64_t>(N) * H * 2;
+    const uint64_t hc_bytes = static_cast<uint64_t>(d.N_pad) * H * 2;
     const uint64_t w_bytes = static_cast<uint64_t>(V) * H * 2;
+    // M of the stats and dH passes (no tile without a live row), of the dZ
+    // pass (at least one tile, so that dZ holds zeros for an empty list), K
+    // of the dW pass (at least one k-tile of those rows)
+    const gemm::DynDim dyn_m{n_live, 0, 0};
+    const gemm::DynDim dyn_m_dz{n_live, 0, 1};
+    const gemm::DynDim dyn_k{n_live, 1, 1};
 
-    // 1. transposed operands of the backward GEMMs
-    if (dweight) {
-        hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.N_pad / kTr), (H + kTr - 1) / kTr),
-                           dim3(256), 0, stream, Hm, N, H, static_cast<int64_t>(H), ht, d.N_pad);
+    // 0. the live rows, in order; the excluded rows' outputs
+    hipLaunchKernelGGL(live_count_kernel, dim3(d.n_seg), dim3(kSegThreads), 0, stream, w_tok, N, seg);
+    if ((st = lc.status()) != LEAP_OK) return st;
+    hipLaunchKernelGGL(compact_rows_kernel, dim3(d.n_seg), dim3(kSegThreads), 0, stream, w_tok, N,
+                       d.N_pad, seg, d.n_seg, rows, n_live, logp_out, tok_loss_out, row_loss);
+    if ((st = lc.status()) != LEAP_OK) return st;
+
+    // 1. gathered and transposed operands
+    hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.N_pad / kTr), (H + kTr - 1) / kTr),
+                       dim3(256), 0, stream, Hm, d.N_pad, H, static_cast<int64_t>(H), rows,
+                       dweight ? ht : nullptr, d.N_pad, hc, static_cast<int64_t>(H));
+    if ((st = lc.status()) != LEAP_OK) return st;
+    if (own_wt) {
+        hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.V_pad / kTr), (H + kTr - 1) / kTr),
+                           dim3(256), 0, stream, Wm, static_cast<int64_t>(V), H, static_cast<int64_t>(H),
+                           nullptr, reinterpret_cast<uint16_t*>(ws + L.wt), static_cast<int64_t>(d.V_pad),
+                           nullptr, int64_t{0});
         if ((st = lc.status()) != LEAP_OK) return st;
     }
-    if (dhidden) {
-        for (int c = 0; c < d.n_chunks; ++c) {
-            const int c0 = c * d.Vc;
-            const int rows = (V - c0) < d.Vc ? (V - c0) : d.Vc;
-            hipLaunchKernelGGL(transpose_pad_kernel, dim3(static_cast<unsigned>(d.Vc / kTr), (H + kTr - 1) / kTr),
-                               dim3(256), 0, stream, Wm + static_cast<int64_t>(c0) * H,
-                               static_cast<int64_t>(rows), H, static_cast<int64_t>(H),
-                               wt + static_cast<int64_t>(c) * H * d.Vc, static_cast<int64_t>(d.Vc));
-            if ((st = lc.status()) != LEAP_OK) return st;
-        }
-    }
 
-    // 2. row statistics and the token logit
+    // 2. row statistics of the live rows
     {
-        const StatsEpi epi{part, N, V, d.tiles_v, c2};
-        if ((st = gemm_nt(Hm, H, h_bytes, Wm, H, w_bytes, H, N, V, epi, stream, lc)) != LEAP_OK) return st;
+        const StatsEpi epi{part, d.N_pad, V, d.tiles_v, c2};
+        if ((st = gemm_nt(hc, H, hc_bytes, Wm, H, w_bytes, H, d.N_pad, V, epi, dyn_m, stream, lc)) !=
+            LEAP_OK)
+            return st;
     }
     // 3. per-token objective
     hipLaunchKernelGGL(lm_combine_kernel, dim3(static_cast<unsigned>(d.N_pad / 4)), dim3(256), 0,
-                       stream, part, d.tiles_v, Hm, Wm, H, N, d.N_pad, V, token_ids, old_logp, ref_logp,
-                       adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
+                       stream, part, d.tiles_v, Hm, Wm, H, rows, d.N_pad, V, token_ids, old_logp,
+                       ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
     if ((st = lc.status()) != LEAP_OK) return st;
     hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
                        row_loss, N, loss_out);
@@ -669,39 +857,46 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     if (!dhidden && !dweight) return LEAP_OK;
 
     // 4. gradients, one vocabulary chunk at a time
+    const uint64_t dz_bytes = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
     for (int c0 = 0; c0 < V; c0 += d.Vc) {
         const int vl = (d.V_pad - c0) < d.Vc ? (d.V_pad - c0) : d.Vc;  // multiple of 256
         {
-            const DzEpi epi{token_ids, lse2, g, dz, d.Vc, N, V, c0, c2};
+            const DzEpi epi{token_ids, rows, lse2, g, dz, d.Vc, d.N_pad, V, c0, c2};
             const uint64_t wb = static_cast<uint64_t>(V - c0) * H * 2;
-            if ((st = gemm_nt(Hm, H, h_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
-                              epi, stream, lc)) != LEAP_OK)
+            if ((st = gemm_nt(hc, H, hc_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
+                              epi, dyn_m_dz, stream, lc)) != LEAP_OK)
                 return st;
         }
         if (dweight) {
-            const int64_t rows = (V - c0) < vl ? (V - c0) : vl;
+            // dW[chunk] = dZ^T Hc: A = dZ read k-major ([N_pad][Vc], the
+            // chunk's vl columns), K = the live rows
+            const int64_t vrows = (V - c0) < vl ? (V - c0) : vl;
             float* C = dweight + static_cast<int64_t>(c0) * H;
-            // A = dZ read k-major: [N_pad][Vc], the chunk's vl columns
-            const uint64_t ab = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
             const uint64_t bb = static_cast<uint64_t>(H) * d.N_pad * 2;
             const int K = static_cast<int>(d.N_pad);
             st = accumulate_dweight
-                     ? gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
-                                     StoreF32Epi<true>{C, H, rows, H}, stream, lc)
-                     : gemm_nt<true>(dz, d.Vc, ab, ht, d.N_pad, bb, K, vl, H,
-                                     StoreF32Epi<false>{C, H, rows, H}, stream, lc);
+                     ? gemm_nt<true>(dz, d.Vc, dz_bytes, ht, d.N_pad, bb, K, vl, H,
+                                     StoreF32Epi<true>{C, H, vrows, H, nullptr}, dyn_k, stream, lc)
+                     : gemm_nt<true>(dz, d.Vc, dz_bytes, ht, d.N_pad, bb, K, vl, H,
+                                     StoreF32Epi<false>{C, H, vrows, H, nullptr}, dyn_k, stream, lc);
             if (st != LEAP_OK) return st;
         }
         if (dhidden) {
-            const uint64_t ab = static_cast<uint64_t>(d.N_pad) * d.Vc * 2;
-            const uint64_t bb = static_cast<uint64_t>(H) * d.Vc * 2;
-            const uint16_t* wc = wt + static_cast<int64_t>(c0 / d.Vc) * H * d.Vc;
-            st = c0 > 0 ? gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
-                                  StoreF32Epi<true>{dhidden, H, N, H}, stream, lc)
-                        : gemm_nt(dz, d.Vc, ab, wc, d.Vc, bb, vl, N, H,
-                                  StoreF32Epi<false>{dhidden, H, N, H}, stream, lc);
+            // dH (+)= dZ Wt[:, c0 .. c0 + vl) (B rows of V_pad, the chunk's
+            // columns), each result row written to its live row's place
+            const uint64_t bb = (static_cast<uint64_t>(H) * d.V_pad - c0) * 2;
+            st = c0 > 0 ? gemm_nt(dz, d.Vc, dz_bytes, wt + c0, d.V_pad, bb, vl, d.N_pad, H,
+                                  StoreF32Epi<true>{dhidden, H, d.N_pad, H, rows}, dyn_m, stream, lc)
+                        : gemm_nt(dz, d.Vc, dz_bytes, wt + c0, d.V_pad, bb, vl, d.N_pad, H,
+                                  StoreF32Epi<false>{dhidden, H, d.N_pad, H, rows}, dyn_m, stream, lc);
             if (st != LEAP_OK) return st;
         }
+    }
+    if (dhidden) {
+        const int64_t blocks = N < 8192 ? N : 8192;
+        hipLaunchKernelGGL(zero_excluded_rows_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                           stream, dhidden, H, w_tok, N);
+        if ((st = lc.status()) != LEAP_OK) return st;
     }
     return LEAP_OK;
 }

@@ -114,10 +114,12 @@ struct Tile {
 // runs at once then cover GROUP x (32 / GROUP) tiles and fetch only that many
 // A and B k-tiles per k-step into the XCD's L2.
 template <int GROUP>
-__device__ __forceinline__ bool tile_of_block(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ bool tile_of_block(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int total = tiles_m * tiles_n;
     const int per = (total + kXcds - 1) / kXcds;
-    const int b = blockIdx.x;
+    // a grid sized for more tiles than a run-time extent leaves: the blocks
+    // past each XCD's share have nothing to do
+    if (b / kXcds >= per) return false;
     const int t = (b % kXcds) * per + b / kXcds;
     if (t >= total) return false;
     const int in_group = GROUP * tiles_n;
@@ -358,17 +360,39 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, int64_t
     stage_barrier();
 }
 
+// A run-time extent of M or K: a count that only the device knows (the rows
+// a compaction kernel kept), read by every workgroup at launch.  The grid and
+// the static tiles_m / K are sized for the largest count; the run-time one is
+// clamped to them.  M: tiles_m = max(min_units, ceil(count / 256)); K: K =
+// 64 * max(min_units, ceil(count / 64)).
+struct DynDim {
+    const int32_t* count;  // nullptr: static extents
+    int k_dim;             // 0: the count sets M, 1: it sets K
+    int min_units;         // least number of M tiles or k-tiles
+};
+
 // One kernel per epilogue and A layout.  The epilogue gets the accumulators,
 // the tile and the (idle) LDS buffer; it is called after the last barrier of
-// the k-loop.
+// the k-loop.  (Written out in the kernel body: the same steps behind an
+// inlined device function made the compiler move the accumulators between
+// AGPRs in the k-loop and spill them.)
 template <class Epi, bool AKM = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 gemm_nt_kernel(const uint16_t* __restrict__ A, int64_t lda, uint32_t a_bytes,
                const uint16_t* __restrict__ B, int64_t ldb, uint32_t b_bytes, int K, int tiles_m,
-               int tiles_n, Epi epi) {
+               int tiles_n, Epi epi, DynDim dyn) {
     __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+    if (dyn.count) {
+        const int n = *dyn.count;
+        if (dyn.k_dim) {
+            const int kt = max((n + kBK - 1) / kBK, dyn.min_units);
+            K = min(K, kt * kBK);
+        } else {
+            tiles_m = min(tiles_m, max((n + kBM - 1) / kBM, dyn.min_units));
+        }
+    }
     int tm, tn;
-    if (!tile_of_block<kGroupM>(tiles_m, tiles_n, tm, tn)) return;
+    if (!tile_of_block<kGroupM>(blockIdx.x, tiles_m, tiles_n, tm, tn)) return;
     f32x4 acc[8][8];
     mainloop<AKM>(A, lda, a_bytes, B, ldb, b_bytes, K, tm, tn, smem, acc);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

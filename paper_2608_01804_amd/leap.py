@@ -39,6 +39,8 @@ EXPORTED = (
     "leap_grpo_logprob_loss_fwd_bwd_noalloc",
     "leap_logprob_fwd",
     "leap_lmhead_workspace_size",
+    "leap_lmhead_weight_t_size",
+    "leap_lmhead_transpose_weight",
     "leap_grpo_lmhead_fwd_bwd",
     "leap_vocab_shard_stats",
     "leap_vocab_merge_workspace_size",
@@ -106,8 +108,12 @@ def lib() -> ctypes.CDLL:
     L.leap_logprob_fwd.argtypes = [P, i64, i64, i32, P, P, f32, P, P, P, P]
     L.leap_lmhead_workspace_size.restype = ctypes.c_size_t
     L.leap_lmhead_workspace_size.argtypes = [i64, i32, i32]
+    L.leap_lmhead_weight_t_size.restype = ctypes.c_size_t
+    L.leap_lmhead_weight_t_size.argtypes = [i32, i32]
+    L.leap_lmhead_transpose_weight.restype = ctypes.c_int
+    L.leap_lmhead_transpose_weight.argtypes = [P, i32, i32, P, ctypes.c_size_t, P]
     L.leap_grpo_lmhead_fwd_bwd.restype = ctypes.c_int
-    L.leap_grpo_lmhead_fwd_bwd.argtypes = [P, P, i64, i32, i32, P, P, P, P, P,
+    L.leap_grpo_lmhead_fwd_bwd.argtypes = [P, P, P, i64, i32, i32, P, P, P, P, P,
                                            ctypes.POINTER(leap_grpo_params), P, P, P, P, P, i32,
                                            P, ctypes.c_size_t, P, P]
     L.leap_vocab_shard_stats.restype = ctypes.c_int
@@ -282,13 +288,24 @@ def leap_lmhead_workspace_size(N, V, H) -> int:
     return int(lib().leap_lmhead_workspace_size(int(N), int(V), int(H)))
 
 
+def leap_lmhead_weight_t_size(V, H) -> int:
+    return int(lib().leap_lmhead_weight_t_size(int(V), int(H)))
+
+
+def leap_lmhead_transpose_weight(weight, V, H, weight_t, nbytes, stream=None) -> None:
+    st = lib().leap_lmhead_transpose_weight(_ptr(weight, "bfloat16", "weight"), int(V), int(H),
+                                            _ptr(weight_t, None, "weight_t"), int(nbytes),
+                                            _stream(stream))
+    _check(st, "leap_lmhead_transpose_weight")
+
+
 def leap_grpo_lmhead_fwd_bwd(hidden, weight, N, V, H, token_ids, old_logp, ref_logp, adv_tok, w_tok,
                              params: leap_grpo_params, logp_out, tok_loss_out, loss_out, dhidden,
                              dweight, accumulate_dweight, workspace, ws_bytes, dev_err=None,
-                             stream=None) -> None:
+                             stream=None, weight_t=None) -> None:
     st = lib().leap_grpo_lmhead_fwd_bwd(
-        _ptr(hidden, "bfloat16", "hidden"), _ptr(weight, "bfloat16", "weight"), int(N), int(V),
-        int(H), _ptr(token_ids, "int32", "token_ids"), _ptr(old_logp, "float32", "old_logp"),
+        _ptr(hidden, "bfloat16", "hidden"), _ptr(weight, "bfloat16", "weight"),
+        _ptr(weight_t, None, "weight_t"), int(N), int(V), int(H), _ptr(token_ids, "int32", "token_ids"), _ptr(old_logp, "float32", "old_logp"),
         _ptr(ref_logp, "float32", "ref_logp"), _ptr(adv_tok, "float32", "adv_tok"),
         _ptr(w_tok, "float32", "w_tok"), ctypes.byref(params) if params is not None else None,
         _ptr(logp_out, "float32", "logp_out"), _ptr(tok_loss_out, "float32", "tok_loss_out"),

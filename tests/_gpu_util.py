@@ -242,9 +242,11 @@ def lmhead_inputs(seed, N, V, H, mask_frac=0.05, bad_rows=(), cur="oracle", inv_
 
 
 def run_lmhead(inp, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0, inv_temp=1.0, want_dH=True,
-               want_dW=True, accumulate=0, dW_init=None, to_host=True):
+               want_dW=True, accumulate=0, dW_init=None, to_host=True, prepared=False):
     """Call leap_grpo_lmhead_fwd_bwd; returns numpy logp, tok_loss, loss, dH,
-    dW (or the device tensors with to_host=False), bad."""
+    dW (or the device tensors with to_host=False), bad.  prepared: pass the
+    weight transposed beforehand by leap_lmhead_transpose_weight, with the
+    workspace cut to what the call then needs."""
     import torch
     from paper_2608_01804_amd import leap as L
     hid, wt = inp["hid"], inp["wt"]
@@ -259,12 +261,18 @@ def run_lmhead(inp, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0, inv_temp=1.
         dW = (T(dW_init.astype(np.float32)) if dW_init is not None
               else torch.full((V, H), float("nan"), dtype=torch.float32, device=dev()))
     ws_bytes = L.leap_lmhead_workspace_size(N, V, H)
+    w_t = None
+    if prepared:
+        nb = L.leap_lmhead_weight_t_size(V, H)
+        w_t = torch.full((nb,), 0x5A, dtype=torch.uint8, device=dev())
+        L.leap_lmhead_transpose_weight(wt, V, H, w_t, nb)
+        ws_bytes -= nb
     ws = torch.full((ws_bytes,), 0xA5, dtype=torch.uint8, device=dev())  # stale contents
     err = zeros_i32(1)
     p = L.leap_grpo_params(eps_lo, eps_hi, kl_coef, kl_type, inv_temp)
     L.leap_grpo_lmhead_fwd_bwd(hid, wt, N, V, H, T(inp["y"]), T(inp["old"]), T(inp["ref"]),
                                T(inp["adv"]), T(inp["w"]), p, lp, tl, loss, dH, dW, accumulate, ws,
-                               ws_bytes, err)
+                               ws_bytes, err, weight_t=w_t)
     torch.cuda.synchronize()
     out = {"logp": lp.cpu().numpy()[:N], "tok_loss": tl.cpu().numpy()[:N],
            "loss": float(loss.item()), "bad": int(err.item())}

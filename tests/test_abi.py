@@ -271,6 +271,7 @@ def _lmhead(**kw):
     (dict(dhidden=FAKE + 8), L.LEAP_ERR_MISALIGNED),
     (dict(workspace=None), L.LEAP_ERR_WORKSPACE),
     (dict(ws_bytes=1024), L.LEAP_ERR_WORKSPACE),
+    (dict(weight_t=FAKE + 8), L.LEAP_ERR_MISALIGNED),
 ])
 def test_lmhead_rejects(kw, status):
     if "ws_bytes" not in kw and "workspace" not in kw:
@@ -278,6 +279,37 @@ def test_lmhead_rejects(kw, status):
     with pytest.raises(L.LeapError) as e:
         _lmhead(**kw)
     assert e.value.status == status
+
+
+def test_lmhead_workspace_with_prepared_weight():
+    # With a caller's transposed weight the call needs the workspace without
+    # its last region (the transposed weight); without one, all of it.
+    full = L.leap_lmhead_workspace_size(8, 1000, 64)
+    wt = L.leap_lmhead_weight_t_size(1000, 64)
+    for weight_t, short in ((None, full - 1), (FAKE + (1 << 30), full - wt - 1)):
+        with pytest.raises(L.LeapError) as e:
+            _lmhead(weight_t=weight_t, ws_bytes=short)
+        assert e.value.status == L.LEAP_ERR_WORKSPACE
+
+
+def test_lmhead_weight_t_size_and_transpose_rejects():
+    assert L.leap_lmhead_weight_t_size(151936, 4096) == 2 * 4096 * 152064
+    assert L.leap_lmhead_weight_t_size(1000, 64) == 2 * 64 * 1024
+    assert L.leap_lmhead_weight_t_size(0, 64) == 0 and L.leap_lmhead_weight_t_size(10, 0) == 0
+    n = L.leap_lmhead_weight_t_size(1000, 64)
+    for kw, status in [(dict(V=0), L.LEAP_ERR_INVALID_ARG), (dict(H=0), L.LEAP_ERR_INVALID_ARG),
+                       (dict(weight=None), L.LEAP_ERR_INVALID_ARG),
+                       (dict(weight_t=None), L.LEAP_ERR_INVALID_ARG),
+                       (dict(H=96), L.LEAP_ERR_UNSUPPORTED),
+                       (dict(V=1 << 20, H=4096), L.LEAP_ERR_UNSUPPORTED),
+                       (dict(weight=FAKE + 2), L.LEAP_ERR_MISALIGNED),
+                       (dict(weight_t=FAKE + 8), L.LEAP_ERR_MISALIGNED),
+                       (dict(nbytes=n - 1), L.LEAP_ERR_WORKSPACE)]:
+        a = dict(weight=FAKE, V=1000, H=64, weight_t=FAKE, nbytes=n, stream=0)
+        a.update(kw)
+        with pytest.raises(L.LeapError) as e:
+            L.leap_lmhead_transpose_weight(**a)
+        assert e.value.status == status, kw
 
 
 def test_lmhead_rejects_params():
@@ -292,21 +324,22 @@ def test_lmhead_workspace_size():
     assert L.leap_lmhead_workspace_size(8, 0, 64) == 0
     small = L.leap_lmhead_workspace_size(8, 1000, 64)
     assert small > 0 and small % 256 == 0
-    # transposes (H*N_pad, and H*chunk per vocabulary chunk, bf16), per-tile
-    # row statistics, three per-row vectors and one bf16 chunk of dZ; chunks
+    # the gathered live rows of H, row-major and transposed (2 H N_pad bf16
+    # each), the transposed weight (H V_pad bf16), per-tile row statistics,
+    # three per-row vectors and the row list (4 N_pad each), one bf16 chunk of
+    # dZ, and the compaction's per-segment counts (4096-row segments); chunks
     # are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
     def want(n, v, h):
         n_pad = (n + 255) // 256 * 256
         v_pad = (v + 255) // 256 * 256
         vc = 32768 if n_pad * 32768 * 2 < (1 << 32) - 64 else 16384
         vc = min(vc, v_pad)
-        chunks = -(-v_pad // vc)
-        return (2 * h * n_pad + 2 * h * vc * chunks + 8 * n_pad * (v_pad // 256) + 3 * 4 * n_pad
-                + 2 * n_pad * vc)
+        return (2 * 2 * h * n_pad + 2 * h * v_pad + 8 * n_pad * (v_pad // 256) + 4 * 4 * n_pad
+                + 2 * n_pad * vc + 4 * -(-n_pad // 4096) + 4)
 
     for n, v, h in [(16384, 151936, 4096), (65280, 151936, 4096), (65281, 151936, 4096),
                     (1000, 20000, 512)]:
-        assert abs(L.leap_lmhead_workspace_size(n, v, h) - want(n, v, h)) <= 9 * 256, (n, v, h)
+        assert abs(L.leap_lmhead_workspace_size(n, v, h) - want(n, v, h)) <= 12 * 256, (n, v, h)
     # the narrow chunk takes over from N_pad = 65536 (a 4 GiB dZ chunk otherwise)
     assert (L.leap_lmhead_workspace_size(65281, 151936, 4096)
             < L.leap_lmhead_workspace_size(65280, 151936, 4096))

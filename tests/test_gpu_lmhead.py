@@ -116,6 +116,22 @@ def test_lmhead_accumulate_and_optional_gradients():
     assert abs(full["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7
 
 
+@pytest.mark.parametrize("N,V,H", [(300, 1000, 192), (129, 33000, 64)])
+def test_lmhead_prepared_weight(N, V, H):
+    # A transposed weight prepared once (leap_lmhead_transpose_weight) and
+    # the call's own transpose give bitwise the same results; the prepared
+    # call runs in the smaller workspace.
+    U.log(f"lmhead prepared weight N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(3401 + N, N, V, H)
+    kw = _kw()
+    own = U.run_lmhead(inp, **kw)
+    prep = U.run_lmhead(inp, prepared=True, **kw)
+    for k in ("logp", "tok_loss", "dH", "dW"):
+        np.testing.assert_array_equal(prep[k], own[k], err_msg=k)
+    assert prep["loss"] == own["loss"]
+    _compare(inp, prep, kw, what="prepared")
+
+
 def test_lmhead_empty_batch():
     import torch
     from paper_2608_01804_amd import leap as L
@@ -136,6 +152,63 @@ def test_lmhead_empty_batch():
         torch.cuda.synchronize()
         assert loss.item() == 0.0
         assert torch.all(dW == (3.0 if accumulate else 0.0)).item()
+
+
+def test_lmhead_all_rows_excluded():
+    # Every weight 0: no live row is left after the compaction, so no GEMM
+    # tile runs on data; every output is still written (zeros), and an
+    # accumulated dW is left as it was.
+    N, V, H = 300, 1000, 64
+    U.log(f"lmhead all rows excluded N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(3101, N, V, H)
+    inp["w"] = np.zeros(N, np.float32)
+    kw = _kw()
+    init = np.random.default_rng(6).normal(0, 1, (V, H)).astype(np.float32)
+    for accumulate in (0, 1):
+        gpu = U.run_lmhead(inp, accumulate=accumulate, dW_init=init if accumulate else None, **kw)
+        assert gpu["bad"] == 0 and gpu["loss"] == 0.0
+        assert np.all(gpu["logp"] == 0.0) and np.all(gpu["tok_loss"] == 0.0)
+        assert np.all(gpu["dH"] == 0.0)
+        np.testing.assert_array_equal(gpu["dW"], init if accumulate else np.zeros((V, H), np.float32))
+
+
+def test_lmhead_excluded_rows_are_not_read():
+    # Excluded rows (w = 0) take no part in the call: NaN and inf hidden
+    # states there reach no output.  The excluded rows include the first and
+    # the last row, a tile edge and a run longer than a 256-row tile; the
+    # oracle scores the same inputs with finite values in those rows.
+    import torch
+    N, V, H = 700, 3000, 128
+    U.log(f"lmhead excluded rows not read N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(3201, N, V, H, mask_frac=0.0)
+    w = inp["w"].copy()
+    excl = np.r_[0, 1, 2, 255, 256, 300:561, 699]
+    w[excl] = 0.0
+    ref_inp = dict(inp, w=w)
+    hid = inp["hid"].clone()
+    hid[torch.from_numpy(excl[0::2]).to(U.dev())] = float("nan")
+    hid[torch.from_numpy(excl[1::2]).to(U.dev())] = float("inf")
+    kw = _kw(kl_coef=0.05)
+    gpu = U.run_lmhead(dict(ref_inp, hid=hid), **kw)
+    _compare(ref_inp, gpu, kw, what="poisoned excluded rows")
+    assert np.all(np.isfinite(gpu["dW"])) and np.all(np.isfinite(gpu["dH"]))
+
+
+def test_lmhead_compaction_over_segments():
+    # 9000 rows: three 4096-row segments of the live-row compaction, 40% of
+    # the rows excluded at random, plus an excluded run that starts a
+    # segment and one that crosses a segment boundary.
+    N, V, H = 9000, 2000, 64
+    U.log(f"lmhead compaction N={N} V={V} H={H}")
+    inp = U.lmhead_inputs(3301, N, V, H, mask_frac=0.4, bad_rows=(4095, 8191))
+    w = inp["w"].copy()
+    w[4096:4700] = 0.0
+    w[8150:8191] = 0.0
+    w[8192:8400] = 0.0
+    inp["w"] = w
+    kw = _kw()
+    gpu = U.run_lmhead(inp, **kw)
+    _compare(inp, gpu, kw, bad_expected=2, what="compaction")
 
 
 def _sampled_rows_and_dw_check(inp, gpu, kw, seed, what):
