@@ -284,6 +284,18 @@ def run_lmhead(inp, eps_lo=0.2, eps_hi=0.2, kl_coef=0.01, kl_type=0, inv_temp=1.
     return out
 
 
+def check_f32_rounding(got, want, what):
+    """got (float32) within one float32 ulp of the exact value want (float64):
+    the ulp at want's magnitude, 2^-149 absolute in the subnormal range, so
+    a value computed in double and rounded once to float (half an ulp off at
+    most) passes and any other error shows."""
+    want = np.asarray(want, np.float64)
+    ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+    err = np.abs(np.asarray(got, np.float64) - want)
+    bad = err > ulp
+    assert not np.any(bad), (what, np.flatnonzero(bad)[:5], err[bad][:5], ulp[bad][:5])
+
+
 def bf16_f64(u16: np.ndarray) -> np.ndarray:
     return (u16.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 

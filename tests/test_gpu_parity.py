@@ -137,9 +137,8 @@ def test_token_adv_parity(name, agg):
     adv_g, w_g, bad_g = U.run_token_adv(A32, tok_r, tok_t, ro.n_turns, ro.n_tokens, gamma, agg,
                                         _denom(agg, ro))
     assert bad_o == 0 and bad_g == 0
-    ulp = 2.0 ** -23
-    assert np.all(np.abs(adv_g - adv_o) <= ulp * np.abs(adv_o))
-    assert np.all(np.abs(w_g - w_o) <= ulp * np.abs(w_o))
+    U.check_f32_rounding(adv_g, adv_o, "token advantage")
+    U.check_f32_rounding(w_g, w_o, "weight")
     assert np.all((tok_r < 0) <= (w_g == 0))
 
 

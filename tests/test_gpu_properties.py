@@ -6,7 +6,7 @@ advantages within 1e-6, token advantages and weights within float32
 rounding)."""
 import numpy as np
 import pytest
-from hypothesis import HealthCheck, given, settings
+from hypothesis import HealthCheck, example, given, settings
 from hypothesis import strategies as st
 
 import oracle
@@ -49,6 +49,12 @@ def test_gate_matches_oracle(G, n_groups, data):
 @SETTINGS
 @given(token_layouts(), st.sampled_from([oracle.AGG_SEQ_MEAN_TOKEN_MEAN, oracle.AGG_TOKEN_MEAN,
                                          oracle.AGG_SUM]))
+# a subnormal advantage: gamma^2 A falls halfway between two subnormal floats
+@example(lay=(np.array([0.0] * 5 + [9.99999935e-39] + [0.0] * 4),
+              np.array([1, 1, 1, 1, 1, 3, 1, 1, 1, 1], dtype=np.int32),
+              np.array([0, 1, 2, 3, 4, 5, 5, 5, 6, 7, 8, 9], dtype=np.int32),
+              np.array([0, 0, 0, 0, 0, 0, 1, 2, 0, 0, 0, 0], dtype=np.int32), 0.5),
+         agg=oracle.AGG_SEQ_MEAN_TOKEN_MEAN)
 def test_token_advantages_match_oracle(lay, agg):
     A, T, tok_r, tok_t, gamma = lay
     A32 = A.astype(np.float32)
@@ -60,8 +66,8 @@ def test_token_advantages_match_oracle(lay, agg):
                                                 g32, agg, denom)
     adv_g, w_g, bad_g = U.run_token_adv(A32, tok_r, tok_t, T, n_gen, gamma, agg, denom)
     assert bad_o == bad_g == 0
-    np.testing.assert_allclose(adv_g, adv_o, rtol=1.2e-7, atol=0)
-    np.testing.assert_allclose(w_g, w_o, rtol=1.2e-7, atol=0)
+    U.check_f32_rounding(adv_g, adv_o, "token advantage")
+    U.check_f32_rounding(w_g, w_o, "weight")
 
 
 @st.composite
