@@ -742,12 +742,13 @@ def mfma_probe(L, torch, dev, random_operands: int = 0, iters: int = 500000, rep
     return flops / float(np.median(ts))
 
 
-def blas_reference(torch, dev):
+def blas_reference(torch, dev, rows: int = 16384):
     """Context only, not part of the path: torch's bf16 matmul (hipBLASLt) on
-    the shapes of the fused LM head's four GEMM passes, as plain products
-    with a bf16 result and no epilogue work.  Median of 3 timed calls."""
-    shapes = {"stats (H W^T)": (16384, 151936, 4096), "dZ chunk": (16384, 32768, 4096),
-              "dW chunk": (32768, 4096, 16384), "dH chunk": (16384, 4096, 32768)}
+    the shapes of the fused LM head's four GEMM passes over `rows` rows (the
+    call's live rows), as plain products with a bf16 result and no epilogue
+    work.  Median of 3 timed calls."""
+    shapes = {"stats (H W^T)": (rows, 151936, 4096), "dZ chunk": (rows, 32768, 4096),
+              "dW chunk": (32768, 4096, rows), "dH chunk": (rows, 4096, 32768)}
     out = {}
     for name, (m, n, k) in shapes.items():
         a = torch.randn(m, k, device=dev, dtype=torch.bfloat16)
@@ -890,7 +891,7 @@ def main():
     if args.lmhead_only:
         out = {"lmhead": lmhead_leg(L, torch, dev, 1005, max(1, args.lmhead_reps))}
         if args.blas_reference:
-            out["blas_reference"] = blas_reference(torch, dev)
+            out["blas_reference"] = blas_reference(torch, dev, out["lmhead"]["live_rows"])
         print(json.dumps(out), flush=True)
         return
 
