@@ -16,7 +16,7 @@ from tests.test_oracle_properties import groups, token_layouts
 
 pytestmark = pytest.mark.gpu
 
-SETTINGS = settings(max_examples=60, deadline=None,
+SETTINGS = settings(max_examples=60, deadline=None, derandomize=True,
                     suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
                                            HealthCheck.function_scoped_fixture])
 
@@ -90,7 +90,7 @@ def objective_cases(draw):
         p_ninf=draw(st.sampled_from([0.0, 0.0, 0.01, 0.3])), entropy=draw(st.booleans()))
 
 
-@settings(max_examples=40, deadline=None,
+@settings(max_examples=40, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
                                  HealthCheck.function_scoped_fixture])
 @given(objective_cases())
@@ -159,7 +159,7 @@ def shard_cases(draw):
                 inplace=draw(st.booleans()))
 
 
-@settings(max_examples=30, deadline=None,
+@settings(max_examples=30, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
                                  HealthCheck.function_scoped_fixture])
 @given(shard_cases())
@@ -207,7 +207,7 @@ def test_vocab_shards_match_unsharded_oracle(c):
         np.testing.assert_allclose(q[live, 1], s[live], rtol=2e-5)
 
 
-@settings(max_examples=30, deadline=None,
+@settings(max_examples=30, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
                                  HealthCheck.function_scoped_fixture])
 @given(st.one_of(st.integers(1, 700), st.integers(701, 70000)), st.sampled_from([0, 8, 64]),

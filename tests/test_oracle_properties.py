@@ -21,7 +21,7 @@ from scipy import stats
 import oracle
 
 EPS = float(np.float32(1e-6))
-SETTINGS = settings(max_examples=150, deadline=None,
+SETTINGS = settings(max_examples=150, deadline=None, derandomize=True,
                     suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 
 
