@@ -192,7 +192,9 @@ leap_status leap_token_advantages(const float *advantage, const int32_t *tok_rol
                                   float *adv_tok, float *w_tok, int32_t *dev_err,
                                   hipStream_t stream);
 
-/* Workspace bytes leap_grpo_logprob_loss_fwd_bwd needs for N rows. */
+/* Workspace bytes leap_grpo_logprob_loss_fwd_bwd needs for N rows: the
+ * per-row weighted losses (4 bytes per row, in whole 256-byte lines) and
+ * one 256-byte line for the row queue of the persistent kernel. */
 size_t leap_grpo_workspace_size(int64_t N, int32_t V);
 
 /*
@@ -255,9 +257,10 @@ leap_status leap_grpo_logprob_loss_fwd_bwd(const void *logits_bf16, int64_t ld, 
  * For callers that cannot allocate device memory -- code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc: the same
  * call as leap_grpo_logprob_loss_fwd_bwd (same kernels, same results bit for
- * bit, same argument rules) without the workspace arguments.  Its per-row
- * scratch is a library-owned device array of LEAP_NOALLOC_MAX_ROWS floats
- * (4 MiB) per device, held until the process ends; the call itself
+ * bit, same argument rules) without the workspace arguments.  Its scratch
+ * (the per-row losses and the row queue) is a library-owned device array of
+ * LEAP_NOALLOC_MAX_ROWS floats plus 256 bytes (4 MiB) per device, held until
+ * the process ends; the call itself
  * allocates and frees nothing.  The first call on a device looks up that
  * device's array (the device must be current).
  * All calls on one device share its array: calls that may overlap on one

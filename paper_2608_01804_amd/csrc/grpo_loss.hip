@@ -26,10 +26,11 @@
 //    16 bytes at a time; the token's own column gets g * (1 - p_y).
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
 //  * For the 19-chunk shape (one workgroup per compute unit) the kernel is
-//    persistent: a grid of one workgroup per CU walks the rows and issues
-//    the next row's loads right behind the current row's stores, so each
-//    CU's reads overlap its writes instead of waiting for a new workgroup
-//    to be dispatched after each row.
+//    persistent: a grid of one workgroup per CU takes rows from a row queue
+//    (a counter in the workspace) and issues the next row's loads right
+//    behind the current row's stores, so each CU's reads overlap its writes
+//    instead of waiting for a new workgroup to be dispatched after each row,
+//    and CUs that stream faster take more rows.
 //  * Up to 270336 columns the part of the row past 196608 columns is held in
 //    LDS (the hybrid kernel); larger vocabularies use a streaming variant
 //    that re-reads the row.
@@ -168,7 +169,9 @@ __device__ __forceinline__ void dlogits_pass_vgpr(u32x4 (&x)[CH], float sc, floa
 // lane maximum, the exponentials (kept as fp16 in x), the block merge, the
 // scalar epilogue, the dlogits stores and the row's outputs.  A row whose
 // logits are all -inf is counted and zero-filled instead.  One barrier
-// (inside the block merge) in every call.
+// (inside the block merge) in every call.  With tk_slot set, thread 0
+// stores tk there after pass A, so the value is in LDS for every thread once
+// the merge's barrier has passed.
 template <int BLOCK, int CH, int SAFE, bool ENT>
 __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row, uint16_t* drow,
                                           int V, int y, float w, const float* __restrict__ old_logp,
@@ -178,11 +181,13 @@ __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row,
                                           float* __restrict__ tok_loss_out,
                                           float* __restrict__ entropy_out,
                                           float* __restrict__ row_loss, int32_t* __restrict__ dev_err,
-                                          RowLds<BLOCK, ENT>& lds, int tid) {
+                                          RowLds<BLOCK, ENT>& lds, int tid, int* tk_slot = nullptr,
+                                          int tk = 0) {
     mask_row_tail<BLOCK, CH, SAFE>(x, V, tid);
 
     // Pass A: lane maximum over the raw bf16 words.
     const float m = row_lane_max<CH>(x);
+    if (tk_slot && tid == 0) *tk_slot = tk;
 
     // Keep the bf16 words as the only live copy of the row.
 #pragma unroll
@@ -228,7 +233,8 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, int64_t N,
                    const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
                    const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
                    float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
-                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+                   float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err,
+                   int32_t* /*queue: the persistent form's only*/) {
     __shared__ RowLds<BLOCK, ENT> lds;
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
@@ -251,15 +257,55 @@ grpo_rows_resident(const uint16_t* logits, int64_t ld, int V, int64_t N,
                                     tid);
 }
 
-// Persistent form: workgroup b takes rows b, b + G, b + 2G, ... (G = the
-// grid).  The next row's token id and weight are fetched while the current
-// row is processed, and its logits loads are issued as soon as the current
-// row's registers are free: after the dlogits stores of a live row, before
-// the zero fill of an excluded one.  On each compute unit the next row's
-// reads thus overlap the current row's writes draining to HBM.  The block
-// merges of consecutive rows alternate between two LDS areas: a wave that
-// runs ahead into the next row's merge cannot overwrite values a slower wave
-// has yet to read from the previous one.
+// Fetch-and-add of k on the row queue, from one lane.  The pointer passes
+// through an empty asm so that the compiler sees a per-lane address: it then
+// emits one global atomic with return instead of a wave-wide aggregation,
+// whose broadcast would wait for the atomic (and, the vector memory counter
+// being in order, for every load and store before it) on the spot.  The
+// result is waited for where it is used.
+__device__ __forceinline__ int queue_take(int32_t* queue, int k) {
+    int32_t* qp = queue;
+    asm volatile("" : "+v"(qp));
+    auto* gp = (__attribute__((address_space(1))) int32_t*)(qp);
+    return __hip_atomic_fetch_add(gp, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Zero the row queue before the persistent kernel (a kernel rather than a
+// memset, so that the call can be captured in a graph).
+__global__ void queue_reset_kernel(int32_t* queue) {
+    if (threadIdx.x == 0) *queue = 0;
+}
+
+// Persistent form: one workgroup per compute unit.  Workgroup b's first four
+// rows are b, b + G, b + 2G and b + 3G (G = the grid); after them it takes
+// rows from a queue, ticket t meaning row 4G + t.  A static stride would tie
+// the call's end to the slowest compute units: measured with per-workgroup
+// timestamps on the MI355X, the workgroups of half of the eight XCDs finish
+// their equal shares ~8% of the call later than the others.
+//
+// The queue is read ahead so that its atomic never stalls the row: the
+// workgroup knows its next three rows.  A live row takes as many tickets as
+// make it three again (one atomic by thread 0 at the top of the row; it
+// returns behind the row's own loads, which pass A waits for anyway),
+// publishes the first ticket in LDS after pass A, and every thread reads it
+// after the block merge's barrier.  An excluded row takes none, so three
+// excluded rows in a row use the known rows up; only then does the
+// workgroup fetch three tickets and wait for them at a barrier of its own.
+// Every row a workgroup takes is larger than its previous one, so it stops
+// at the first row >= N, and tickets it holds then are past N as well.
+//
+// The next row's token id and weight are fetched while the current row is
+// processed, and its logits loads are issued as soon as the current row's
+// registers are free: after the dlogits stores of a live row, before the
+// zero fill of an excluded one.  On each compute unit the next row's reads
+// thus overlap the current row's writes draining to HBM.  The token's
+// logit is kept as raw bits until the epilogue, so that nothing waits for
+// its load early.  The block merges of consecutive rows alternate between
+// two LDS areas, and so do the published tickets: a wave that runs ahead
+// into the next row cannot overwrite values a slower wave has yet to read.
+// Which workgroup processes a row depends on timing, but every row's outputs
+// are computed the same way wherever it runs, so results stay bitwise
+// reproducible.
 template <int BLOCK, int CH, int SAFE, bool ENT>
 __global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(4))) void
 grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
@@ -267,44 +313,82 @@ grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
                   const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
                   const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
                   float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
-                  float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+                  float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err,
+                  int32_t* queue) {
     __shared__ RowLds<BLOCK, ENT> lds[2];
+    __shared__ int tks[2];
+    constexpr int64_t kUnknown = -1;
     const int tid = threadIdx.x;
     const int nchunks = (V + 7) >> 3;
+    const int64_t G = gridDim.x;
+    const int64_t base = 4 * G;
     int64_t row = blockIdx.x;
     if (row >= N) return;
+    // the next three rows; unknown ones (kUnknown) are always the last
+    int64_t q1 = row + G, q2 = row + 2 * G, q3 = row + 3 * G;
     u32x4 x[CH];
-    float xy = 0.0f;
-    // Issue the loads of row r (live) into x; its token logit into xy.
+    uint32_t xyb = 0;  // the token's bf16 logit
+    // Issue the loads of row r (live) into x; its token logit into xyb.
     auto issue_row = [&](int64_t r, int yr) {
         const uint16_t* xrow = logits + r * ld;
         load_row<BLOCK, CH, SAFE>(x, xrow, nchunks, tid * 16);
-        xy = __uint_as_float(static_cast<uint32_t>(xrow[yr]) << 16);
+        xyb = xrow[yr];
     };
     float w = w_tok[row];
     int y = token_ids[row];
     bool live = row_live(w, y, V);
     if (live) issue_row(row, y);
     int parity = 0;
+    int tp = 0;
     while (true) {
-        const int64_t next = row + gridDim.x;
-        const bool more = next < N;
-        const float w_next = more ? w_tok[next] : 0.0f;
-        const int y_next = more ? token_ids[next] : 0;
+        if (q1 == kUnknown) {
+            if (tid == 0) tks[tp] = queue_take(queue, 3);
+            __syncthreads();
+            const int64_t t = base + __builtin_amdgcn_readfirstlane(tks[tp]);
+            tp ^= 1;
+            q1 = t;
+            q2 = t + 1;
+            q3 = t + 2;
+        }
+        const bool more = q1 < N;
+        const int k = 1 + (q2 == kUnknown) + (q3 == kUnknown);
+        int tk;  // set and read in thread 0 of a live row only
+        if (live && tid == 0) tk = queue_take(queue, k);
+        const float w_next = more ? w_tok[q1] : 0.0f;
+        const int y_next = more ? token_ids[q1] : 0;
         const bool live_next = more && row_live(w_next, y_next, V);
         uint16_t* drow = dlogits + row * ld;
         if (live) {
-            fused_row<BLOCK, CH, SAFE, ENT>(x, xy, row, drow, V, y, w, old_logp, ref_logp, adv_tok,
-                                            p, logp_out, tok_loss_out, entropy_out, row_loss,
-                                            dev_err, lds[parity], tid);
+            fused_row<BLOCK, CH, SAFE, ENT>(x, __uint_as_float(xyb << 16), row, drow, V, y, w,
+                                            old_logp, ref_logp, adv_tok, p, logp_out,
+                                            tok_loss_out, entropy_out, row_loss, dev_err,
+                                            lds[parity], tid, &tks[tp], tk);
             parity ^= 1;
         }
-        if (live_next) issue_row(next, y_next);
+        if (live_next) issue_row(q1, y_next);
         if (!live)
             excluded_row<BLOCK, ENT>(row, drow, V, w != 0.0f, logp_out, tok_loss_out, entropy_out,
                                      row_loss, dev_err, tid);
         if (!more) break;
-        row = next;
+        int64_t q4 = kUnknown;
+        if (live) {  // the k new rows t, t + 1, ... fill the unknown places
+            const int64_t t = base + __builtin_amdgcn_readfirstlane(tks[tp]);
+            tp ^= 1;
+            if (q2 == kUnknown) {
+                q2 = t;
+                q3 = t + 1;
+                q4 = t + 2;
+            } else if (q3 == kUnknown) {
+                q3 = t;
+                q4 = t + 1;
+            } else {
+                q4 = t;
+            }
+        }
+        row = q1;
+        q1 = q2;
+        q2 = q3;
+        q3 = q4;
         w = w_next;
         y = y_next;
         live = live_next;
@@ -488,7 +572,8 @@ grpo_rows_hybrid(const uint16_t* logits, int64_t ld, int V, int64_t N,
                  const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
                  const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
                  float* __restrict__ tok_loss_out, float* __restrict__ entropy_out,
-                 float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err) {
+                 float* __restrict__ row_loss, uint16_t* dlogits, int32_t* __restrict__ dev_err,
+                   int32_t* /*queue: the persistent form's only*/) {
     __shared__ HybridLds<ENT> lds;
     const int tid = threadIdx.x;
     const int64_t row = blockIdx.x;
@@ -520,7 +605,7 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
     const float* __restrict__ adv_tok, const float* __restrict__ w_tok, Params p,
     float* __restrict__ logp_out, float* __restrict__ tok_loss_out,
     float* __restrict__ entropy_out, float* __restrict__ row_loss, uint16_t* dlogits,
-    int32_t* __restrict__ dev_err) {
+    int32_t* __restrict__ dev_err, int32_t* /*queue: the persistent form's only*/) {
     __shared__ float s_m[BLOCK / kWave];
     __shared__ float s_s[BLOCK / kWave];
     __shared__ float s_t[ENT ? BLOCK / kWave : 1];
@@ -641,14 +726,14 @@ __global__ __launch_bounds__(BLOCK) void grpo_rows_stream(
 // ---------------------------------------------------------------------------
 using RowKernel = void (*)(const uint16_t*, int64_t, int, int64_t, const int32_t*, const float*,
                            const float*, const float*, const float*, Params, float*, float*,
-                           float*, float*, uint16_t*, int32_t*);
+                           float*, float*, uint16_t*, int32_t*, int32_t*);
 
 struct RowConfig {
     RowKernel fn;      // without the entropy output
     RowKernel fn_ent;  // with it
     int block;
     int ch;           // 0: streaming variant
-    bool persistent;  // one workgroup per compute unit, rows strided by the grid
+    bool persistent;  // one workgroup per compute unit, rows from a queue
 };
 
 #define LEAP_RES(B, C, S) \
@@ -663,8 +748,12 @@ struct RowConfig {
 // 12 and 16 chunks it measured equal or slower (at 8 chunks the one-row
 // kernel fits two workgroups per compute unit, the persistent loop one), and
 // at 20 and 24 chunks the loop's extra live state would spill, so those
-// shapes keep one workgroup per row.
-RowConfig pick_row_config(int V) {
+// shapes keep one workgroup per row.  The persistent kernel's row queue
+// counts in 32 bits: beyond kQueueMaxRows rows (far more than any device
+// holds at these widths) the same shape runs one workgroup per row.
+constexpr int64_t kQueueMaxRows = int64_t{1} << 30;
+
+RowConfig pick_row_config(int V, int64_t N) {
     static const RowConfig table[] = {
         LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
         LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
@@ -674,6 +763,9 @@ RowConfig pick_row_config(int V) {
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
+    if (i >= 0 && table[i].persistent && N > kQueueMaxRows)
+        return RowConfig{grpo_rows_resident<1024, 19, 16, false>,
+                         grpo_rows_resident<1024, 19, 16, true>, 1024, 19, false};
     if (i >= 0) return table[i];
     if (V <= kHybridMaxV)
         return RowConfig{grpo_rows_hybrid<false>, grpo_rows_hybrid<true>, 1024, kHybridCH, false};
@@ -686,11 +778,21 @@ RowConfig pick_row_config(int V) {
 }  // namespace
 }  // namespace leap
 
-LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
-    (void)V;
-    // one fp32 weighted loss per row, in whole 256-byte lines
+namespace leap {
+namespace {
+// Workspace of the fused call: one fp32 weighted loss per row in whole
+// 256-byte lines, then one line holding the persistent kernel's row queue.
+size_t row_loss_bytes(int64_t N) {
     const size_t b = static_cast<size_t>(N > 0 ? N : 1) * sizeof(float);
     return (b + 255) & ~static_cast<size_t>(255);
+}
+constexpr size_t kQueueBytes = 256;
+}  // namespace
+}  // namespace leap
+
+LEAP_API size_t leap_grpo_workspace_size(int64_t N, int32_t V) {
+    (void)V;
+    return leap::row_loss_bytes(N) + leap::kQueueBytes;
 }
 
 namespace leap {
@@ -730,20 +832,22 @@ leap_status check_fused_args(const void* logits_bf16, int64_t ld, int64_t N, int
 }
 
 // The row kernel, then the fixed-order loss sum, with the per-row weighted
-// losses in row_loss (N floats).
+// losses in row_loss (N floats) and the persistent kernel's row queue in
+// *queue (zeroed here before that kernel).
 leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t V,
                          const int32_t* token_ids, const float* old_logp, const float* ref_logp,
                          const float* adv_tok, const float* w_tok, const leap_grpo_params& pp,
                          float* logp_out, float* tok_loss_out, float* entropy_out, float* loss_out,
-                         void* dlogits_bf16, float* row_loss, int32_t* dev_err,
+                         void* dlogits_bf16, float* row_loss, int32_t* queue, int32_t* dev_err,
                          hipStream_t stream) {
     const LaunchCheck lc;
     const Params p{pp.clip_eps_low, pp.clip_eps_high, pp.kl_coef, pp.inv_temperature, pp.kl_type};
     if (N > 0) {
-        const RowConfig rc = pick_row_config(V);
+        const RowConfig rc = pick_row_config(V, N);
         int64_t grid = N;
         const RowKernel fn = entropy_out ? rc.fn_ent : rc.fn;
         if (rc.persistent) {
+            hipLaunchKernelGGL(queue_reset_kernel, dim3(1), dim3(kWave), 0, stream, queue);
             // as many workgroups as the device holds at once
             int dev = 0, cus = 0, per_cu = 0;
             if (hipGetDevice(&dev) != hipSuccess ||
@@ -759,7 +863,7 @@ leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t
                            dim3(rc.block), 0, stream, static_cast<const uint16_t*>(logits_bf16), ld,
                            V, N, token_ids, old_logp, ref_logp, adv_tok, w_tok, p, logp_out,
                            tok_loss_out, entropy_out, row_loss,
-                           static_cast<uint16_t*>(dlogits_bf16), dev_err);
+                           static_cast<uint16_t*>(dlogits_bf16), dev_err, queue);
         const leap_status st = lc.status();
         if (st != LEAP_OK) return st;
     }
@@ -768,12 +872,15 @@ leap_status launch_fused(const void* logits_bf16, int64_t ld, int64_t N, int32_t
     return lc.status();
 }
 
-// Per-row loss scratch of the no-allocation entry point: one array per
-// device, held from the library's load until the process ends.  Every call
-// on a device reuses it, so calls that overlap on one device (different
-// streams without ordering) race on it.  Nothing needs clearing: the row
-// kernel writes all N entries before the loss sum reads them.
-static __device__ __align__(256) float scratch[LEAP_NOALLOC_MAX_ROWS];
+// Scratch of the no-allocation entry point: the per-row losses, then one
+// 256-byte line for the row queue; one array per device, held from the
+// library's load until the process ends.  Every call on a device reuses it,
+// so calls that overlap on one device (different streams without ordering)
+// race on it.  Nothing needs clearing by the caller: the row kernel writes
+// all N losses before the loss sum reads them, and the call zeroes the
+// queue itself.
+constexpr int kScratchFloats = LEAP_NOALLOC_MAX_ROWS + static_cast<int>(kQueueBytes / sizeof(float));
+static __device__ __align__(256) float scratch[kScratchFloats];
 
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
@@ -812,9 +919,11 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd(
     if (st != LEAP_OK) return st;
     if (!workspace || ws_bytes < leap_grpo_workspace_size(N, V)) return LEAP_ERR_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return LEAP_ERR_MISALIGNED;
+    char* ws = static_cast<char*>(workspace);
     return launch_fused(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
                         *params, logp_out, tok_loss_out, entropy_out, loss_out, dlogits_bf16,
-                        static_cast<float*>(workspace), dev_err, stream);
+                        reinterpret_cast<float*>(ws),
+                        reinterpret_cast<int32_t*>(ws + row_loss_bytes(N)), dev_err, stream);
 }
 
 LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd_noalloc(
@@ -831,5 +940,6 @@ LEAP_API leap_status leap_grpo_logprob_loss_fwd_bwd_noalloc(
     if ((st = scratch_for_current_device(&row_loss)) != LEAP_OK) return st;
     return launch_fused(logits_bf16, ld, N, V, token_ids, old_logp, ref_logp, adv_tok, w_tok,
                         *params, logp_out, tok_loss_out, entropy_out, loss_out, dlogits_bf16,
-                        row_loss, dev_err, stream);
+                        row_loss, reinterpret_cast<int32_t*>(row_loss + LEAP_NOALLOC_MAX_ROWS),
+                        dev_err, stream);
 }

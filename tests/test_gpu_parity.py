@@ -363,6 +363,63 @@ def test_grpo_inplace_and_deterministic(V, N):
                     kw=KW)
 
 
+# The persistent kernel's row queue (131072 < V <= 155648): each workgroup's
+# four fixed rows, then rows taken from the queue three ahead; runs of
+# excluded rows long enough that workgroups take three or more in a row and
+# refill the queue synchronously; tickets past N.  131080 columns is the
+# shape's narrowest width (its last two register chunks are empty in the
+# first wave).
+def _queue_weights(pattern, N, rng):
+    w = rng.choice([0.5, 1.0], N).astype(np.float32)
+    if pattern == "alt":
+        w[1::2] = 0.0
+    elif pattern == "runs":  # masked runs of 900 and 500 rows, and a tail run
+        w[1024:1924] = 0.0
+        w[2000:2500] = 0.0
+        w[N - 40:] = 0.0
+    elif pattern == "sparse":  # 5% live
+        w[rng.random(N) >= 0.05] = 0.0
+    return w
+
+
+QUEUE_CASES = [(151936, 1, "live"), (151936, 255, "live"), (151936, 1024, "alt"),
+               (151936, 1100, "live"), (151936, 2600, "runs"), (131080, 2600, "sparse"),
+               (131080, 1500, "alt")]
+
+
+@pytest.mark.parametrize("V,N,pattern", QUEUE_CASES,
+                         ids=[f"V{v}-N{n}-{p}" for v, n, p in QUEUE_CASES])
+def test_grpo_row_queue(V, N, pattern):
+    import torch
+    rng = np.random.default_rng(N + V)
+    ld = (V + 7) // 8 * 8
+    U.log(f"grpo row queue V={V} N={N} {pattern}: generating logits")
+    lg_dev = torch.empty((N, ld), dtype=torch.bfloat16, device=U.dev())
+    wl.logits_device(4242 + N, N, V, ld=ld, device=U.dev(), out=lg_dev)
+    tok = wl.sample_tokens_device(lg_dev[:, :V], V, 4242 + N).cpu().numpy()
+    lg = lg_dev.view(torch.int16).cpu().numpy().view(np.uint16)
+    cur, _ = oracle.logprob_rows(lg, tok, V=V)
+    old = (cur + rng.normal(0, 0.05, N)).astype(np.float32)
+    ref = (cur + rng.normal(0, 0.1, N)).astype(np.float32)
+    adv = rng.normal(0, 1.5, N).astype(np.float32)
+    w = _queue_weights(pattern, N, rng)
+    a = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, want_entropy=True, **KW)
+    b = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, want_entropy=True, **KW)
+    assert torch.equal(a["dl_dev"].view(torch.int16), b["dl_dev"].view(torch.int16))
+    assert a["loss"] == b["loss"] and np.array_equal(a["logp"], b["logp"])
+    assert np.array_equal(a["entropy"], b["entropy"])
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
+    valid = w != 0
+    _check_rows(a, o, valid, f"V={V} N={N} {pattern}")
+    dead = torch.as_tensor(np.flatnonzero(~valid), device=U.dev())
+    if dead.numel():
+        assert int(a["dl_dev"].index_select(0, dead)[:, :V].view(torch.int16).abs().max()) == 0
+    live = np.flatnonzero(valid)
+    rows = live if live.size <= 48 else live[np.linspace(0, live.size - 1, 48).astype(int)]
+    U.check_dlogits(U.dl_rows(a["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
+                    atol=2e-2, kw=KW)
+
+
 def test_grpo_all_masked_and_empty():
     N, V = 32, 1024
     lg, tok, old, ref = U.make_inputs_host(3, N, V)
