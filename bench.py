@@ -960,7 +960,7 @@ def main():
                    "vocab": V, "microbatch_rows": R, "G": meta["G"], "max_turns": meta["M"]},
         "roofline": {"bound": "hbm", "achieved": m["achieved"] / 1e9, "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": m["achieved"] / HBM_PEAK, "traffic": traffic,
-                     "kernel": "grpo_rows_persist<1024,19,16,false> + loss_reduce (one fused call)",
+                     "kernel": "queue_reset + grpo_rows_persist<1024,19,16,false> + loss_reduce (one fused call)",
                      "avg_launch_us": m["k4_avg_s"] * 1e6, "median_launch_us": m["k4_median_us"],
                      "bytes_per_launch": m["bytes_per_launch"], "probe_GBps": probe,
                      "frac_of_probe_copy": m["achieved"] / 1e9 / probe["copy_GBps"]},
