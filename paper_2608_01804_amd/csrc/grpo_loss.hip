@@ -170,8 +170,8 @@ __device__ __forceinline__ void dlogits_pass_vgpr(u32x4 (&x)[CH], float sc, floa
 // scalar epilogue, the dlogits stores and the row's outputs.  A row whose
 // logits are all -inf is counted and zero-filled instead.  One barrier
 // (inside the block merge) in every call.  With tk_slot set, thread 0
-// stores tk there after pass A, so the value is in LDS for every thread once
-// the merge's barrier has passed.
+// stores *tk there after pass A, so the value is in LDS for every thread
+// once the merge's barrier has passed (*tk is read in thread 0 only).
 template <int BLOCK, int CH, int SAFE, bool ENT>
 __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row, uint16_t* drow,
                                           int V, int y, float w, const float* __restrict__ old_logp,
@@ -182,12 +182,12 @@ __device__ __forceinline__ void fused_row(u32x4 (&x)[CH], float xy, int64_t row,
                                           float* __restrict__ entropy_out,
                                           float* __restrict__ row_loss, int32_t* __restrict__ dev_err,
                                           RowLds<BLOCK, ENT>& lds, int tid, int* tk_slot = nullptr,
-                                          int tk = 0) {
+                                          const int* tk = nullptr) {
     mask_row_tail<BLOCK, CH, SAFE>(x, V, tid);
 
     // Pass A: lane maximum over the raw bf16 words.
     const float m = row_lane_max<CH>(x);
-    if (tk_slot && tid == 0) *tk_slot = tk;
+    if (tk_slot && tid == 0) *tk_slot = *tk;
 
     // Keep the bf16 words as the only live copy of the row.
 #pragma unroll
@@ -352,7 +352,7 @@ grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
         }
         const bool more = q1 < N;
         const int k = 1 + (q2 == kUnknown) + (q3 == kUnknown);
-        int tk;  // set and read in thread 0 of a live row only
+        int tk;  // set, and read through fused_row's pointer, in thread 0 of a live row only
         if (live && tid == 0) tk = queue_take(queue, k);
         const float w_next = more ? w_tok[q1] : 0.0f;
         const int y_next = more ? token_ids[q1] : 0;
@@ -362,7 +362,7 @@ grpo_rows_persist(const uint16_t* logits, int64_t ld, int V, int64_t N,
             fused_row<BLOCK, CH, SAFE, ENT>(x, __uint_as_float(xyb << 16), row, drow, V, y, w,
                                             old_logp, ref_logp, adv_tok, p, logp_out,
                                             tok_loss_out, entropy_out, row_loss, dev_err,
-                                            lds[parity], tid, &tks[tp], tk);
+                                            lds[parity], tid, &tks[tp], &tk);
             parity ^= 1;
         }
         if (live_next) issue_row(q1, y_next);
