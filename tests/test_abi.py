@@ -38,6 +38,39 @@ def test_library_exports_every_declared_symbol():
     assert exported == set(_declared())
 
 
+C_CALLER = r"""
+#include <stdio.h>
+#include "leap.h"
+int main(void) {
+    int32_t lo = -1, hi = -1;
+    leap_status st = leap_dcp_tau_from_pass_rate(16, 0, 1, 1, 3, 4, 1, &lo, &hi);
+    printf("%s %s %d %d\n", leap_version(), leap_status_string(st), (int)lo, (int)hi);
+    printf("%zu %zu\n", leap_grpo_workspace_size(16384, 151936),
+           leap_vocab_merge_workspace_size(16384));
+    return st == LEAP_OK ? 0 : 1;
+}
+"""
+
+
+def test_header_compiles_as_c99_and_links(tmp_path):
+    """A C99 caller (strict warnings on everything but the ROCm headers)
+    includes leap.h, links libleap.so and calls its host-only entry points."""
+    src = tmp_path / "caller.c"
+    src.write_text(C_CALLER)
+    exe = tmp_path / "caller"
+    pkg = os.path.dirname(L.LIB_PATH)
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                    "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
+                    "-isystem", os.path.join(rocm, "include"), str(src), "-L" + pkg, "-lleap",
+                    "-Wl,-rpath," + pkg, "-o", str(exe)], check=True, capture_output=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
+    tmin, tmax = L.leap_dcp_tau_from_pass_rate(16, 0, 1, 1, 3, 4, 1)
+    assert out[:4] == [L.leap_version(), "LEAP_OK", str(tmin), str(tmax)]
+    assert int(out[4]) == L.leap_grpo_workspace_size(16384, 151936)
+    assert int(out[5]) == L.leap_vocab_merge_workspace_size(16384)
+
+
 def test_status_strings_and_version():
     assert L.leap_status_string(0) == "LEAP_OK"
     assert L.leap_status_string(3) == "LEAP_ERR_WORKSPACE"
