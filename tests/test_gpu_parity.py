@@ -420,6 +420,58 @@ def test_grpo_row_queue(V, N, pattern):
                     atol=2e-2, kw=KW)
 
 
+def test_grpo_overlapping_calls_on_two_streams():
+    """Two fused calls with their own workspaces and outputs, launched on two
+    streams without ordering between them, give bitwise the results of the
+    same calls run one after the other.  Each call's row queue lives in its
+    own workspace, and no workgroup waits for another, so the two persistent
+    grids need not be resident together."""
+    import torch
+    from paper_2608_01804_amd import leap as L
+    V, N = 151936, 2000
+    cases = []
+    for seed in (11, 12):
+        rng = np.random.default_rng(seed)
+        lg = torch.empty((N, V), dtype=torch.bfloat16, device=U.dev())
+        wl.logits_device(seed, N, V, device=U.dev(), out=lg)
+        tok = wl.sample_tokens_device(lg, V, seed)
+        old = torch.from_numpy(rng.normal(-11.0, 0.5, N).astype(np.float32)).to(U.dev())
+        adv = torch.from_numpy(rng.normal(0, 1, N).astype(np.float32)).to(U.dev())
+        w = torch.from_numpy(rng.choice([0.0, 1.0], N, p=[0.3, 0.7]).astype(np.float32)).to(U.dev())
+        cases.append((lg, tok, old, adv, w))
+    p = L.leap_grpo_params(0.2, 0.2, 0.01, 0, 1.0)
+    wsb = L.leap_grpo_workspace_size(N, V)
+
+    def outputs():
+        return [dict(dl=torch.empty((N, V), dtype=torch.bfloat16, device=U.dev()),
+                     lp=torch.empty(N, dtype=torch.float32, device=U.dev()),
+                     loss=torch.empty(1, dtype=torch.float32, device=U.dev()),
+                     ws=torch.empty(wsb, dtype=torch.uint8, device=U.dev())) for _ in cases]
+
+    def launch(case, o, stream):
+        lg, tok, old, adv, w = case
+        L.leap_grpo_logprob_loss_fwd_bwd(lg, V, N, V, tok, old, old, adv, w, p, o["lp"], None,
+                                         None, o["loss"], o["dl"], o["ws"], wsb, None,
+                                         stream=stream)
+
+    U.log("fused calls one after the other, then overlapping on two streams")
+    seq = outputs()
+    for c, o in zip(cases, seq):
+        launch(c, o, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    par = outputs()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        for c, o, s in zip(cases, par, streams):
+            launch(c, o, s)
+    torch.cuda.synchronize()
+    for a, b in zip(seq, par):
+        assert torch.equal(a["dl"].view(torch.int16), b["dl"].view(torch.int16))
+        assert torch.equal(a["lp"], b["lp"]) and torch.equal(a["loss"], b["loss"])
+
+
 def test_grpo_all_masked_and_empty():
     N, V = 32, 1024
     lg, tok, old, ref = U.make_inputs_host(3, N, V)
