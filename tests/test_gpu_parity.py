@@ -257,6 +257,8 @@ def test_grpo_wide_range_and_peaked_rows(V):
 SHAPES = [(16, 16, 64), (100, 104, 64), (1000, 1008, 64), (4093, 4096, 32), (8192, 8192, 32),
           (32000, 32000, 32), (32768, 32768, 32), (50257, 50264, 16), (65536, 65536, 16),
           (100000, 100000, 16), (128256, 128256, 16), (151936, 151936, 16),
+          # the persistent kernel with a partial last chunk and padding columns
+          (150001, 150016, 300),
           (152064, 152064, 16), (160000, 160000, 8), (196608, 196608, 8),
           # rows held partly in LDS (196608 < V <= 270336): one LDS slot with a
           # partial chunk, a ragged middle, exactly 32768 chunks, the largest
