@@ -25,8 +25,8 @@
 //    value directly, packed to bf16 with v_cvt_pk_bf16_f32 (RNE) and stored
 //    16 bytes at a time; the token's own column gets g * (1 - p_y).
 //  * Rows with zero weight are not read: their dlogits row is zero-filled.
-//  * For the 19-chunk shape (one workgroup per compute unit) the kernel is
-//    persistent: a grid of one workgroup per CU takes rows from a row queue
+//  * From 55296 to 155648 columns (one workgroup per compute unit) the kernel
+//    is persistent: a grid of one workgroup per CU takes rows from a row queue
 //    (a counter in the workspace) and issues the next row's loads right
 //    behind the current row's stores, so each CU's reads overlap its writes
 //    instead of waiting for a new workgroup to be dispatched after each row,
@@ -742,34 +742,44 @@ struct RowConfig {
     RowConfig{grpo_rows_persist<B, C, S, false>, grpo_rows_persist<B, C, S, true>, B, C, true}
 
 // The kernel for V: the resident shape row::pick_resident_shape chooses, or
-// the streaming variant.  The 19-chunk shape (131072 < V <= 155648, which
-// holds the 151936- and 152064-column vocabularies) runs persistent: measured
-// on the MI355X it is 2-3% faster there than one workgroup per row.  At 8,
-// 12 and 16 chunks it measured equal or slower (at 8 chunks the one-row
-// kernel fits two workgroups per compute unit, the persistent loop one), and
-// at 20 and 24 chunks the loop's extra live state would spill, so those
-// shapes keep one workgroup per row.  The persistent kernel's row queue
-// counts in 32 bits: beyond kQueueMaxRows rows (far more than any device
-// holds at these widths) the same shape runs one workgroup per row.
+// the streaming variant.  From 55296 to 155648 columns (the 1024-lane shapes
+// of 8, 12, 16 and 19 chunks per lane) the row kernel runs persistent with
+// the row queue: measured on the MI355X with every row live it is 1.4-13.5%
+// faster there than one workgroup per row (6-10% at 12 chunks; 2-3% at 16
+// and 19 chunks on full lines).  Below 55296 columns the 8-chunk one-row
+// kernel, which fits two workgroups per compute unit against the persistent
+// loop's one, stays ahead (1-24%), and at 20 and 24 chunks the loop's live
+// state would spill, so those widths keep one workgroup per row.  The row
+// queue counts in 32 bits: beyond kQueueMaxRows rows (far more than any
+// device holds at these widths) the one-row kernel of the same shape runs.
 constexpr int64_t kQueueMaxRows = int64_t{1} << 30;
+constexpr int kPersistMinV = 55297;
 
 RowConfig pick_row_config(int V, int64_t N) {
     static const RowConfig table[] = {
         LEAP_RES(64, 1, 0),     LEAP_RES(64, 2, 1),     LEAP_RES(64, 4, 2),
         LEAP_RES(64, 8, 4),     LEAP_RES(256, 4, 0),    LEAP_RES(256, 8, 4),
         LEAP_RES(256, 12, 8),   LEAP_RES(256, 16, 12),  LEAP_RES(1024, 8, 0),
-        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_PER(1024, 19, 16),
+        LEAP_RES(1024, 12, 8),  LEAP_RES(1024, 16, 12), LEAP_RES(1024, 19, 16),
         LEAP_RES(1024, 20, 19), LEAP_RES(1024, 24, 20),
+    };
+    static const RowConfig persist[] = {
+        LEAP_PER(1024, 8, 0), LEAP_PER(1024, 12, 8), LEAP_PER(1024, 16, 12),
+        LEAP_PER(1024, 19, 16),
     };
     static_assert(sizeof(table) / sizeof(table[0]) == kNumResidentShapes, "shape table");
     const int i = pick_resident_shape(V);
-    if (i >= 0 && table[i].persistent && N > kQueueMaxRows)
-        return RowConfig{grpo_rows_resident<1024, 19, 16, false>,
-                         grpo_rows_resident<1024, 19, 16, true>, 1024, 19, false};
-    if (i >= 0) return table[i];
-    if (V <= kHybridMaxV)
-        return RowConfig{grpo_rows_hybrid<false>, grpo_rows_hybrid<true>, 1024, kHybridCH, false};
-    return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0, false};
+    if (i < 0) {
+        if (V <= kHybridMaxV)
+            return RowConfig{grpo_rows_hybrid<false>, grpo_rows_hybrid<true>, 1024, kHybridCH,
+                             false};
+        return RowConfig{grpo_rows_stream<1024, false>, grpo_rows_stream<1024, true>, 1024, 0,
+                         false};
+    }
+    if (V >= kPersistMinV && N <= kQueueMaxRows && table[i].block == 1024 && table[i].ch <= 19)
+        for (const RowConfig& rc : persist)
+            if (rc.ch == table[i].ch) return rc;
+    return table[i];
 }
 
 #undef LEAP_RES

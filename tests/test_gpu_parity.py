@@ -365,12 +365,12 @@ def test_grpo_inplace_and_deterministic(V, N):
                     kw=KW)
 
 
-# The persistent kernel's row queue (131072 < V <= 155648): each workgroup's
+# The persistent kernel's row queue (55296 < V <= 155648): each workgroup's
 # four fixed rows, then rows taken from the queue three ahead; runs of
 # excluded rows long enough that workgroups take three or more in a row and
 # refill the queue synchronously; tickets past N.  131080 columns is the
-# shape's narrowest width (its last two register chunks are empty in the
-# first wave).
+# 19-chunk shape's narrowest width (its last two register chunks are empty
+# in the first wave), 55297 the persistent range's first.
 def _queue_weights(pattern, N, rng):
     w = rng.choice([0.5, 1.0], N).astype(np.float32)
     if pattern == "alt":
@@ -386,7 +386,12 @@ def _queue_weights(pattern, N, rng):
 
 QUEUE_CASES = [(151936, 1, "live"), (151936, 255, "live"), (151936, 1024, "alt"),
                (151936, 1100, "live"), (151936, 2600, "runs"), (131080, 2600, "sparse"),
-               (131080, 1500, "alt")]
+               (131080, 1500, "alt"),
+               # the 16-, 12- and 8-chunk shapes' persistent ranges, and the
+               # width just below them (one workgroup per row)
+               (100003, 2600, "runs"), (128256, 1300, "live"), (73728, 2600, "sparse"),
+               (98304, 1100, "alt"), (55297, 2600, "runs"), (65536, 1300, "live"),
+               (55296, 1100, "alt")]
 
 
 @pytest.mark.parametrize("V,N,pattern", QUEUE_CASES,
