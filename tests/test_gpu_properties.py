@@ -142,6 +142,74 @@ def test_fused_objective_matches_oracle(c):
 
 
 @st.composite
+def queue_cases(draw):
+    """A microbatch for the persistent row-queue kernel: a width in its range
+    (55297-155648 columns), more rows than the workgroups' four fixed rows
+    each cover, masked runs of random lengths (long runs make workgroups
+    refill the queue synchronously), random clip bounds, KL and the entropy
+    output."""
+    V = draw(st.integers(55297, 155648))
+    N = draw(st.integers(1025, 3000))
+    runs = draw(st.lists(st.tuples(st.integers(0, N - 1), st.integers(1, 1200)), max_size=4))
+    return dict(V=V, N=N, runs=runs, seed=draw(st.integers(0, 2**31 - 1)),
+                p_masked=draw(st.floats(0.0, 0.3)),
+                eps_lo=draw(st.floats(0.0, 0.5)), eps_hi=draw(st.floats(0.0, 0.5)),
+                kl_coef=draw(st.floats(0.0, 0.5)),
+                kl_type=draw(st.sampled_from([oracle.KL_K3, oracle.KL_K1, oracle.KL_K2])),
+                entropy=draw(st.booleans()))
+
+
+@settings(max_examples=8, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(queue_cases())
+def test_row_queue_matches_oracle(c):
+    """The persistent row-queue kernel on random widths, row counts and mask
+    runs against the oracle: every log-prob and per-token loss, the loss,
+    the entropy, excluded rows zero-filled, and 32 sampled rows of dlogits
+    (1e-2 of the largest entry)."""
+    import torch
+    V, N = c["V"], c["N"]
+    ld = (V + 7) // 8 * 8
+    rng = np.random.default_rng(c["seed"])
+    U.log(f"row-queue property case V={V} N={N} runs={c['runs']}")
+    lg_dev = torch.empty((N, ld), dtype=torch.bfloat16, device=U.dev())
+    seed = c["seed"] % 100000
+    wl.logits_device(seed, N, V, ld=ld, device=U.dev(), out=lg_dev)
+    tok = wl.sample_tokens_device(lg_dev[:, :V], V, seed).cpu().numpy()
+    lg = lg_dev.view(torch.int16).cpu().numpy().view(np.uint16)
+    cur, _ = oracle.logprob_rows(lg, tok, V=V)
+    old = (cur + rng.normal(0, 0.05, N)).astype(np.float32)
+    ref = (cur + rng.normal(0, 0.1, N)).astype(np.float32)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = rng.uniform(0.1, 1.0, N).astype(np.float32)
+    w[rng.random(N) < c["p_masked"]] = 0.0
+    for s0, length in c["runs"]:
+        w[s0:s0 + length] = 0.0
+    kw = dict(eps_lo=c["eps_lo"], eps_hi=c["eps_hi"], kl_coef=c["kl_coef"],
+              kl_type=c["kl_type"])
+    gpu = U.run_grpo(lg_dev, V, tok, old, ref, adv, w, want_entropy=c["entropy"], **kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **kw)
+    valid = w != 0
+    assert gpu["bad"] == o["bad"] == 0
+    assert np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0) < 2e-3
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-6
+    dead = torch.as_tensor(np.flatnonzero(~valid), device=U.dev())
+    if dead.numel():
+        assert int(gpu["dl_dev"].index_select(0, dead)[:, :V].view(torch.int16).abs().max()) == 0
+    live = np.flatnonzero(valid)
+    rows = live if live.size <= 32 else live[np.linspace(0, live.size - 1, 32).astype(int)]
+    U.check_dlogits(U.dl_rows(gpu["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V,
+                    atol=1e-2, kw=kw, rel_to_max=True, floor=1e-6)
+    if c["entropy"]:
+        h, _ = oracle.entropy_rows(lg, V=V)
+        assert np.all(gpu["entropy"][~valid] == 0)
+        np.testing.assert_allclose(gpu["entropy"][valid], h[valid], rtol=1e-4, atol=2e-4)
+
+
+@st.composite
 def shard_cases(draw):
     """A vocabulary split into 1-8 shards of random widths (one column
     upwards), with the objective's parameters drawn as for the fused call
