@@ -61,11 +61,16 @@ def _assert_same(a, b):
 
 
 def test_noalloc_matches_workspace_form_two_calls():
-    # 1: 3000 rows of a 151936-column vocabulary; 2: 700 rows of 32768
+    # 1: 3000 rows of a 151936-column vocabulary; 2: 1500 rows of 100000 (the
+    # 16-chunk persistent kernel); 3: 700 rows of 32768 (one workgroup per
+    # row); each call smaller than the one before
     U.log("noalloc call 1: N=3000 V=151936")
     a, b = _run_both(3000, 151936, 71, want_entropy=True)
     _assert_same(a, b)
-    U.log("noalloc call 2: N=700 V=32768 (smaller)")
+    U.log("noalloc call 2: N=1500 V=100000 (smaller)")
+    a, b = _run_both(1500, 100000, 74, want_entropy=False)
+    _assert_same(a, b)
+    U.log("noalloc call 3: N=700 V=32768 (smaller)")
     a, b = _run_both(700, 32768, 72, want_entropy=False)
     _assert_same(a, b)
 
