@@ -849,6 +849,60 @@ def all_live_leg(L, torch, s, reps: int = 20):
             "bytes_per_call": nbytes}
 
 
+# Vocabulary widths of the width leg, with their row strides (odd widths on
+# the 128-byte grid): the one-row kernels, the persistent row-queue range
+# (55297-155648 columns) and the hybrid register + LDS rows.
+WIDTHS = [(32768, 32768), (50257, 50304), (65536, 65536), (100000, 100000), (128256, 128256),
+          (151936, 151936), (200003, 200064), (262144, 262144)]
+
+
+def width_leg(L, torch, dev, reps: int = 20, R: int = 16384):
+    """The fused call across vocabulary widths: 16384 rows of synthetic
+    logits per width (bf16 N(0, 2^2), tokens sampled from them), every row
+    live (weight 1/R), HIP events around `reps` back-to-back calls after a
+    settling run; algorithmic bytes as in the headline (4V + 28 per row)."""
+    import workloads as wl
+    out = []
+    for V, ld in WIDTHS:
+        lg = torch.empty((R, ld), dtype=torch.bfloat16, device=dev)
+        wl.logits_device(4000 + V, R, V, ld=ld, device=dev, out=lg)
+        tok = wl.sample_tokens_device(lg[:, :V], V, 4000 + V)
+        dl = torch.empty_like(lg)
+        cur = torch.empty(R, dtype=torch.float32, device=dev)
+        L.leap_logprob_fwd(lg, ld, R, V, tok, None, 1.0, cur)
+        rng = np.random.default_rng(V)
+        old = cur + torch.from_numpy(rng.normal(0, 0.05, R).astype(np.float32)).to(dev)
+        adv = torch.from_numpy(rng.normal(0, 1, R).astype(np.float32)).to(dev)
+        w = torch.full((R,), 1.0 / R, dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        ws_bytes = L.leap_grpo_workspace_size(R, V)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        p = L.leap_grpo_params(0.2, 0.2, 0.01, L.LEAP_KL_K3, 1.0)
+        stream = torch.cuda.current_stream()
+
+        def call():
+            L.leap_grpo_logprob_loss_fwd_bwd(lg, ld, R, V, tok, old, cur, adv, w, p, None, None,
+                                             None, loss, dl, ws, ws_bytes, None)
+
+        settle(torch, call, 200)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps / 1e3
+        nbytes = R * row_bytes(V, True)
+        log(f"[bench] width {V} (ld {ld}): {t * 1e6:.1f} us, {nbytes / t / 1e9:.0f} GB/s = "
+            f"{nbytes / t / HBM_PEAK:.3f} of 8 TB/s")
+        out.append({"V": V, "ld": ld, "call_us": t * 1e6, "GBps": nbytes / t / 1e9,
+                    "frac": nbytes / t / HBM_PEAK})
+        del lg, dl
+        torch.cuda.empty_cache()
+    return {"workload": f"fused call, {R} rows per width, every row live", "widths": out}
+
+
 WORKLOAD_TEXT = {
     "full": "full: 64 prompts x G=16, up to 3 turns, U[512,4096] tokens/turn with U[64,512] "
             "masked feedback rows between turns, V={V}, {n_mb} microbatches x {R} rows "
@@ -875,6 +929,8 @@ def main():
     ap.add_argument("--lmhead-reps", type=int, default=5,
                     help="timed calls of the fused LM-head variant (0 skips it)")
     ap.add_argument("--no-shard", action="store_true", help="skip the vocabulary-shard leg")
+    ap.add_argument("--no-widths", action="store_true",
+                    help="skip the leg across vocabulary widths")
     ap.add_argument("--no-mid", action="store_true", help="skip the secondary mid-step leg")
     ap.add_argument("--no-legs", action="store_true",
                     help="only the headline step (for profiling its kernel)")
@@ -925,6 +981,7 @@ def main():
             log(f"[bench] oracle on the host ({args.cpu_seconds:.0f} s sample)")
             cpu = cpu_baseline(s, args.cpu_seconds)
         legs["all_live"] = all_live_leg(L, torch, s)
+        legs["widths"] = width_leg(L, torch, dev) if not args.no_widths else None
         legs["vocab_shard"] = shard_leg(L, torch, s) if not args.no_shard else None
         legs["logprob_fwd"] = logprob_leg(L, torch, s)
         legs["entropy"] = entropy_leg(L, torch, s)
