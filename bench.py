@@ -860,7 +860,9 @@ def width_leg(L, torch, dev, reps: int = 20, R: int = 16384):
     """The fused call across vocabulary widths: 16384 rows of synthetic
     logits per width (bf16 N(0, 2^2), tokens sampled from them), every row
     live (weight 1/R), HIP events around `reps` back-to-back calls after a
-    settling run; algorithmic bytes as in the headline (4V + 28 per row)."""
+    settling run; algorithmic bytes as in the headline (4V + 28 per row).
+    The forward-only log-prob call on the same rows beside it (2V + 8 bytes
+    per row)."""
     import workloads as wl
     out = []
     for V, ld in WIDTHS:
@@ -884,20 +886,27 @@ def width_leg(L, torch, dev, reps: int = 20, R: int = 16384):
             L.leap_grpo_logprob_loss_fwd_bwd(lg, ld, R, V, tok, old, cur, adv, w, p, None, None,
                                              None, loss, dl, ws, ws_bytes, None)
 
-        settle(torch, call, 200)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            call()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        t = e0.elapsed_time(e1) / reps / 1e3
+        def timed(fn):
+            settle(torch, fn, 200)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps / 1e3
+
+        t = timed(call)
+        t_fwd = timed(lambda: L.leap_logprob_fwd(lg, ld, R, V, tok, None, 1.0, cur))
         nbytes = R * row_bytes(V, True)
+        fwd_bytes = R * (2 * V + 8)
         log(f"[bench] width {V} (ld {ld}): {t * 1e6:.1f} us, {nbytes / t / 1e9:.0f} GB/s = "
-            f"{nbytes / t / HBM_PEAK:.3f} of 8 TB/s")
+            f"{nbytes / t / HBM_PEAK:.3f} of 8 TB/s; forward-only {t_fwd * 1e6:.1f} us = "
+            f"{fwd_bytes / t_fwd / HBM_PEAK:.3f}")
         out.append({"V": V, "ld": ld, "call_us": t * 1e6, "GBps": nbytes / t / 1e9,
-                    "frac": nbytes / t / HBM_PEAK})
+                    "frac": nbytes / t / HBM_PEAK, "logprob_fwd_us": t_fwd * 1e6,
+                    "logprob_fwd_frac": fwd_bytes / t_fwd / HBM_PEAK})
         del lg, dl
         torch.cuda.empty_cache()
     return {"workload": f"fused call, {R} rows per width, every row live", "widths": out}
