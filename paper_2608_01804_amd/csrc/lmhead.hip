@@ -363,7 +363,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
     const float* __restrict__ ref_logp, const float* __restrict__ adv_tok,
     const float* __restrict__ w_tok, Params p, float* __restrict__ logp_out,
     float* __restrict__ tok_loss_out, float* __restrict__ row_loss, float* __restrict__ g_out,
-    float* __restrict__ lse2_out, int32_t* __restrict__ dev_err) {
+    float* __restrict__ lse2_out, float* __restrict__ dzy_out, int32_t* __restrict__ dev_err) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t j = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + (threadIdx.x / kWave);
     if (j >= n_rows) return;
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
     // log-sum-exp make every dZ entry of the row exactly zero.
     const int64_t row = rows[j];
     if (row < 0) {
-        if (lane == 0) g_out[j] = 0.0f, lse2_out[j] = INFINITY;
+        if (lane == 0) g_out[j] = 0.0f, lse2_out[j] = INFINITY, dzy_out[j] = 0.0f;
         return;
     }
     const float w = w_tok[row];
@@ -382,6 +382,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
             obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
             g_out[j] = 0.0f;
             lse2_out[j] = INFINITY;
+            dzy_out[j] = 0.0f;
         }
         return;
     }
@@ -418,6 +419,7 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
         obj::write_row_outputs(row, 0.0f, 0.0f, 0.0f, logp_out, tok_loss_out, row_loss);
         g_out[j] = 0.0f;
         lse2_out[j] = INFINITY;
+        dzy_out[j] = 0.0f;
         return;
     }
     const float lse2 = m + __builtin_amdgcn_logf(s);
@@ -425,6 +427,10 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
     obj::write_row_outputs(row, o.logp, o.loss, w, logp_out, tok_loss_out, row_loss);
     g_out[j] = o.g;
     lse2_out[j] = lse2;
+    // the token's own dZ entry, g (1 - p_y), in fp32 from the log-prob: the
+    // dZ epilogue stores it in place of -g p_y, so it keeps its relative
+    // precision when p_y is close to 1
+    dzy_out[j] = o.g * (1.0f - obj::hw_exp(o.logp));
 }
 
 // ---------------------------------------------------------------------------
@@ -438,7 +444,9 @@ __global__ __launch_bounds__(256) void lm_combine_kernel(
 // group h row 4h + p, columns 8q .. 8q+7 of the pair (the read pointer of
 // lane j is column 8 (j % 4) + j / 4, then 4 columns on).  Every element is
 // first -g p; the one lane of the grid that stores a row's token column
-// then adds g to it (in fp32 from the rounded value: within 2^-8 |g|).
+// then replaces that element with the row's g (1 - p_y), formed in fp32 by
+// the combine kernel (rounding -g p_y to bf16 first and adding g would cost
+// up to 2^-9 |g|, far more than g (1 - p_y) itself when p_y is near 1).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -468,7 +476,7 @@ __device__ __forceinline__ void quad_transpose(float (&d)[4], int lane) {
     }
 }
 
-constexpr int kDzStageBase = 4096;  // after the per-row arrays (3 KiB)
+constexpr int kDzStageBase = 4096;  // after the per-row arrays (4 KiB)
 constexpr int kDzStageBuf = 1024;   // [h][32 columns][4 rows] bf16
 static_assert(kDzStageBase + 4 * 2 * kDzStageBuf <= gemm::kLdsBytes, "dZ staging exceeds the LDS");
 
@@ -477,13 +485,12 @@ __device__ __forceinline__ uint2 read_tr16(const uint8_t* p) {
     return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p)));
 }
 
-// Add g to element e (0..7) of 8 packed bf16, through fp32.
-__device__ __forceinline__ u32x4 add_to_element(u32x4 x, int e, float gv) {
+// Element e (0..7) of 8 packed bf16 set to v (rounded to bf16).
+__device__ __forceinline__ u32x4 set_element(u32x4 x, int e, float v) {
     const int wi = e >> 1;
     const bool hi = (e & 1) != 0;
     uint32_t w = wi == 0 ? x.x : wi == 1 ? x.y : wi == 2 ? x.z : x.w;
-    const uint32_t bits = hi ? (w >> 16) : (w & 0xffffu);
-    const uint32_t nb = pack_bf16(__uint_as_float(bits << 16) + gv, 0.0f) & 0xffffu;
+    const uint32_t nb = pack_bf16(v, 0.0f) & 0xffffu;
     w = hi ? ((w & 0xffffu) | (nb << 16)) : ((w & 0xffff0000u) | nb);
     return u32x4{wi == 0 ? w : x.x, wi == 1 ? w : x.y, wi == 2 ? w : x.z, wi == 3 ? w : x.w};
 }
@@ -493,6 +500,7 @@ struct DzEpi {
     const int32_t* rows;       // [N_pad], compacted row -> caller row (-1: none)
     const float* lse2;         // [N_pad], compacted rows
     const float* g;            // [N_pad], compacted rows
+    const float* dzy;          // [N_pad], compacted rows: the token column's g (1 - p_y)
     uint16_t* dz;              // [N_pad][ld_dz], compacted rows, chunk-local columns
     int64_t ld_dz;
     int64_t N;                 // rows of lse2 / g / rows (N_pad)
@@ -503,6 +511,7 @@ struct DzEpi {
         float* s_l = reinterpret_cast<float*>(smem);
         float* s_g = s_l + kTile;
         int* s_y = reinterpret_cast<int*>(s_g + kTile);
+        float* s_dy = reinterpret_cast<float*>(s_y + kTile);
         const int tid = threadIdx.x;
         const int64_t row0 = static_cast<int64_t>(t.tm) * kTile;
         {
@@ -513,10 +522,12 @@ struct DzEpi {
                 const int src = rows[r];
                 const int y = src >= 0 ? token_ids[src] : -1;
                 s_y[tid] = (y >= c0 && y < V) ? y - c0 : -1;
+                s_dy[tid] = dzy[r];
             } else {
                 s_l[tid] = INFINITY;
                 s_g[tid] = 0.0f;
                 s_y[tid] = -1;
+                s_dy[tid] = 0.0f;
             }
         }
         __syncthreads();
@@ -535,7 +546,7 @@ struct DzEpi {
                 const int rb = t.wm * 128 + i * 16;  // tile row of the block
                 const int rs = rb + 4 * h + p;       // the row this lane stores
                 const int ys = s_y[rs];
-                const float gs = s_g[rs];
+                const float dys = s_dy[rs];
                 // the lane's 4 rows: read once (the staging writes below
                 // would otherwise force re-reads)
                 float lr[4], ngr[4];
@@ -564,7 +575,7 @@ struct DzEpi {
                     u32x4 out = u32x4{lo.x, lo.y, hi.x, hi.y};
                     const int v0 = vw + 32 * jp + 8 * q;
                     const int off = ys - v0;  // the row's token column (chunk-local, -1: none)
-                    if (static_cast<unsigned>(off) < 8u) out = add_to_element(out, off, gs);
+                    if (static_cast<unsigned>(off) < 8u) out = set_element(out, off, dys);
                     __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dz + (row0 + rs) * ld_dz + v0));
                 }
             }
@@ -648,7 +659,7 @@ Dims dims_of(int64_t N, int V, int H) {
 }
 
 struct Layout {
-    size_t ht, hc, wt, part, lse2, g, row_loss, dz, rows, seg, n_live, total;
+    size_t ht, hc, wt, part, lse2, g, dzy, row_loss, dz, rows, seg, n_live, total;
 };
 
 // The transposed weight Wt [H][V_pad] bf16, zero padded.
@@ -667,6 +678,7 @@ Layout layout_of(const Dims& d) {
     L.part = take(static_cast<size_t>(d.N_pad) * d.tiles_v * sizeof(float2));
     L.lse2 = take(static_cast<size_t>(d.N_pad) * 4);
     L.g = take(static_cast<size_t>(d.N_pad) * 4);
+    L.dzy = take(static_cast<size_t>(d.N_pad) * 4);
     L.row_loss = take(static_cast<size_t>(d.N_pad) * 4);
     L.dz = take(static_cast<size_t>(d.N_pad) * d.Vc * 2);
     L.rows = take(static_cast<size_t>(d.N_pad) * 4);
@@ -788,6 +800,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     float2* part = reinterpret_cast<float2*>(ws + L.part);
     float* lse2 = reinterpret_cast<float*>(ws + L.lse2);
     float* g = reinterpret_cast<float*>(ws + L.g);
+    float* dzy = reinterpret_cast<float*>(ws + L.dzy);
     float* row_loss = reinterpret_cast<float*>(ws + L.row_loss);
     uint16_t* dz = reinterpret_cast<uint16_t*>(ws + L.dz);
     int32_t* rows = reinterpret_cast<int32_t*>(ws + L.rows);
@@ -849,7 +862,8 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     // 3. per-token objective
     hipLaunchKernelGGL(lm_combine_kernel, dim3(static_cast<unsigned>(d.N_pad / 4)), dim3(256), 0,
                        stream, part, d.tiles_v, Hm, Wm, H, rows, d.N_pad, V, token_ids, old_logp,
-                       ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dev_err);
+                       ref_logp, adv_tok, w_tok, p, logp_out, tok_loss_out, row_loss, g, lse2, dzy,
+                       dev_err);
     if ((st = lc.status()) != LEAP_OK) return st;
     hipLaunchKernelGGL(obj::loss_reduce_kernel, dim3(1), dim3(obj::kReduceBlock), 0, stream,
                        row_loss, N, loss_out);
@@ -861,7 +875,7 @@ LEAP_API leap_status leap_grpo_lmhead_fwd_bwd(
     for (int c0 = 0; c0 < V; c0 += d.Vc) {
         const int vl = (d.V_pad - c0) < d.Vc ? (d.V_pad - c0) : d.Vc;  // multiple of 256
         {
-            const DzEpi epi{token_ids, rows, lse2, g, dz, d.Vc, d.N_pad, V, c0, c2};
+            const DzEpi epi{token_ids, rows, lse2, g, dzy, dz, d.Vc, d.N_pad, V, c0, c2};
             const uint64_t wb = static_cast<uint64_t>(V - c0) * H * 2;
             if ((st = gemm_nt(hc, H, hc_bytes, Wm + static_cast<int64_t>(c0) * H, H, wb, H, d.N_pad, vl,
                               epi, dyn_m_dz, stream, lc)) != LEAP_OK)

@@ -315,3 +315,30 @@ def check_grad(got, want, bound, what, slack=1e-6):
     assert not bad.any(), f"{what}: {int(bad.sum())} entries beyond the bound; first at " \
                           f"{np.argwhere(bad)[0].tolist()}"
     return fro
+
+
+def compare_lmhead(inp, gpu, kw, bad_expected=0, what=""):
+    """The fused LM-head call's outputs against oracle.lmhead on the same
+    inputs: log-probs within 2e-3, per-token loss within 2e-3 relative, the
+    loss within 1e-3 relative, dH and dW under check_grad's bound scaled by
+    |dZ| |W| and |dZ|^T |H|; excluded rows exactly zero."""
+    o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
+                      inp["w"], **kw)
+    V = inp["wt"].shape[0]
+    y, w = inp["y"], inp["w"]
+    valid = (w != 0) & (y >= 0) & (y < V)
+    assert gpu["bad"] == o["bad"] == bad_expected, (gpu["bad"], o["bad"])
+    err = np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0)
+    log(f"  {what} logp max err {err:.3e}")
+    assert err < 2e-3
+    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
+    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
+    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
+    Hf, Wf = bf16_f64(inp["h_u16"]), bf16_f64(inp["w_u16"])
+    aZ = np.abs(o["dZ"])
+    if gpu["dH"] is not None:
+        check_grad(gpu["dH"], o["dH"], aZ @ np.abs(Wf), f"{what} dH")
+        assert np.all(gpu["dH"][~valid] == 0.0)
+    if gpu["dW"] is not None:
+        check_grad(gpu["dW"], o["dW"], aZ.T @ np.abs(Hf), f"{what} dW")
+    return o

@@ -364,7 +364,7 @@ def test_lmhead_workspace_size():
     assert small > 0 and small % 256 == 0
     # the gathered live rows of H, row-major and transposed (2 H N_pad bf16
     # each), the transposed weight (H V_pad bf16), per-tile row statistics,
-    # three per-row vectors and the row list (4 N_pad each), one bf16 chunk of
+    # four per-row vectors and the row list (4 N_pad each), one bf16 chunk of
     # dZ, and the compaction's per-segment counts (4096-row segments); chunks
     # are 32768 columns unless a 32768-wide dZ chunk would reach 4 GiB
     def want(n, v, h):
@@ -372,7 +372,7 @@ def test_lmhead_workspace_size():
         v_pad = (v + 255) // 256 * 256
         vc = 32768 if n_pad * 32768 * 2 < (1 << 32) - 64 else 16384
         vc = min(vc, v_pad)
-        return (2 * 2 * h * n_pad + 2 * h * v_pad + 8 * n_pad * (v_pad // 256) + 4 * 4 * n_pad
+        return (2 * 2 * h * n_pad + 2 * h * v_pad + 8 * n_pad * (v_pad // 256) + 5 * 4 * n_pad
                 + 2 * n_pad * vc + 4 * -(-n_pad // 4096) + 4)
 
     for n, v, h in [(16384, 151936, 4096), (65280, 151936, 4096), (65281, 151936, 4096),

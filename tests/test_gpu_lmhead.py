@@ -25,27 +25,7 @@ def _kw(kl_type=0, inv_temp=1.0, kl_coef=0.01):
     return dict(eps_lo=0.2, eps_hi=0.2, kl_coef=kl_coef, kl_type=kl_type, inv_temp=inv_temp)
 
 
-def _compare(inp, gpu, kw, bad_expected=0, what=""):
-    o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
-                      inp["w"], **kw)
-    V = inp["wt"].shape[0]
-    y, w = inp["y"], inp["w"]
-    valid = (w != 0) & (y >= 0) & (y < V)
-    assert gpu["bad"] == o["bad"] == bad_expected, (gpu["bad"], o["bad"])
-    err = np.max(np.abs(gpu["logp"][valid] - o["logp"][valid]), initial=0)
-    U.log(f"  {what} logp max err {err:.3e}")
-    assert err < 2e-3
-    assert np.all(gpu["logp"][~valid] == 0) and np.all(gpu["tok_loss"][~valid] == 0)
-    np.testing.assert_allclose(gpu["tok_loss"][valid], o["tok_loss"][valid], rtol=2e-3, atol=2e-4)
-    assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
-    Hf, Wf = U.bf16_f64(inp["h_u16"]), U.bf16_f64(inp["w_u16"])
-    aZ = np.abs(o["dZ"])
-    if gpu["dH"] is not None:
-        U.check_grad(gpu["dH"], o["dH"], aZ @ np.abs(Wf), f"{what} dH")
-        assert np.all(gpu["dH"][~valid] == 0.0)
-    if gpu["dW"] is not None:
-        U.check_grad(gpu["dW"], o["dW"], aZ.T @ np.abs(Hf), f"{what} dW")
-    return o
+_compare = U.compare_lmhead
 
 
 def test_lmhead_reduced_shape_full_parity():

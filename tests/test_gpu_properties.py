@@ -304,3 +304,40 @@ def test_logprob_fwd_matches_oracle(V, pad, N, seed, inv_temp, p_ninf, masked):
     assert np.all(got[~live] == 0) and np.all(ent[~live] == 0)
     assert np.max(np.abs(got[live] - want[live]), initial=0) < 2e-3
     np.testing.assert_allclose(ent[live], h[live], rtol=1e-4, atol=2e-4)
+
+
+@st.composite
+def lmhead_cases(draw):
+    """Small fused LM-head problems the fp64 oracle scores in well under a
+    second: hidden width a multiple of the 64-deep k-tile, ragged rows and
+    vocabularies (one to two 32768-column chunks), every KL estimator,
+    temperatures, symmetric and clip-higher bounds, any share of excluded
+    rows, and either gradient left out."""
+    H = draw(st.sampled_from([64, 128, 192, 320]))
+    V = draw(st.one_of(st.integers(1, 700), st.integers(701, 40000)))
+    N = draw(st.integers(1, max(1, min(600, int(6e7 // (V * H))))))
+    return dict(N=N, V=V, H=H, seed=draw(st.integers(0, 2**16)),
+                inv_temp=draw(st.sampled_from([1.0, 0.7, 1.3])),
+                kl_type=draw(st.sampled_from([0, 1, 2])),
+                eps=draw(st.sampled_from([(0.2, 0.2), (0.2, 0.28)])),
+                mask_frac=draw(st.sampled_from([0.0, 0.05, 0.5, 1.0])),
+                want=draw(st.sampled_from([(True, True), (True, False), (False, True)])))
+
+
+@settings(max_examples=20, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(lmhead_cases())
+def test_lmhead_matches_oracle(c):
+    """The fused LM-head call against oracle.lmhead on random shapes and
+    options, to the LM-head parity bars (log-prob 2e-3, loss 1e-3 relative,
+    gradients under the |dZ|-scaled bound, excluded rows zero)."""
+    N, V, H = c["N"], c["V"], c["H"]
+    U.log(f"lmhead property case N={N} V={V} H={H} seed={c['seed']} T^-1={c['inv_temp']} "
+          f"kl={c['kl_type']} eps={c['eps']} masked={c['mask_frac']} grads={c['want']}")
+    inp = U.lmhead_inputs(c["seed"], N, V, H, mask_frac=c["mask_frac"], inv_temp=c["inv_temp"])
+    kw = dict(eps_lo=c["eps"][0], eps_hi=c["eps"][1], kl_coef=0.05, kl_type=c["kl_type"],
+              inv_temp=c["inv_temp"])
+    gpu = U.run_lmhead(inp, want_dH=c["want"][0], want_dW=c["want"][1], **kw)
+    assert (gpu["dH"] is None) != c["want"][0] and (gpu["dW"] is None) != c["want"][1]
+    U.compare_lmhead(inp, gpu, kw, what=f"N={N} V={V} H={H}")
