@@ -341,3 +341,47 @@ def test_lmhead_matches_oracle(c):
     gpu = U.run_lmhead(inp, want_dH=c["want"][0], want_dW=c["want"][1], **kw)
     assert (gpu["dH"] is None) != c["want"][0] and (gpu["dW"] is None) != c["want"][1]
     U.compare_lmhead(inp, gpu, kw, what=f"N={N} V={V} H={H}")
+
+
+@st.composite
+def stats_cases(draw):
+    """Rollout statistics inputs: group sizes 1-1024, 1-6 turns, any gate,
+    passes on any turn, advantages with ties and zeros (or none), bucket
+    counts 1-256, and a few malformed rollouts."""
+    G = draw(st.one_of(st.integers(1, 16), st.integers(17, 1024)))
+    n_groups = draw(st.integers(1, max(1, min(64, 20000 // G))))
+    return dict(G=G, n_groups=n_groups, M=draw(st.integers(1, 6)),
+                nb=draw(st.one_of(st.integers(1, 16), st.integers(17, 256))),
+                seed=draw(st.integers(0, 2**31 - 1)), with_adv=draw(st.booleans()),
+                p_bad=draw(st.sampled_from([0.0, 0.0, 0.01])))
+
+
+@settings(max_examples=40, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
+                                 HealthCheck.function_scoped_fixture])
+@given(stats_cases())
+def test_rollout_stats_match_oracle(c):
+    """Every counter of leap_rollout_stats bit-exact against the oracle on
+    random groups, turn counts, gates, advantages and bucket counts."""
+    from tests import test_gpu_rollout_stats as S
+    G, M, n, nb = c["G"], c["M"], c["n_groups"], c["nb"]
+    rng = np.random.default_rng(c["seed"])
+    gate = rng.integers(0, 2, n).astype(np.uint8)
+    p_pass = rng.random(n).repeat(G)
+    pt = np.where(rng.random(n * G) < p_pass, rng.integers(1, M + 1, n * G), 0).astype(np.int32)
+    single = np.repeat(gate == 0, G)
+    pt[single & (pt > 1)] = 0  # groups without expansion stop after the first turn
+    nt = np.where(pt >= 1, pt, np.where(single, 1, M)).astype(np.int32)
+    bad = rng.random(n * G) < c["p_bad"]
+    pt[bad & (rng.random(n * G) < 0.5)] = M + 1
+    nt[bad & (pt <= M)] = 0
+    adv = None
+    if c["with_adv"]:
+        adv = np.round(rng.normal(0, 1, n * G), 1)
+        adv[rng.random(n * G) < 0.2] = 0.0
+    U.log(f"rollout stats property case {n} x {G}, M={M}, buckets={nb}, "
+          f"adv={c['with_adv']}, bad={int(bad.sum())}")
+    got, gbad = S._gpu(pt, nt, gate, adv, G, M, nb)
+    want, wbad = S._expect(pt, nt, gate, adv, G, M, nb)
+    np.testing.assert_array_equal(got, want)
+    assert gbad == wbad
