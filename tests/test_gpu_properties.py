@@ -324,7 +324,7 @@ def lmhead_cases(draw):
                 want=draw(st.sampled_from([(True, True), (True, False), (False, True)])))
 
 
-@settings(max_examples=20, deadline=None, derandomize=True,
+@settings(max_examples=40, deadline=None, derandomize=True,
           suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large,
                                  HealthCheck.function_scoped_fixture])
 @given(lmhead_cases())
