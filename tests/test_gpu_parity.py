@@ -202,7 +202,9 @@ def test_grpo_tiny_full_parity(mode):
                         rel_to_max=(mode == "seq_mean"))
 
 
-@pytest.mark.parametrize("V", [32768, 151936])
+# every row-kernel family: one-wave and 256-lane resident rows, the
+# persistent row queue, rows partly in LDS, the streaming kernel
+@pytest.mark.parametrize("V", [2, 7, 300, 5000, 32768, 151936, 200003, 300000])
 def test_grpo_wide_range_and_peaked_rows(V):
     """Entry-wise relative check of dlogits on rows whose probabilities span
     many orders of magnitude: logits of std 6 and 12, and rows with one
@@ -229,7 +231,7 @@ def test_grpo_wide_range_and_peaked_rows(V):
         for k in list(range(16)) + list(range(48, N)):  # tokens of the rescaled rows
             tok[k] = rng.integers(0, V)
 
-    lg, tok, old, ref = U.make_inputs_host(V + 6, N, V, edit=edit)
+    lg, tok, old, ref = U.make_inputs_host(V + 6, N, V, ld=(V + 7) // 8 * 8, edit=edit)
     adv = rng.normal(0, 1, N).astype(np.float32)
     w = np.ones(N, np.float32)
     kw = dict(KW, kl_coef=0.05)
@@ -250,8 +252,9 @@ def test_grpo_wide_range_and_peaked_rows(V):
     U.log(f"  max |err| / bound {ratio.max():.3f} at row {k}, column {v}")
     assert ratio.max() <= 1.0
     # the check is not vacuous: entries below fp16's normal range are present
-    p = np.abs(want) / np.maximum(g_max[:, None], 1e-300)
-    assert np.sum((p > 2.0 ** -24) & (p < 2.0 ** -14)) > 1000
+    if V >= 32768:
+        p = np.abs(want) / np.maximum(g_max[:, None], 1e-300)
+        assert np.sum((p > 2.0 ** -24) & (p < 2.0 ** -14)) > 1000
 
 
 SHAPES = [(16, 16, 64), (100, 104, 64), (1000, 1008, 64), (4093, 4096, 32), (8192, 8192, 32),
