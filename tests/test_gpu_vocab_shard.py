@@ -262,3 +262,48 @@ def test_stats_every_shape(width):
     assert bad == 0
     got_h = np.log(2.0) * (np.log2(q[live, 1].astype(np.float64)) - qt[live] / q[live, 1])
     np.testing.assert_allclose(got_h, h, rtol=1e-4, atol=2e-4)
+
+
+@pytest.mark.parametrize("widths", [[1, 1], [3, 4, 300], [18992] * 8])
+def test_shards_wide_range_and_peaked_rows(widths):
+    """Entry-wise relative check of the sharded dlogits on rows whose
+    probabilities span many orders of magnitude (logit std 6 and 12) and on
+    rows with one logit 30 above the rest (the token on the spike, so that
+    p_y is within e^-30 of 1, or away from it).  The shard backward forms
+    every entry in fp32 from the merged log-sum-exp and rounds it once to
+    bf16 (2^-9), the token's own column as -g p_y + g in fp32: each entry is
+    within 2^-8 |d| + 2^-24 |g| of the oracle, the token's column within
+    2^-8 |d| + 2^-12 |g| (the fp32 log-sum-exp's error times g)."""
+    V = sum(widths)
+    N = 64
+    seed = 3301 + V
+    rng = np.random.default_rng(seed)
+    lg = wl.logits_host(seed, N, V)
+    x = wl.bf16_bits_to_f32(lg[:, :V]).astype(np.float32)
+    x[:16] *= 3.0
+    x[48:] *= 6.0
+    tok = rng.integers(0, V, N).astype(np.int32)
+    spike = rng.integers(0, V, N)
+    for k in range(16, 48):
+        x[k, spike[k]] += 30.0
+        tok[k] = spike[k] if (k < 32 or V == 1) else (spike[k] + 1 + rng.integers(0, V - 1)) % V
+    lg[:, :V] = wl.f32_to_bf16_bits(x)
+    cur, _ = oracle.logprob_rows(lg, tok, V=V)
+    n_old, n_ref = wl.logp_noise(seed, N)
+    old, ref = (cur + n_old).astype(np.float32), (cur + n_ref).astype(np.float32)
+    adv = rng.normal(0, 1, N).astype(np.float32)
+    w = np.ones(N, np.float32)
+    kw = dict(KW, kl_coef=0.05)
+    U.log(f"vocab shards wide-range / peaked rows {widths[:3]} V={V}")
+    gpu = _run(lg, V, tok, old, ref, adv, w, _shards(V, widths), kw)
+    o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, **kw)
+    assert gpu["bad"] == o["bad"] == 0
+    got, want = U.bf16_f64(gpu["dl"]), o["dlogits"]
+    rho = np.exp(o["logp"] - old.astype(np.float64))
+    g_max = w * (np.abs(adv) * rho + kw["kl_coef"] * np.abs(1.0 - np.exp(ref - o["logp"])))
+    tol = 2.0 ** -8 * np.abs(want) + 2.0 ** -24 * g_max[:, None]
+    tol[np.arange(N), tok] = 2.0 ** -8 * np.abs(want[np.arange(N), tok]) + 2.0 ** -12 * g_max
+    ratio = np.abs(got - want) / tol
+    k, v = np.unravel_index(np.argmax(ratio), ratio.shape)
+    U.log(f"  max |err| / bound {ratio.max():.3f} at row {k}, column {v}")
+    assert ratio.max() <= 1.0
