@@ -211,13 +211,17 @@ def torch_token_logp(hidden, weight, y, row_chunk=256) -> np.ndarray:
     return out.double().cpu().numpy()
 
 
-def lmhead_inputs(seed, N, V, H, mask_frac=0.05, bad_rows=(), cur="oracle", inv_temp=1.0):
+def lmhead_inputs(seed, N, V, H, mask_frac=0.05, bad_rows=(), cur="oracle", inv_temp=1.0,
+                  h_scale=1.0):
     """Seeded LM-head inputs: bf16 hidden / weight on the device (with host
     bit patterns), Gumbel-max tokens, old/ref = current log-prob + noise,
     advantages ~ N(0, 1), weights 1/N with a fraction of excluded rows, and
-    optional rows with an out-of-range token id."""
+    optional rows with an out-of-range token id.  h_scale multiplies the
+    hidden states (and so the logits) before the tokens are drawn."""
     import torch
     hid, wt = wl.lmhead_operands_device(seed, N, V, H, dev())
+    if h_scale != 1.0:
+        hid = (hid.float() * h_scale).to(torch.bfloat16)
     y_t = wl.lmhead_tokens_device(hid, wt, seed)
     y = y_t.cpu().numpy().astype(np.int32)
     h_u16, w_u16 = bf16_tensor_bits(hid), bf16_tensor_bits(wt)
