@@ -342,11 +342,14 @@ def test_grpo_special_values_and_errors():
     U.check_dlogits(got, lg, rows, tok, old, ref, adv, w, V, atol=2e-2, kw=KW)
 
 
-@pytest.mark.parametrize("V,N", [(151936, 300), (230000, 64)])
+@pytest.mark.parametrize("V,N", [(151936, 300), (100003, 2600), (230000, 64)])
 def test_grpo_inplace_and_deterministic(V, N):
     # 151936: the persistent kernel with more rows than one per workgroup for
-    # some workgroups only; 230000: rows held partly in LDS
-    lg, tok, old, ref = U.make_inputs_host(9, N, V)
+    # some workgroups only; 100003 x 2600: every workgroup taking rows from
+    # the queue, in place (each row's loads are issued only after the
+    # previous row's stores, never for a row already written), with a
+    # partial last chunk; 230000: rows held partly in LDS
+    lg, tok, old, ref = U.make_inputs_host(9, N, V, ld=(V + 7) // 8 * 8)
     rng = np.random.default_rng(9)
     adv = rng.normal(0, 1, N).astype(np.float32)
     w = rng.choice([0.0, 1.0], N, p=[0.2, 0.8]).astype(np.float32)
@@ -356,14 +359,17 @@ def test_grpo_inplace_and_deterministic(V, N):
     c = U.run_grpo(U.bf16_device(lg), V, tok, old, ref, adv, w, inplace=True, want_entropy=True,
                    **KW)
     import torch
-    assert torch.equal(a["dl_dev"].view(torch.int16), b["dl_dev"].view(torch.int16))
-    assert torch.equal(a["dl_dev"].view(torch.int16), c["dl_dev"].view(torch.int16))
+    # columns V .. ld - 1 are not the call's (NaN-filled out of place, the
+    # logits' padding in place)
+    da, db, dc = (x["dl_dev"].view(torch.int16)[:, :V] for x in (a, b, c))
+    assert torch.equal(da, db)
+    assert torch.equal(da, dc)
     assert a["loss"] == b["loss"] == c["loss"]
     assert np.array_equal(a["logp"], c["logp"])
     assert np.array_equal(a["entropy"], c["entropy"])  # in place: the row is read before written
     o = oracle.grpo_rows(lg, tok, old, ref, adv, w, V=V, want_dlogits=False, **KW)
     _check_rows(a, o, w != 0, f"V={V}")
-    rows = np.arange(N)
+    rows = np.arange(N) if N <= 512 else np.sort(rng.choice(N, 48, replace=False))
     U.check_dlogits(U.dl_rows(a["dl_dev"], rows, V), lg, rows, tok, old, ref, adv, w, V, atol=2e-2,
                     kw=KW)
 
