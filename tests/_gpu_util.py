@@ -325,7 +325,10 @@ def compare_lmhead(inp, gpu, kw, bad_expected=0, what=""):
     """The fused LM-head call's outputs against oracle.lmhead on the same
     inputs: log-probs within 2e-3, per-token loss within 2e-3 relative, the
     loss within 1e-3 relative, dH and dW under check_grad's bound scaled by
-    |dZ| |W| and |dZ|^T |H|; excluded rows exactly zero."""
+    |dZ| |W| and |dZ|^T |H|, where each row's token entry of |dZ| also
+    carries 2^-12 |g| (g (1 - p_y) is formed from the fp32 log-prob, whose
+    error dominates when p_y is within ~1e-4 of 1); excluded rows exactly
+    zero."""
     o = oracle.lmhead(inp["h_u16"], inp["w_u16"], inp["y"], inp["old"], inp["ref"], inp["adv"],
                       inp["w"], **kw)
     V = inp["wt"].shape[0]
@@ -340,6 +343,15 @@ def compare_lmhead(inp, gpu, kw, bad_expected=0, what=""):
     assert abs(gpu["loss"] - o["loss"]) <= 1e-3 * abs(o["loss"]) + 1e-7, (gpu["loss"], o["loss"])
     Hf, Wf = bf16_f64(inp["h_u16"]), bf16_f64(inp["w_u16"])
     aZ = np.abs(o["dZ"])
+    # |g| <= w T^-1 (|A| rho + beta |d KL / d logp|)
+    lp = np.where(valid, o["logp"], 0.0)
+    rho = np.exp(lp - inp["old"].astype(np.float64))
+    ref = inp["ref"].astype(np.float64)
+    dkl = {oracle.KL_K3: np.abs(1.0 - np.exp(ref - lp)), oracle.KL_K1: np.ones_like(lp),
+           oracle.KL_K2: np.abs(lp - ref)}[kw["kl_type"]]
+    g_max = np.abs(w) * kw["inv_temp"] * (np.abs(inp["adv"]) * rho + kw["kl_coef"] * dkl)
+    r = np.flatnonzero(valid)
+    aZ[r, y[r]] += 2.0 ** -12 / (2.0 ** -8 + 1e-4) * g_max[r]
     if gpu["dH"] is not None:
         check_grad(gpu["dH"], o["dH"], aZ @ np.abs(Wf), f"{what} dH")
         assert np.all(gpu["dH"][~valid] == 0.0)

@@ -312,7 +312,8 @@ def lmhead_cases(draw):
     second: hidden width a multiple of the 64-deep k-tile, ragged rows and
     vocabularies (one to two 32768-column chunks), every KL estimator,
     temperatures, symmetric and clip-higher bounds, any share of excluded
-    rows, and either gradient left out."""
+    rows, either gradient left out, and the weight transposed beforehand or
+    by the call."""
     H = draw(st.sampled_from([64, 128, 192, 320]))
     V = draw(st.one_of(st.integers(1, 700), st.integers(701, 40000)))
     N = draw(st.integers(1, max(1, min(600, int(6e7 // (V * H))))))
@@ -321,7 +322,8 @@ def lmhead_cases(draw):
                 kl_type=draw(st.sampled_from([0, 1, 2])),
                 eps=draw(st.sampled_from([(0.2, 0.2), (0.2, 0.28)])),
                 mask_frac=draw(st.sampled_from([0.0, 0.05, 0.5, 1.0])),
-                want=draw(st.sampled_from([(True, True), (True, False), (False, True)])))
+                want=draw(st.sampled_from([(True, True), (True, False), (False, True)])),
+                prepared=draw(st.booleans()))
 
 
 @settings(max_examples=40, deadline=None, derandomize=True,
@@ -334,11 +336,13 @@ def test_lmhead_matches_oracle(c):
     gradients under the |dZ|-scaled bound, excluded rows zero)."""
     N, V, H = c["N"], c["V"], c["H"]
     U.log(f"lmhead property case N={N} V={V} H={H} seed={c['seed']} T^-1={c['inv_temp']} "
-          f"kl={c['kl_type']} eps={c['eps']} masked={c['mask_frac']} grads={c['want']}")
+          f"kl={c['kl_type']} eps={c['eps']} masked={c['mask_frac']} grads={c['want']} "
+          f"prepared={c['prepared']}")
     inp = U.lmhead_inputs(c["seed"], N, V, H, mask_frac=c["mask_frac"], inv_temp=c["inv_temp"])
     kw = dict(eps_lo=c["eps"][0], eps_hi=c["eps"][1], kl_coef=0.05, kl_type=c["kl_type"],
               inv_temp=c["inv_temp"])
-    gpu = U.run_lmhead(inp, want_dH=c["want"][0], want_dW=c["want"][1], **kw)
+    gpu = U.run_lmhead(inp, want_dH=c["want"][0], want_dW=c["want"][1], prepared=c["prepared"],
+                       **kw)
     assert (gpu["dH"] is None) != c["want"][0] and (gpu["dW"] is None) != c["want"][1]
     U.compare_lmhead(inp, gpu, kw, what=f"N={N} V={V} H={H}")
 
